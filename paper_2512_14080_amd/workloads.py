@@ -1,0 +1,118 @@
+"""Seeded synthetic MoE-layer workloads.
+
+This module holds the layer shapes that are exercised and the seeded input
+generator that both the HIP path's tests/benchmark and the CPU oracle consume.
+It contains none of the method's arithmetic: only random draws, the fp32 -> bf16
+round-to-nearest-even conversion used to materialise bf16 inputs, and the
+per-expert router bias that skews expert popularity.
+
+Shapes follow the paper's problem statement (Appendix A, notation table):
+X[T,d], router W_r[d,E], expert up-projection W1[E,d,2n] (gate columns first,
+then up columns), down-projection W2[E,n,d], top-K routing.
+"""
+from __future__ import annotations
+
+import dataclasses
+import numpy as np
+
+
+@dataclasses.dataclass(frozen=True)
+class MoEConfig:
+    name: str
+    T: int
+    d: int
+    n: int
+    E: int
+    K: int
+    m_tile: int
+    # std of X, W1, W2 draws
+    w_std: float = 0.02
+    # "std1": router weights scaled so logits are ~N(0,1); "w_std": same std as weights
+    router: str = "std1"
+    # Zipf exponent of the per-expert bias (0 = no bias)
+    zipf_s: float = 0.0
+
+    @property
+    def P(self) -> int:
+        return self.T * self.K
+
+    def model_flops(self, rows: int | None = None) -> float:
+        """Model FLOPs of fwd+bwd: 18 * d * n * (sum of expert row counts)."""
+        r = self.T * self.K if rows is None else rows
+        return 18.0 * self.d * self.n * r
+
+
+CONFIGS = {
+    # Tiny correctness layer: everything ~N(0, 0.02), softmax top-2 router.
+    "tiny": MoEConfig("tiny", T=512, d=128, n=64, E=8, K=2, m_tile=16, router="w_std"),
+    # Fine-grained 1B-shaped layer, roughly balanced std-1 router logits.
+    "1b": MoEConfig("1b", T=16384, d=1024, n=256, E=64, K=8, m_tile=128),
+    # Fine-grained 7B-shaped layer (the headline workload).
+    "7b": MoEConfig("7b", T=32768, d=1536, n=256, E=128, K=8, m_tile=128),
+    # High-sparsity layer with a Zipf(1.1) per-expert bias on the logits.
+    "sparse": MoEConfig("sparse", T=32768, d=2048, n=128, E=256, K=8, m_tile=128, zipf_s=1.1),
+    # Coarse-grained layer (large GEMMs).
+    "coarse": MoEConfig("coarse", T=16384, d=4096, n=14336, E=8, K=2, m_tile=128),
+}
+
+
+def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
+    """Round fp32 values to bf16 (round-to-nearest-even) and return raw uint16 bits."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    b = x.view(np.uint32).astype(np.uint64)
+    r = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return r.astype(np.uint16)
+
+
+def f32_from_bf16_bits(u: np.ndarray) -> np.ndarray:
+    """Exact upcast of raw bf16 bits to fp32."""
+    return (np.ascontiguousarray(u, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+@dataclasses.dataclass
+class MoEInputs:
+    cfg: MoEConfig
+    seed: int
+    # raw bf16 bits (uint16) -- what the device consumes
+    X: np.ndarray
+    Wr: np.ndarray
+    W1: np.ndarray
+    W2: np.ndarray
+    dO: np.ndarray
+    # fp32 per-expert logit bias, or None
+    bias: np.ndarray | None
+
+    def f32(self, name: str) -> np.ndarray:
+        return f32_from_bf16_bits(getattr(self, name))
+
+
+def make_inputs(cfg: MoEConfig, seed: int = 0, T: int | None = None) -> MoEInputs:
+    """Draw the layer's inputs from a fixed seed.
+
+    Streams are spawned from one SeedSequence in the fixed order
+    [X, W_r, W1, W2, dO, bias-permutation].  Draws are fp32, then rounded to
+    bf16.  ``T`` overrides the token count (the first T rows of the X/dO
+    streams are the same as for the full config, so a sample is a prefix).
+    """
+    T = cfg.T if T is None else T
+    ss = np.random.SeedSequence(seed)
+    gx, gr, g1, g2, gd, gb = [np.random.Generator(np.random.Philox(s)) for s in ss.spawn(6)]
+    d, n, E = cfg.d, cfg.n, cfg.E
+    X = gx.standard_normal((T, d), dtype=np.float32) * np.float32(cfg.w_std)
+    r_std = cfg.w_std if cfg.router == "w_std" else 1.0 / (cfg.w_std * np.sqrt(d))
+    Wr = gr.standard_normal((d, E), dtype=np.float32) * np.float32(r_std)
+    W1 = g1.standard_normal((E, d, 2 * n), dtype=np.float32) * np.float32(cfg.w_std)
+    W2 = g2.standard_normal((E, n, d), dtype=np.float32) * np.float32(cfg.w_std)
+    dO = gd.standard_normal((T, d), dtype=np.float32)
+    bias = None
+    if cfg.zipf_s > 0:
+        rank = gb.permutation(E) + 1  # expert e gets popularity rank rank[e]
+        bias = (-cfg.zipf_s * np.log(rank.astype(np.float64))).astype(np.float32)
+    return MoEInputs(cfg, seed, bf16_bits_from_f32(X), bf16_bits_from_f32(Wr),
+                     bf16_bits_from_f32(W1), bf16_bits_from_f32(W2),
+                     bf16_bits_from_f32(dO), bias)
+
+
+def scaled(cfg: MoEConfig, **kw) -> MoEConfig:
+    """A copy of ``cfg`` with some fields replaced (for reduced parity shapes)."""
+    return dataclasses.replace(cfg, **kw)
