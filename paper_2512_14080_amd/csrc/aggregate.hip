@@ -1,0 +1,177 @@
+// Expert aggregation (gather-and-sum) and the small helper kernels.
+//
+// Forward O kernel (Section 3, forward algorithm): every token gathers its
+// experts' Y rows and sums them weighted by the routing scores.  Backward dX
+// kernel (Appendix E, up-projection backward): the same gather-and-sum over
+// dX~ rows, with the router's gradient term fused in.  Each token is owned by
+// one wave, so the sum order is fixed and no atomics are used (the paper's
+// gather-and-sum choice keeps the result deterministic).
+#include "device_common.h"
+#include "launch.h"
+
+namespace smoe {
+
+// One wave per token; lanes cover 8 consecutive bf16 (16 bytes) of the row.
+__global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__ Y, const int32_t* __restrict__ tok_offsets,
+                                                    const int32_t* __restrict__ tok_rows, const float* __restrict__ row_w,
+                                                    uint16_t* __restrict__ O, int T, int d) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int lane = lane_id();
+  const int j0 = tok_offsets[t], j1 = tok_offsets[t + 1];
+  for (int c = lane * 8; c < d; c += 512) {
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = j0; j < j1; ++j) {
+      const int r = tok_rows[j];
+      const float w = row_w[r];
+      const u32x4 v = *(const u32x4*)(Y + (size_t)r * d + c);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += w * bf_lo(v[q]);
+        acc[2 * q + 1] += w * bf_hi(v[q]);
+      }
+    }
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[2 * q], acc[2 * q + 1]);
+    *(u32x4*)(O + (size_t)t * d + c) = o;
+  }
+}
+
+// dX_t = sum over the token's rows of dX~ + sum_j dl_j W_r[:, e_j], with the
+// router gradient on the token's selected set dl_j = s_j (dS_j - sum_k s_k dS_k).
+// Also writes the dense router-logit gradient row dL[t, :] (bf16) for dW_r.
+__global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict__ dXt, const float* __restrict__ dS,
+                                                     const float* __restrict__ WrT, const int32_t* __restrict__ tok_offsets,
+                                                     const int32_t* __restrict__ tok_rows,
+                                                     const int32_t* __restrict__ row_expert,
+                                                     const float* __restrict__ row_w, uint16_t* __restrict__ dX,
+                                                     uint16_t* __restrict__ dL, int T, int d, int E) {
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int lane = lane_id();
+  const int j0 = tok_offsets[t], j1 = tok_offsets[t + 1];
+  float g = 0.f;
+  if (WrT)
+    for (int j = j0; j < j1; ++j) {
+      const int r = tok_rows[j];
+      g += row_w[r] * dS[r];
+    }
+  for (int c = lane * 8; c < d; c += 512) {
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int j = j0; j < j1; ++j) {
+      const int r = tok_rows[j];
+      const u32x4 v = *(const u32x4*)(dXt + (size_t)r * d + c);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += bf_lo(v[q]);
+        acc[2 * q + 1] += bf_hi(v[q]);
+      }
+    }
+    if (WrT) {
+      for (int j = j0; j < j1; ++j) {
+        const int r = tok_rows[j];
+        const float w = row_w[r];
+        const float dl = w * (dS[r] - g);
+        const float* wr = WrT + (size_t)row_expert[r] * d + c;
+        const f32x4 a = *(const f32x4*)wr;
+        const f32x4 b = *(const f32x4*)(wr + 4);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[q] += dl * a[q];
+          acc[4 + q] += dl * b[q];
+        }
+      }
+    }
+    u32x4 o;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[2 * q], acc[2 * q + 1]);
+    *(u32x4*)(dX + (size_t)t * d + c) = o;
+  }
+  if (dL) {
+    for (int e = lane; e < E; e += 64) {
+      float v = 0.f;
+      for (int j = j0; j < j1; ++j) {
+        const int r = tok_rows[j];
+        if (row_expert[r] == e) v = row_w[r] * (dS[r] - g);
+      }
+      dL[(size_t)t * E + e] = f2bf(v);
+    }
+  }
+}
+
+// out[i] = sum_s part[s * n + i] (fixed order)
+__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, float* __restrict__ out, int n,
+                                                            int parts) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int k = 0; k < parts; ++k) s += part[(size_t)k * n + i];
+  out[i] = s;
+}
+
+// out[i] = sum_k part[i * parts + k] (fixed order)
+__global__ __launch_bounds__(256) void reduce_rowparts_kernel(const float* __restrict__ part, float* __restrict__ out,
+                                                              int n, int parts) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int k = 0; k < parts; ++k) s += part[(size_t)i * parts + k];
+  out[i] = s;
+}
+
+// WrT[e][i] = W_r[i][e] as fp32
+__global__ __launch_bounds__(256) void transpose_wr_kernel(const uint16_t* __restrict__ Wr, float* __restrict__ WrT, int d,
+                                                           int E) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= d * E) return;
+  const int e = idx / d, i = idx % d;
+  WrT[idx] = bf2f(Wr[(size_t)i * E + e]);
+}
+
+// dbias[e] = sum_t dL[t][e], one block per expert, fixed reduction tree
+__global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* __restrict__ dL, float* __restrict__ out, int T,
+                                                     int E) {
+  __shared__ float red[4];
+  const int e = blockIdx.x;
+  float s = 0.f;
+  for (int t = threadIdx.x; t < T; t += 256) s += bf2f(dL[(size_t)t * E + e]);
+  s = wave_sum(s);
+  if (lane_id() == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) out[e] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s) {
+  agg_o_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>(Y, r.tok_offsets, r.tok_rows, r.row_w, O, T, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const float* WrT, const moe_routing& r, uint16_t* dX,
+                         uint16_t* dL, int T, int d, int E, hipStream_t s) {
+  agg_dx_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>(dXt, dS, WrT, r.tok_offsets, r.tok_rows, r.row_expert, r.row_w,
+                                                        dX, dL, T, d, E);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_rows(const float* part, float* out, int rows, int parts, hipStream_t s) {
+  reduce_splits_kernel<<<dim3((rows + 255) / 256), dim3(256), 0, s>>>(part, out, rows, parts);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s) {
+  reduce_rowparts_kernel<<<dim3((rows + 255) / 256), dim3(256), 0, s>>>(part, out, rows, parts);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_wr(const uint16_t* Wr, float* WrT, int d, int E, hipStream_t s) {
+  transpose_wr_kernel<<<dim3((d * E + 255) / 256), dim3(256), 0, s>>>(Wr, WrT, d, E);
+  return hipGetLastError();
+}
+
+hipError_t launch_colsum_bf16(const uint16_t* dL, float* dbias, int T, int E, hipStream_t s) {
+  colsum_kernel<<<dim3(E), dim3(256), 0, s>>>(dL, dbias, T, E);
+  return hipGetLastError();
+}
+
+}  // namespace smoe

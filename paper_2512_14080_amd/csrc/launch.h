@@ -1,0 +1,79 @@
+// Internal launchers of the HIP kernels (host side, C++).  The C ABI in
+// moe_abi.cpp validates arguments, carves workspaces and calls these.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/sonicmoe.h"
+
+namespace smoe {
+
+// routing
+hipError_t launch_softmax_topk(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
+                               int T, int E, int K, int do_softmax, hipStream_t s);
+hipError_t launch_build_mask(const int32_t* topk_idx, uint64_t* mask, int T, int E, int K, int W, hipStream_t s);
+hipError_t launch_metadata(const moe_routing& r, const float* scores, int T, int E, hipStream_t s);
+hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
+                        hipStream_t s);
+
+// GEMMs (all bf16 in, fp32 accumulation)
+struct RouterGemmArgs {
+  const uint16_t* X; const uint16_t* Wr; const float* bias; float* logits; int T, d, E;
+};
+hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s);
+
+struct UpArgs {
+  const uint16_t* X; const uint16_t* W1; const int32_t* offsets; const int32_t* row_token;
+  uint16_t* H; uint16_t* A; int d, n, E, capacity;
+};
+hipError_t launch_up(const UpArgs& a, hipStream_t s);
+
+struct DownArgs {
+  const uint16_t* A; const uint16_t* W2; const int32_t* offsets; uint16_t* Y; int d, n, E, capacity;
+};
+hipError_t launch_down(const DownArgs& a, hipStream_t s);
+
+struct DHArgs {
+  const uint16_t* dO; const uint16_t* W2; const uint16_t* H; const int32_t* offsets; const int32_t* row_token;
+  const float* row_w; uint16_t* dH; uint16_t* Ap; float* dS; float* dS_part; int d, n, E, capacity;
+};
+int dh_n_tiles(int n);
+hipError_t launch_dh(const DHArgs& a, hipStream_t s);
+
+struct DXtArgs {
+  const uint16_t* dH; const uint16_t* W1; const int32_t* offsets; uint16_t* dXt; int d, n, E, capacity;
+};
+hipError_t launch_dxt(const DXtArgs& a, hipStream_t s);
+
+struct DW2Args {
+  const uint16_t* Ap; const uint16_t* dO; const int32_t* offsets; const int32_t* row_token; uint16_t* dW2;
+  int d, n, E;
+};
+hipError_t launch_dw2(const DW2Args& a, hipStream_t s);
+
+struct DW1Args {
+  const uint16_t* X; const uint16_t* dH; const int32_t* offsets; const int32_t* row_token; uint16_t* dW1;
+  int d, n, E;
+};
+hipError_t launch_dw1(const DW1Args& a, hipStream_t s);
+
+struct DWrArgs {
+  const uint16_t* X; const uint16_t* dL; float* part; float* dWr; int T, d, E, splits;
+};
+int dwr_splits(int T, int d, int E);
+hipError_t launch_dwr(const DWrArgs& a, hipStream_t s);
+
+// aggregation and small kernels
+hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s);
+hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const float* WrT, const moe_routing& r, uint16_t* dX,
+                         uint16_t* dL, int T, int d, int E, hipStream_t s);
+hipError_t launch_reduce_rows(const float* part, float* out, int rows, int parts, hipStream_t s);
+hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s);
+hipError_t launch_transpose_wr(const uint16_t* Wr, float* WrT, int d, int E, hipStream_t s);
+hipError_t launch_colsum_bf16(const uint16_t* dL, float* dbias, int T, int E, hipStream_t s);
+
+// timing hooks (moe_abi.cpp)
+void prof_begin(int kernel_class, hipStream_t s);
+void prof_end(int kernel_class, hipStream_t s);
+
+}  // namespace smoe

@@ -1,0 +1,198 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Routing contract: the oracle computes the fp32 scores S_full from the seeded
+inputs and the device consumes them (MOE_ROUTE_SCORES_IN), so every integer
+routing result -- top-K, mask, counts, offsets, row order, token-major lists,
+rounding decisions -- must match bit for bit.  Outputs and gradients must
+match the fp32 oracle within max|gpu - ref| / max|ref| <= 2e-2.  The device's
+own router (GEMM + softmax) is checked against the oracle's logits/scores
+within the same tolerance, and its top-K is checked for validity against its
+own scores.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from dense_reference import rel_err
+from paper_2512_14080_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def oracle_scores(inp):
+    L = oracle.router_logits(inp.f32("X"), inp.f32("Wr"), inp.bias, np.float32)
+    return L, oracle.softmax_scores(L).astype(np.float32)
+
+
+def oracle_routing(S, K, round_mode=None, m_tile=None, u=None):
+    idx = oracle.topk_select(S, K)
+    member = oracle.tc_membership(idx, S.shape[1])
+    rdir = None
+    if round_mode:
+        member, _, rdir = oracle.round_tokens(S, member, m_tile, mode=round_mode, u=u)
+    return idx, rdir, oracle.routing_from_membership(member, S, np.float32)
+
+
+def mask_bits(member):
+    """Oracle membership -> the device's [E, ceil(T/64)] uint64 bitmap."""
+    T, E = member.shape
+    Wd = (T + 63) // 64
+    out = np.zeros((E, Wd), np.uint64)
+    for e in range(E):
+        for w in range(Wd):
+            seg = member[w * 64:(w + 1) * 64, e]
+            out[e, w] = np.uint64(sum(int(b) << i for i, b in enumerate(seg)))
+    return out
+
+
+def check_routing(layer, R, idx=None, rdir=None):
+    a = {k: (v.cpu().numpy() if v is not None else None) for k, v in layer.routing.arrays().items()}
+    P = R.P
+    np.testing.assert_array_equal(a["counts"], R.counts)
+    np.testing.assert_array_equal(a["offsets"], R.offsets)
+    np.testing.assert_array_equal(a["row_token"][:P], R.row_token)
+    np.testing.assert_array_equal(a["row_expert"][:P], R.row_expert)
+    np.testing.assert_array_equal(a["tok_offsets"], R.tok_offsets)
+    np.testing.assert_array_equal(a["tok_rows"][:P], R.tok_rows)
+    np.testing.assert_array_equal(a["mask"].view(np.uint64), mask_bits(R.member))
+    # same fp32 operations in the same order: the weights agree exactly
+    np.testing.assert_array_equal(a["row_w"][:P], R.row_w)
+    if idx is not None:
+        tc = {k: v.cpu().numpy() for k, v in layer.tc.arrays().items() if v is not None}
+        np.testing.assert_array_equal(tc["topk_idx"], idx)
+    if rdir is not None:
+        np.testing.assert_array_equal(a["round_dir"], rdir)
+
+
+def run_layer(cfg, seed=0, T=None, round_mode=None, u=None, router_grad=True, bias=None):
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    inp = W.make_inputs(cfg, seed, T=T)
+    if bias is not None:
+        inp.bias = np.asarray(bias, np.float32)
+    _, S = oracle_scores(inp)
+    layer = DeviceLayer(inp, round_mode=round_mode, scores_in=S, u=u, router_grad=router_grad)
+    layer.step()
+    torch.cuda.synchronize()
+    return inp, S, layer
+
+
+def check_layer(cfg, seed=0, T=None, round_mode=None, u=None, bias=None):
+    inp, S, layer = run_layer(cfg, seed, T, round_mode, u, bias=bias)
+    idx, rdir, R = oracle_routing(S, cfg.K, round_mode, cfg.m_tile, u)
+    check_routing(layer, R, idx, rdir)
+    X, W1, W2, Wr, dO = (inp.f32(k) for k in ("X", "W1", "W2", "Wr", "dO"))
+    fw = oracle.forward(X, W1, W2, R)
+    bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R)
+    P = R.P
+    got = {
+        "O": layer.O.float().cpu().numpy(), "H": layer.H[:P].float().cpu().numpy(),
+        "dX": layer.dX.float().cpu().numpy(), "dW1": layer.dW1.float().cpu().numpy(),
+        "dW2": layer.dW2.float().cpu().numpy(), "dWr": layer.dWr.cpu().numpy(),
+        "dbias": layer.dbias.cpu().numpy(), "dS": layer.dS[:P].cpu().numpy(),
+    }
+    ref = {"O": fw["O"], "H": fw["H"], "dX": bw["dX"], "dW1": bw["dW1"], "dW2": bw["dW2"],
+           "dWr": bw["dWr"], "dbias": bw["dbias"], "dS": bw["dS"]}
+    errs = {k: rel_err(got[k], ref[k]) for k in ref}
+    print(cfg.name, T, round_mode, {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    for k, v in errs.items():
+        assert v <= TOL, (k, v, errs)
+    return layer, R
+
+
+TINY = W.CONFIGS["tiny"]
+
+
+def test_tiny_token_choice():
+    check_layer(TINY)
+
+
+@pytest.mark.parametrize("mode", ["nearest", "up", "down", "balance", "stochastic"])
+def test_tiny_token_rounding(mode):
+    u = np.random.default_rng(5).random(TINY.E).astype(np.float32) if mode == "stochastic" else None
+    check_layer(TINY, seed=1, round_mode=mode, u=u)
+
+
+# several tiles per expert with a ragged tail; T not a multiple of 64
+MID = W.MoEConfig("mid", T=3000, d=512, n=256, E=16, K=4, m_tile=128)
+# d not a multiple of 256 (128-wide tiles), n = 192 (dS reduced over three N tiles)
+ODD = W.MoEConfig("odd", T=1000, d=384, n=192, E=24, K=3, m_tile=32)
+# n = 512: dS over two 256-wide N tiles
+WIDE = W.MoEConfig("wide", T=700, d=256, n=512, E=8, K=2, m_tile=64)
+# many experts, Zipf-skewed popularity: empty and tiny experts
+SKEW = W.MoEConfig("skew", T=700, d=256, n=128, E=256, K=8, m_tile=128, zipf_s=1.1)
+
+
+@pytest.mark.parametrize("cfg,mode", [(MID, None), (MID, "nearest"), (ODD, None), (ODD, "up"), (WIDE, None),
+                                      (SKEW, None), (SKEW, "nearest")])
+def test_shapes(cfg, mode):
+    check_layer(cfg, seed=2, round_mode=mode)
+
+
+def test_k_equals_e_and_k_one():
+    check_layer(W.MoEConfig("kE", T=300, d=128, n=64, E=8, K=8, m_tile=16, router="w_std"), seed=3)
+    check_layer(W.MoEConfig("k1", T=300, d=128, n=64, E=8, K=1, m_tile=16), seed=4)
+
+
+def test_single_token_and_one_hot_expert():
+    check_layer(TINY, seed=5, T=1)
+    check_layer(TINY, seed=6, T=65, round_mode="nearest")
+    # expert 3 outranks every other expert for every token: it takes all T rows
+    bias = np.zeros(TINY.E, np.float32)
+    bias[3] = 60.0
+    layer, R = check_layer(TINY, seed=7, T=200, bias=bias)
+    assert R.counts[3] == 200
+
+
+def test_device_router_matches_oracle_scores():
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    for cfg, seed in ((TINY, 0), (MID, 1), (SKEW, 2)):
+        inp = W.make_inputs(cfg, seed)
+        L, S = oracle_scores(inp)
+        layer = DeviceLayer(inp)
+        layer.route()
+        torch.cuda.synchronize()
+        a = {k: v.cpu().numpy() for k, v in layer.tc.arrays().items() if v is not None}
+        assert rel_err(a["logits"], L) <= 1e-4, rel_err(a["logits"], L)
+        assert rel_err(a["scores"], S) <= 1e-4
+        # the device's top-K is a valid stable top-K of the device's own scores
+        Sg, idx = a["scores"], a["topk_idx"]
+        for t in range(0, cfg.T, max(1, cfg.T // 200)):
+            sel = list(idx[t])
+            assert len(set(sel)) == cfg.K
+            worst = min(Sg[t, e] for e in sel)
+            for e in range(cfg.E):
+                if e not in sel:
+                    assert Sg[t, e] < worst or (Sg[t, e] == worst and e > max(x for x in sel if Sg[t, x] == worst))
+        assert a["counts"].sum() == cfg.T * cfg.K
+        np.testing.assert_array_equal(a["counts"], np.bincount(idx.ravel(), minlength=cfg.E))
+
+
+def test_deterministic_bitwise():
+    torch = _torch()
+    inp, S, layer = run_layer(MID, seed=8, round_mode="nearest")
+    first = [t.clone() for t in (layer.O, layer.H, layer.dX, layer.dW1, layer.dW2, layer.dWr, layer.dS)]
+    layer.step()
+    torch.cuda.synchronize()
+    for a, b in zip(first, (layer.O, layer.H, layer.dX, layer.dW1, layer.dW2, layer.dWr, layer.dS)):
+        assert torch.equal(a, b)
+
+
+def test_no_router_grad_path():
+    torch = _torch()
+    inp, S, layer = run_layer(TINY, seed=9, router_grad=False)
+    idx, rdir, R = oracle_routing(S, TINY.K)
+    X, W1, W2, dO = (inp.f32(k) for k in ("X", "W1", "W2", "dO"))
+    fw = oracle.forward(X, W1, W2, R)
+    bw = oracle.backward(dO, X, fw["H"], W1, W2, None, R)
+    assert rel_err(layer.dX.float().cpu().numpy(), bw["dX"]) <= TOL
