@@ -1,25 +1,34 @@
 // Grouped GEMM core for gfx950: bf16 MFMA (v_mfma_f32_32x32x16_bf16) with
-// fp32 accumulation, LDS double buffering and gather-fused operand loads.
+// fp32 accumulation, operands streamed HBM -> LDS by direct (LDS-DMA) loads.
 //
 // The paper builds its whole MoE computation from one grouped GEMM with
 // modular fusion plus an aggregation kernel (Section 3.1).  This core is that
-// grouped GEMM, written for CDNA4: a 256-thread workgroup (4 wave64, 2 x 2)
-// computes a BM x BN tile of C[M,N] = sum_k Mside[m,k] * Nside[n,k].
+// grouped GEMM written for CDNA4.  A 512-thread workgroup (8 wave64, two per
+// SIMD) computes a BM x BN tile of C[M,N] = sum_k Mside[m,k] * Nside[n,k].
 //
-// Both operands are staged in LDS as [rows][64 k] bf16 tiles, k contiguous,
-// with the 16-byte chunk index XOR-swizzled by (row & 7) so the fragment reads
-// of 32 consecutive rows hit distinct banks.  Operands are fetched in one of
-// two source layouts:
-//   ROWS   : operand rows with k contiguous in memory (X, dO, A, dH, weight
-//            rows of W1/W2 read transposed); rows may be gathered through an
-//            index list (the token gather of Section 4.1.1 fused into the load)
-//   KOUTER : k is the outer (row) index in memory and the operand's m/n index
-//            is contiguous (W1/W2 in the forward, all operands of the weight
-//            gradients); a thread loads an 8(k) x 8(m) block with 16-byte
-//            loads, transposes it in registers and writes 8 k-contiguous
-//            16-byte rows to LDS.  k rows may be gathered (varlen-K weight
-//            gradients over an expert's tokens) and are zero-filled past the
-//            end of the reduction.
+// Operands never pass through registers on their way to LDS:
+// global_load_lds_dwordx4 writes 16 bytes per lane straight into LDS.  The
+// LDS layout of a stage is chosen per operand:
+//   ROWS   : operand rows with k contiguous in memory (X, dO, A, dH, W rows).
+//            LDS tile [rows][64 k], 128-byte rows, 16-byte chunk index
+//            XOR-swizzled by (row & 7).  Rows may be gathered through an index
+//            list -- the token gather of Section 4.1.1 fused into the load.
+//            MFMA fragments are read with ds_read_b128.
+//   KOUTER : k is the outer index in memory, m/n contiguous (W1/W2 in the
+//            forward, every operand of the weight gradients).  LDS tile
+//            [64 k][R], stored as in memory with a 16-byte chunk XOR swizzle
+//            on the k row.  MFMA fragments (8 consecutive k of one column)
+//            are read with the CDNA4 transposing load ds_read_b64_tr_b16, so
+//            no register transpose is needed.  k rows may be gathered
+//            (varlen-K weight gradients over an expert's tokens) and rows past
+//            the end of the reduction read a zero page.
+//
+// The k loop keeps STAGES LDS buffers; each step waits for its own stage
+// (s_waitcnt vmcnt + s_barrier), then issues the DMA for the stage
+// STAGES-1 ahead, then runs the MFMAs, so loads overlap a full stage of
+// compute with one barrier per step.  The DMA and the wait are inline
+// assembly so the compiler's conservative LDS-DMA tracking does not serialise
+// the pipeline; every wait that orders DMA data is explicit here.
 //
 // The MFMA is issued as D = Nfrag x Mfrag, so a lane's accumulator holds one
 // m (lane % 32) and 16 n values in four runs of 4 consecutive columns; row
@@ -29,10 +38,17 @@
 
 namespace smoe {
 
-constexpr int kBK = 64;          // k per LDS stage
-constexpr int kRowBytes = 128;   // one LDS tile row: 64 bf16
+constexpr int kThreads = 512;
+constexpr int kWaves = kThreads / 64;
+constexpr int kBK = 64;
 
 enum SrcMode { ROWS = 0, KOUTER = 1 };
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+#define SMOE_LDS __attribute__((address_space(3)))
+
+// read-only zero page for masked k rows / columns of KOUTER operands
+__device__ __attribute__((aligned(4096))) uint32_t g_zero_page[1024];
 
 struct TileInfo {
   int e;        // expert (group)
@@ -44,87 +60,175 @@ struct TileInfo {
   int k_len;    // reduction length
 };
 
-__device__ __forceinline__ int lds_off(int row, int chunk) { return row * kRowBytes + ((chunk ^ (row & 7)) << 4); }
-
-// 8x8 transpose of bf16: in[j] holds 8 consecutive m of k-row j; out[c] holds
-// 8 consecutive k of m-column c.
-__device__ __forceinline__ void transpose8x8(const u32x4 (&in)[8], u32x4 (&out)[8]) {
-#pragma unroll
-  for (int c = 0; c < 8; ++c) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t a = in[2 * q][c >> 1];
-      const uint32_t b = in[2 * q + 1][c >> 1];
-      out[c][q] = (c & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
-    }
-  }
+// One 16-byte-per-lane LDS DMA.  lds_byte must be wave-uniform (it goes to M0).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_byte) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_byte), "v"(g) : "memory", "m0");
 }
+// Wait until at most N of this wave's vector-memory ops are outstanding, then
+// workgroup barrier.  LDS reads of the previous step are complete as well.
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// ---------------------------------------------------------------------------
-// ROWS loader: R rows x 64 k per stage; thread -> (row = tid/8 + 32p, chunk = tid%8)
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_>
+struct GemmCfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_;
+  static constexpr int RM = BM / WM / 32, RN = BN / WN / 32;
+  static constexpr int M_BYTES = BM * kBK * 2, N_BYTES = BN * kBK * 2;
+  static constexpr int STAGE_BYTES = M_BYTES + N_BYTES;
+  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
+  static constexpr int QM = BM / 64, QN = BN / 64;  // DMA instructions per wave per stage
+  static_assert(WM * WN == kWaves, "8 waves");
+  static_assert(RM >= 1 && RN >= 1 && BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "wave tile");
+  static_assert(BM % 64 == 0 && BN % 64 == 0, "tile multiple of 64");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+};
+
+// ---------------------------------------------------------------- ROWS side
+// LDS: [R][64] bf16, chunk c of row r at r*128 + ((c ^ (r & 7)) << 4).
+// DMA instruction q covers rows 8q..8q+7; lane l -> row 8q + l/8, physical
+// chunk l%8, logical chunk (l%8) ^ (l/8).
 template <int R>
-struct RowsLoader {
-  static constexpr int P = R / 32;
-  const char* ptr[P];  // byte pointer to the row start (k = 0)
-  u32x4 buf[P];
-
-  __device__ __forceinline__ void stage_load(int k0) {
-    const int chunk = threadIdx.x & 7;
+struct RowsSide {
+  static constexpr int Q = R / 64;  // instructions per wave
+  const char* ptr[Q];               // row start (k = 0) of the row this lane loads, per instruction
+  __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, const int32_t* idx, int row_base, int nrows) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int logical = (lane & 7) ^ (lane >> 3);
 #pragma unroll
-    for (int p = 0; p < P; ++p) buf[p] = *(const u32x4*)(ptr[p] + (size_t)(k0 + chunk * 8) * 2);
-  }
-  __device__ __forceinline__ void stage_store(char* lds) const {
-    const int chunk = threadIdx.x & 7;
-#pragma unroll
-    for (int p = 0; p < P; ++p) {
-      const int row = (threadIdx.x >> 3) + 32 * p;
-      *(u32x4*)(lds + lds_off(row, chunk)) = buf[p];
+    for (int j = 0; j < Q; ++j) {
+      const int q = wave + kWaves * j;
+      const int r = min(8 * q + (lane >> 3), nrows - 1);
+      const int64_t row = idx ? (int64_t)idx[row_base + r] : (int64_t)(row_base + r);
+      ptr[j] = (const char*)(base + row * ld) + logical * 16;
     }
+  }
+  __device__ __forceinline__ void issue(uint32_t lds_side, int k0) const {
+    const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+#pragma unroll
+    for (int j = 0; j < Q; ++j) dma16(ptr[j] + k0 * 2, lds_side + (w + kWaves * j) * 1024);
+  }
+  static __device__ __forceinline__ bf16x8 frag(const char* lds_side, int r0, int s) {
+    const int lane = threadIdx.x & 63;
+    const int row = r0 + (lane & 31);
+    const int c = (2 * s + (lane >> 5)) ^ (row & 7);
+    return *(const bf16x8*)(lds_side + row * 128 + c * 16);
   }
 };
 
-// KOUTER loader: R (m) x 64 k per stage from a [k][ld] matrix.
-// thread -> kb = tid%8 (k rows 8kb..8kb+7), rb = tid/8 (m cols 8rb..8rb+7)
+// --------------------------------------------------------------- KOUTER side
+// LDS: [64 k][R] bf16 (2R bytes per k row, L = R/8 chunks), chunk c of row k
+// at k*2R + ((c ^ x(k)) << 4) with x(k) = 4*(k%4) for L >= 16 and
+// 4*((k/2)%2) for L = 8; with it, the 8 k rows x 64 bytes one transposing
+// read touches spread over all banks.
 template <int R>
-struct KOuterLoader {
-  static constexpr bool kActive = true;
-  const char* colptr;  // byte pointer to element (k row 0 of the matrix, this thread's m col block), or null
+struct KOuterSide {
+  static constexpr int L = R / 8;
+  static constexpr int RPI = 512 / R;  // k rows per DMA instruction
+  static constexpr int Q = R / 64;     // instructions per wave
+  static_assert(L >= 8, "R >= 64");
+  static __device__ __forceinline__ int swz(int k) { return L >= 16 ? 4 * (k & 3) : 4 * ((k >> 1) & 1); }
+
+  const char* base;      // matrix base (bytes)
   int64_t ld_bytes;
-  const int32_t* gidx; // gathered k rows (index into the matrix rows), or null
+  const int32_t* gidx;   // gathered k rows, or null
   int k_begin, k_len;
-  bool active;         // this thread owns an m block inside R and inside the valid columns
-  u32x4 raw[8];
+  int krow[Q];           // tile-local k row this lane loads, per instruction
+  int colb[Q];           // byte offset of this lane's 16 bytes within the stored row (or -1: masked column)
+  int gnext[Q];          // gathered row index for the next stage to issue
 
-  __device__ __forceinline__ void stage_load(int k0) {
-    const int kb = threadIdx.x & 7;
+  // colmap(local_col) -> global column of tile-local column local_col (multiple of 8)
+  template <class ColMap>
+  __device__ __forceinline__ void init(const uint16_t* b, int64_t ld, const int32_t* g, int kb, int kl, int cvalid,
+                                       ColMap colmap) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    base = (const char*)b;
+    ld_bytes = ld * 2;
+    gidx = g;
+    k_begin = kb;
+    k_len = kl;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int k = k0 + kb * 8 + j;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (active && k < k_len) {
-        const int64_t row = gidx ? (int64_t)gidx[k_begin + k] : (int64_t)(k_begin + k);
-        v = *(const u32x4*)(colptr + row * ld_bytes);
-      }
-      raw[j] = v;
+    for (int j = 0; j < Q; ++j) {
+      const int q = wave + kWaves * j;
+      const int row = q * RPI + lane / L;
+      const int phys = lane % L;
+      const int logical = phys ^ swz(row);
+      const int gc = colmap(8 * logical);
+      krow[j] = row;
+      colb[j] = gc < cvalid ? gc * 2 : -1;
     }
   }
-  __device__ __forceinline__ void stage_store(char* lds) const {
-    const int kb = threadIdx.x & 7;
-    const int r0 = (threadIdx.x >> 3) * 8;
-    if (r0 >= R) return;
-    u32x4 t[8];
-    transpose8x8(raw, t);
+  // gathered operands: fetch the row indices of the stage at k0 (registers)
+  __device__ __forceinline__ void prefetch_idx(int k0) {
+    if (!gidx) return;
 #pragma unroll
-    for (int c = 0; c < 8; ++c) *(u32x4*)(lds + (r0 + c) * kRowBytes + ((kb ^ c) << 4)) = t[c];
+    for (int j = 0; j < Q; ++j) {
+      const int k = k0 + krow[j];
+      gnext[j] = k < k_len ? gidx[k_begin + k] : 0;
+    }
+  }
+  // make the compiler complete the index loads before the DMA asm below
+  __device__ __forceinline__ void idx_ready() {
+    if (!gidx) return;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) asm volatile("" ::"v"(gnext[j]));
+  }
+  __device__ __forceinline__ void issue(uint32_t lds_side, int k0) const {
+    const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      const int k = k0 + krow[j];
+      const char* src;
+      if (k < k_len && colb[j] >= 0) {
+        const int64_t row = gidx ? (int64_t)gnext[j] : (int64_t)(k_begin + k);
+        src = base + row * ld_bytes + colb[j];
+      } else {
+        src = (const char*)g_zero_page + lane * 16;
+      }
+      dma16(src, lds_side + (w + kWaves * j) * 1024);
+    }
+  }
+  static __device__ __forceinline__ bf16x8 frag(const char* lds_side, int c0, int s) {
+    // 32 columns c0..c0+31, 8 k (16s + 8*(lane/32) ..) per lane, two transposing reads
+    const int lane = threadIdx.x & 63;
+    const int g = lane >> 4, i = lane & 15;
+    const int m = c0 + 16 * (g & 1) + 4 * (i & 3);
+    const int kb = 16 * s + 8 * (g >> 1) + (i >> 2);
+    v4i16 lo, hi;
+    {
+      const int k = kb;
+      const char* p = lds_side + k * (2 * R) + (((m >> 3) ^ swz(k)) << 4) + (m & 7) * 2;
+      lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SMOE_LDS v4i16*)p);
+    }
+    {
+      const int k = kb + 4;
+      const char* p = lds_side + k * (2 * R) + (((m >> 3) ^ swz(k)) << 4) + (m & 7) * 2;
+      hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SMOE_LDS v4i16*)p);
+    }
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
   }
 };
 
-template <int BM, int BN>
-struct MfmaTile {
-  static constexpr int RM = BM / 64;
-  static constexpr int RN = BN / 64;
-  f32x16 acc[RM][RN];
+template <int MODE, int R>
+struct SideT;
+template <int R>
+struct SideT<ROWS, R> {
+  using type = RowsSide<R>;
+};
+template <int R>
+struct SideT<KOUTER, R> {
+  using type = KOuterSide<R>;
+};
 
+template <class Cfg>
+struct Acc {
+  static constexpr int RM = Cfg::RM, RN = Cfg::RN;
+  f32x16 acc[RM][RN];
   __device__ __forceinline__ void zero() {
 #pragma unroll
     for (int i = 0; i < RM; ++i)
@@ -133,44 +237,16 @@ struct MfmaTile {
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
   }
-
-  // one 64-wide k stage from LDS tiles lm [BM][64] and ln [BN][64]
-  __device__ __forceinline__ void compute(const char* lm, const char* ln) {
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int wm = wave & 1, wn = wave >> 1;
-    const int r32 = lane & 31, hi = lane >> 5;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int chunk = 2 * s + hi;
-      bf16x8 fm[RM], fn[RN];
-#pragma unroll
-      for (int i = 0; i < RM; ++i) {
-        const int row = wm * (BM / 2) + i * 32 + r32;
-        fm[i] = *(const bf16x8*)(lm + lds_off(row, chunk));
-      }
-#pragma unroll
-      for (int j = 0; j < RN; ++j) {
-        const int row = wn * (BN / 2) + j * 32 + r32;
-        fn[j] = *(const bf16x8*)(ln + lds_off(row, chunk));
-      }
-#pragma unroll
-      for (int i = 0; i < RM; ++i)
-#pragma unroll
-        for (int j = 0; j < RN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc[i][j], 0, 0, 0);
-    }
-  }
-
-  // coordinates of accumulator element (i, j, v) for this lane, tile-local
+  // tile-local coordinates of accumulator element (i, j, 4g..4g+3) of this lane
   __device__ __forceinline__ static int m_of(int i) {
     const int wave = threadIdx.x >> 6;
-    return (wave & 1) * (BM / 2) + i * 32 + (threadIdx.x & 31);
+    return (wave % Cfg::WM) * (Cfg::BM / Cfg::WM) + i * 32 + (threadIdx.x & 31);
   }
-  // first of the 4 consecutive columns of group g (v = 4g..4g+3) in block j
   __device__ __forceinline__ static int n_of(int j, int g) {
     const int wave = threadIdx.x >> 6;
-    return (wave >> 1) * (BN / 2) + j * 32 + 8 * g + 4 * ((threadIdx.x >> 5) & 1);
+    return (wave / Cfg::WM) * (Cfg::BN / Cfg::WN) + j * 32 + 8 * g + 4 * ((threadIdx.x >> 5) & 1);
   }
+  __device__ __forceinline__ static int wave_n() { return (threadIdx.x >> 6) / Cfg::WM; }
 };
 
 // XCD-aware remap of the flat workgroup id: workgroups are dispatched to the
@@ -230,47 +306,86 @@ __device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets,
 }
 
 // The main loop shared by every GEMM.  Op supplies:
-//   Op::BM, Op::BN, Op::kMinBlocks
-//   bool tile(const Params&, TileInfo&, int* sh)     -- scheduling
-//   MLoader / NLoader types with stage_load/stage_store, built by
-//   make_m(p, ti) / make_n(p, ti)
-//   void epilogue(const Params&, const TileInfo&, MfmaTile&, char* smem)
+//   using Cfg = GemmCfg<...>;  static constexpr int M_MODE, N_MODE;
+//   bool tile(const Params&, TileInfo&, int* sh)          -- scheduling
+//   void init_m(const Params&, const TileInfo&, Side&)      -- operand sides
+//   void init_n(const Params&, const TileInfo&, Side&)
+//   void epilogue(const Params&, const TileInfo&, Acc<Cfg>&, char* smem)
 template <class Op>
-__global__ __launch_bounds__(256, Op::kMinBlocks) void grouped_gemm_kernel(const typename Op::Params p) {
-  constexpr int BM = Op::BM, BN = Op::BN;
-  constexpr int kStage = (BM + BN) * kRowBytes;
-  __shared__ __attribute__((aligned(16))) char smem[2 * kStage];
+__global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typename Op::Params p) {
+  using Cfg = typename Op::Cfg;
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, S = Cfg::STAGES;
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES];
   __shared__ int sh[8];
   TileInfo ti;
   if (!Op::tile(p, ti, sh)) return;
-  auto ml = Op::make_m(p, ti);
-  auto nl = Op::make_n(p, ti);
-  MfmaTile<BM, BN> mt;
-  mt.zero();
+  typename SideT<Op::M_MODE, BM>::type ms;
+  typename SideT<Op::N_MODE, BN>::type ns;
+  Op::init_m(p, ti, ms);
+  Op::init_n(p, ti, ns);
+  Acc<Cfg> acc;
+  acc.zero();
   const int nk = (ti.k_len + kBK - 1) / kBK;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
+  const int wave = threadIdx.x >> 6;
+  const int wm0 = (wave % Cfg::WM) * (BM / Cfg::WM);
+  const int wn0 = (wave / Cfg::WM) * (BN / Cfg::WN);
+  constexpr int kPerStage = Cfg::QM + Cfg::QN;  // DMA ops per wave per stage
+
   if (nk > 0) {
-    ml.stage_load(0);
-    nl.stage_load(0);
-    ml.stage_store(smem);
-    nl.stage_store(smem + BM * kRowBytes);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      char* cur = smem + (kt & 1) * kStage;
-      char* nxt = smem + ((kt + 1) & 1) * kStage;
-      const bool more = kt + 1 < nk;
-      if (more) {
-        ml.stage_load((kt + 1) * kBK);
-        nl.stage_load((kt + 1) * kBK);
+    // prologue: stages 0 .. S-2
+#pragma unroll
+    for (int st = 0; st < S - 1; ++st) {
+      if (st < nk) {
+        if constexpr (Op::M_MODE == KOUTER) { ms.prefetch_idx(st * kBK); ms.idx_ready(); }
+        if constexpr (Op::N_MODE == KOUTER) { ns.prefetch_idx(st * kBK); ns.idx_ready(); }
+        ms.issue(lds0 + st * Cfg::STAGE_BYTES, st * kBK);
+        ns.issue(lds0 + st * Cfg::STAGE_BYTES + Cfg::M_BYTES, st * kBK);
       }
-      mt.compute(cur, cur + BM * kRowBytes);
-      if (more) {
-        ml.stage_store(nxt);
-        nl.stage_store(nxt + BM * kRowBytes);
-      }
-      __syncthreads();
     }
+    if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((S - 1) * kBK);
+    if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((S - 1) * kBK);
+    for (int kt = 0; kt < nk; ++kt) {
+      // stage kt is complete when at most (stages issued after it) * kPerStage ops remain
+      const int ahead = min(S - 2, nk - 1 - kt);
+      if constexpr (S == 3) {
+        if (ahead >= 1)
+          wait_vm_barrier<kPerStage>();
+        else
+          wait_vm_barrier<0>();
+      } else {
+        wait_vm_barrier<0>();
+      }
+      const int knext = kt + S - 1;
+      if (knext < nk) {
+        const uint32_t st = lds0 + (knext % S) * Cfg::STAGE_BYTES;
+        if constexpr (Op::M_MODE == KOUTER) ms.idx_ready();
+        if constexpr (Op::N_MODE == KOUTER) ns.idx_ready();
+        ms.issue(st, knext * kBK);
+        ns.issue(st + Cfg::M_BYTES, knext * kBK);
+        if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * kBK);
+        if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * kBK);
+      }
+      const char* cur = smem + (kt % S) * Cfg::STAGE_BYTES;
+      const char* lm = cur;
+      const char* ln = cur + Cfg::M_BYTES;
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        bf16x8 fm[Cfg::RM], fn[Cfg::RN];
+#pragma unroll
+        for (int i = 0; i < Cfg::RM; ++i) fm[i] = SideT<Op::M_MODE, BM>::type::frag(lm, wm0 + 32 * i, s);
+#pragma unroll
+        for (int j = 0; j < Cfg::RN; ++j) fn[j] = SideT<Op::N_MODE, BN>::type::frag(ln, wn0 + 32 * j, s);
+#pragma unroll
+        for (int i = 0; i < Cfg::RM; ++i)
+#pragma unroll
+          for (int j = 0; j < Cfg::RN; ++j)
+            acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc.acc[i][j], 0, 0, 0);
+      }
+    }
+    barrier_lds();  // every wave done with the LDS stages before the epilogue reuses them
   }
-  Op::epilogue(p, ti, mt, smem);
+  Op::epilogue(p, ti, acc, smem);
 }
 
 }  // namespace smoe

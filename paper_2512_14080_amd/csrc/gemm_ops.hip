@@ -80,58 +80,34 @@ __device__ __forceinline__ bool tile_varlen_k(const int32_t* offsets, int M, int
   return true;
 }
 
-// ROWS loader over rows [row_base, row_base + mrows) of a [*, ld] bf16 matrix,
-// optionally gathered through idx.  Rows past mrows are clamped to the last
-// valid row; their results are never stored.
-template <int R>
-__device__ __forceinline__ RowsLoader<R> rows_loader(const uint16_t* base, int64_t ld, const int32_t* idx, int row_base,
-                                                     int mrows) {
-  RowsLoader<R> L;
-#pragma unroll
-  for (int p = 0; p < R / 32; ++p) {
-    const int m = min((threadIdx.x >> 3) + 32 * p, mrows - 1);
-    const int64_t row = idx ? (int64_t)idx[row_base + m] : (int64_t)(row_base + m);
-    L.ptr[p] = (const char*)(base + row * ld);
-  }
-  return L;
-}
-
-// KOUTER loader: columns [c0 + 8rb, +8) of a [*, ld] matrix, k rows
-// k_begin.. (optionally gathered), valid columns < cvalid.
-template <int R>
-__device__ __forceinline__ KOuterLoader<R> kouter_loader(const uint16_t* base, int64_t ld, int c0, int cvalid,
-                                                         const int32_t* gidx, int k_begin, int k_len) {
-  KOuterLoader<R> L;
-  const int r0 = (threadIdx.x >> 3) * 8;
-  L.active = (r0 < R) && (c0 + r0 < cvalid);
-  L.colptr = (const char*)(base + c0 + r0);
-  L.ld_bytes = ld * 2;
-  L.gidx = gidx;
-  L.k_begin = k_begin;
-  L.k_len = k_len;
-  return L;
-}
+struct ColOffset {
+  int c0;
+  __device__ __forceinline__ int operator()(int c) const { return c0 + c; }
+};
 
 // ================================================================== router
-template <int BN_>
+template <class Cfg_>
 struct OpRouter {
-  static constexpr int BM = 128, BN = BN_, kMinBlocks = BN_ >= 256 ? 1 : 2;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
   struct Params { RouterGemmArgs a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int*) { return tile_plain_m<BM, BN>(p.a.T, p.a.E, p.a.d, ti); }
-  static __device__ RowsLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return rows_loader<BM>(p.a.X, p.a.d, nullptr, ti.row_base, ti.mrows);
+  static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
+    return tile_plain_m<Cfg::BM, Cfg::BN>(p.a.T, p.a.E, p.a.d, ti);
   }
-  static __device__ KOuterLoader<BN> make_n(const Params& p, const TileInfo& ti) {
-    return kouter_loader<BN>(p.a.Wr, p.a.E, ti.n0, p.a.E, nullptr, 0, p.a.d);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+    s.init(p.a.X, p.a.d, nullptr, ti.row_base, ti.mrows);
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char*) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+    s.init(p.a.Wr, p.a.E, nullptr, 0, p.a.d, p.a.E, ColOffset{ti.n0});
+  }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
 #pragma unroll
-    for (int i = 0; i < t.RM; ++i) {
+    for (int i = 0; i < Cfg::RM; ++i) {
       const int m = t.m_of(i);
       if (m >= ti.mrows) continue;
       float* out = p.a.logits + (size_t)(ti.row_base + m) * p.a.E;
 #pragma unroll
-      for (int j = 0; j < t.RN; ++j)
+      for (int j = 0; j < Cfg::RN; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int col = ti.n0 + t.n_of(j, g);
@@ -146,38 +122,41 @@ struct OpRouter {
 };
 
 // ================================================================== up-proj
-// N tile: BN/2 gate columns [j0, j0 + BN/2) and the matching up columns.
-// Wave half wn owns gate columns j0 + wn*BN/4 + [0, BN/4) in its first RN/2
-// accumulator blocks and the matching up columns in the last RN/2 blocks.
-template <int BM_, int BN_>
+// N tile: BN/2 gate columns starting at j0 = nt * BN/2 and the matching up
+// columns.  Wave column group wn owns Wn = BN/WN tile columns: its first
+// Wn/2 are gate columns j0 + wn*Wn/2 + [0, Wn/2) (accumulator blocks
+// j < RN/2) and its last Wn/2 the matching up columns (blocks j >= RN/2).
+template <class Cfg_>
 struct OpUp {
-  static constexpr int BM = BM_, BN = BN_, kMinBlocks = 1;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
+  static constexpr int Wn = Cfg::BN / Cfg::WN;
+  static_assert(Cfg::RN % 2 == 0, "gate and up blocks in one wave");
   struct Params { UpArgs a; };
+  struct ColMap {
+    int j0, n;
+    __device__ __forceinline__ int operator()(int c) const {
+      const int wn = c / Wn, q = c % Wn;
+      return q < Wn / 2 ? j0 + wn * (Wn / 2) + q : n + j0 + wn * (Wn / 2) + (q - Wn / 2);
+    }
+  };
   static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<BM, BN>(p.a.offsets, p.a.E, 2 * p.a.n, p.a.d, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, p.a.d, sh, ti);
   }
-  static __device__ RowsLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return rows_loader<BM>(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+    s.init(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
   }
-  static __device__ __forceinline__ int w1_col(const Params& p, const TileInfo& ti, int r) {
-    const int j0 = (ti.n0 / BN) * (BN / 2);
-    const int wn = r / (BN / 2), q = r % (BN / 2);
-    return q < BN / 4 ? j0 + wn * (BN / 4) + q : p.a.n + j0 + wn * (BN / 4) + (q - BN / 4);
-  }
-  static __device__ KOuterLoader<BN> make_n(const Params& p, const TileInfo& ti) {
-    const int r0 = (threadIdx.x >> 3) * 8;
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
     const uint16_t* w = p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n);
-    KOuterLoader<BN> L = kouter_loader<BN>(w, 2 * p.a.n, 0, 1 << 30, nullptr, 0, p.a.d);
-    L.colptr = (const char*)(w + (r0 < BN ? w1_col(p, ti, r0) : 0));
-    return L;
+    s.init(w, 2 * p.a.n, nullptr, 0, p.a.d, 2 * p.a.n, ColMap{(ti.n0 / Cfg::BN) * (Cfg::BN / 2), p.a.n});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char*) {
-    constexpr int RN = MfmaTile<BM, BN>::RN;
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
+    constexpr int RN = Cfg::RN;
     const int n = p.a.n;
-    const int j0 = (ti.n0 / BN) * (BN / 2);
-    const int wn = (threadIdx.x >> 6) >> 1;
+    const int j0 = (ti.n0 / Cfg::BN) * (Cfg::BN / 2);
+    const int wn = t.wave_n();
 #pragma unroll
-    for (int i = 0; i < t.RM; ++i) {
+    for (int i = 0; i < Cfg::RM; ++i) {
       const int m = t.m_of(i);
       if (m >= ti.mrows) continue;
       const size_t row = (size_t)(ti.row_base + m);
@@ -187,8 +166,8 @@ struct OpUp {
       for (int j = 0; j < RN / 2; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int q = t.n_of(j, g) - wn * (BN / 2);
-          const int col = j0 + wn * (BN / 4) + q;
+          const int q = t.n_of(j, g) - wn * Wn;
+          const int col = j0 + wn * (Wn / 2) + q;
           float gv[4], uv[4], av[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -205,35 +184,42 @@ struct OpUp {
   }
 };
 
+template <class Cfg>
+__device__ __forceinline__ void store_rows_bf16(uint16_t* out, int64_t ld, int row_base, int mrows, int n0,
+                                                Acc<Cfg>& t) {
+#pragma unroll
+  for (int i = 0; i < Cfg::RM; ++i) {
+    const int m = t.m_of(i);
+    if (m >= mrows) continue;
+    uint16_t* y = out + (size_t)(row_base + m) * ld + n0;
+#pragma unroll
+    for (int j = 0; j < Cfg::RN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = t.n_of(j, g);
+        store_bf16x4(y + c, t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
+      }
+  }
+}
+
 // ================================================================== down-proj
-template <int BM_, int BN_>
+template <class Cfg_>
 struct OpDown {
-  static constexpr int BM = BM_, BN = BN_, kMinBlocks = 1;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
   struct Params { DownArgs a; };
   static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<BM, BN>(p.a.offsets, p.a.E, p.a.d, p.a.n, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, p.a.n, sh, ti);
   }
-  static __device__ RowsLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return rows_loader<BM>(p.a.A, p.a.n, nullptr, ti.row_base, ti.mrows);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+    s.init(p.a.A, p.a.n, nullptr, ti.row_base, ti.mrows);
   }
-  static __device__ KOuterLoader<BN> make_n(const Params& p, const TileInfo& ti) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
     const uint16_t* w = p.a.W2 + (size_t)ti.e * p.a.n * p.a.d;
-    return kouter_loader<BN>(w, p.a.d, ti.n0, p.a.d, nullptr, 0, p.a.n);
+    s.init(w, p.a.d, nullptr, 0, p.a.n, p.a.d, ColOffset{ti.n0});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char*) {
-#pragma unroll
-    for (int i = 0; i < t.RM; ++i) {
-      const int m = t.m_of(i);
-      if (m >= ti.mrows) continue;
-      uint16_t* y = p.a.Y + (size_t)(ti.row_base + m) * p.a.d + ti.n0;
-#pragma unroll
-      for (int j = 0; j < t.RN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c = t.n_of(j, g);
-          store_bf16x4(y + c, t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
-        }
-    }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
+    store_rows_bf16<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t);
   }
 };
 
@@ -241,28 +227,28 @@ struct OpDown {
 // Epilogue (down-proj backward): with A recomputed from the cached H,
 // dS = <dA', A> (reduced over this tile's n columns), dA = s dA',
 // dH = dSwiGLU(dA, H), A' = s A.
-template <int BM_, int BN_>
+template <class Cfg_>
 struct OpDH {
-  static constexpr int BM = BM_, BN = BN_, kMinBlocks = 1;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DHArgs a; };
   static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<BM, BN>(p.a.offsets, p.a.E, p.a.n, p.a.d, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, p.a.d, sh, ti);
   }
-  static __device__ RowsLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return rows_loader<BM>(p.a.dO, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+    s.init(p.a.dO, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
   }
-  static __device__ RowsLoader<BN> make_n(const Params& p, const TileInfo& ti) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, RowsSide<Cfg::BN>& s) {
     // rows of W2_e [n][d] are the n columns of dA', with d contiguous
-    const uint16_t* w = p.a.W2 + (size_t)ti.e * p.a.n * p.a.d;
-    return rows_loader<BN>(w, p.a.d, nullptr, ti.n0, BN);
+    s.init(p.a.W2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, nullptr, ti.n0, Cfg::BN);
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char* smem) {
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* smem) {
     const int n = p.a.n;
     const int lane = threadIdx.x & 63;
-    const int wn = (threadIdx.x >> 6) >> 1;
-    float* red = (float*)smem;  // [BM][2]
+    const int wn = t.wave_n();
+    float* red = (float*)smem;  // [BM][WN]
 #pragma unroll
-    for (int i = 0; i < t.RM; ++i) {
+    for (int i = 0; i < Cfg::RM; ++i) {
       const int m = t.m_of(i);
       const bool valid = m < ti.mrows;
       const size_t row = (size_t)(ti.row_base + (valid ? m : 0));
@@ -271,39 +257,42 @@ struct OpDH {
       uint16_t* dh = p.a.dH + row * (2 * n);
       uint16_t* ap = p.a.Ap + row * n;
       float part = 0.f;
+      if (valid) {
 #pragma unroll
-      for (int j = 0; j < t.RN; ++j)
+        for (int j = 0; j < Cfg::RN; ++j)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          if (!valid) continue;
-          const int col = ti.n0 + t.n_of(j, g);
-          float gv[4], uv[4], dg[4], du[4], apv[4];
-          load_bf16x4(h + col, gv);
-          load_bf16x4(h + n + col, uv);
+          for (int g = 0; g < 4; ++g) {
+            const int col = ti.n0 + t.n_of(j, g);
+            float gv[4], uv[4], dg[4], du[4], apv[4];
+            load_bf16x4(h + col, gv);
+            load_bf16x4(h + n + col, uv);
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float dap = t.acc[i][j][4 * g + r];
-            float sg;
-            const float sl = silu_sig(gv[r], &sg);
-            const float av = sl * uv[r];
-            part += dap * av;
-            const float da = s * dap;
-            dg[r] = da * uv[r] * sg * (1.f + gv[r] * (1.f - sg));
-            du[r] = da * sl;
-            apv[r] = s * av;
+            for (int r = 0; r < 4; ++r) {
+              const float dap = t.acc[i][j][4 * g + r];
+              float sg;
+              const float sl = silu_sig(gv[r], &sg);
+              const float av = sl * uv[r];
+              part += dap * av;
+              const float da = s * dap;
+              dg[r] = da * uv[r] * sg * (1.f + gv[r] * (1.f - sg));
+              du[r] = da * sl;
+              apv[r] = s * av;
+            }
+            store_bf16x4(dh + col, dg[0], dg[1], dg[2], dg[3]);
+            store_bf16x4(dh + n + col, du[0], du[1], du[2], du[3]);
+            store_bf16x4(ap + col, apv[0], apv[1], apv[2], apv[3]);
           }
-          store_bf16x4(dh + col, dg[0], dg[1], dg[2], dg[3]);
-          store_bf16x4(dh + n + col, du[0], du[1], du[2], du[3]);
-          store_bf16x4(ap + col, apv[0], apv[1], apv[2], apv[3]);
-        }
+      }
       part += __shfl_xor(part, 32, kWave);
-      if (lane < 32) red[m * 2 + wn] = part;
+      if (lane < 32) red[m * Cfg::WN + wn] = part;
     }
     __syncthreads();
-    const int nnt = n / BN;
-    const int nt = ti.n0 / BN;
-    for (int m = threadIdx.x; m < ti.mrows; m += 256) {
-      const float v = red[m * 2] + red[m * 2 + 1];
+    const int nnt = n / Cfg::BN;
+    const int nt = ti.n0 / Cfg::BN;
+    for (int m = threadIdx.x; m < ti.mrows; m += kThreads) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < Cfg::WN; ++w) v += red[m * Cfg::WN + w];
       const size_t row = (size_t)(ti.row_base + m);
       if (nnt == 1)
         p.a.dS[row] = v;
@@ -314,122 +303,101 @@ struct OpDH {
 };
 
 // ================================================================== dX~
-template <int BM_, int BN_>
+template <class Cfg_>
 struct OpDXt {
-  static constexpr int BM = BM_, BN = BN_, kMinBlocks = 1;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DXtArgs a; };
   static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<BM, BN>(p.a.offsets, p.a.E, p.a.d, 2 * p.a.n, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, 2 * p.a.n, sh, ti);
   }
-  static __device__ RowsLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return rows_loader<BM>(p.a.dH, 2 * p.a.n, nullptr, ti.row_base, ti.mrows);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+    s.init(p.a.dH, 2 * p.a.n, nullptr, ti.row_base, ti.mrows);
   }
-  static __device__ RowsLoader<BN> make_n(const Params& p, const TileInfo& ti) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, RowsSide<Cfg::BN>& s) {
     // rows of W1_e [d][2n] are the d columns of dX~, with 2n contiguous
-    const uint16_t* w = p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n);
-    return rows_loader<BN>(w, 2 * p.a.n, nullptr, ti.n0, BN);
+    s.init(p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, nullptr, ti.n0, Cfg::BN);
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char*) {
-#pragma unroll
-    for (int i = 0; i < t.RM; ++i) {
-      const int m = t.m_of(i);
-      if (m >= ti.mrows) continue;
-      uint16_t* y = p.a.dXt + (size_t)(ti.row_base + m) * p.a.d + ti.n0;
-#pragma unroll
-      for (int j = 0; j < t.RN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c = t.n_of(j, g);
-          store_bf16x4(y + c, t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
-        }
-    }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
+    store_rows_bf16<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t);
   }
 };
 
 // ================================================================== weight gradients (varlen-K)
-template <int BM, int BN>
-__device__ __forceinline__ void store_weight_tile(uint16_t* out, int64_t ld, const TileInfo& ti, MfmaTile<BM, BN>& t) {
-#pragma unroll
-  for (int i = 0; i < t.RM; ++i) {
-    const int m = t.m_of(i);
-    uint16_t* y = out + (size_t)(ti.m0 + m) * ld + ti.n0;
-#pragma unroll
-    for (int j = 0; j < t.RN; ++j)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = t.n_of(j, g);
-        store_bf16x4(y + c, t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
-      }
-  }
-}
-
 // dW2_e[n,d] = A'_e^T gather(dO): M = n (A' columns), N = d (dO columns)
-template <int BM_, int BN_>
+template <class Cfg_>
 struct OpDW2 {
-  static constexpr int BM = BM_, BN = BN_, kMinBlocks = 1;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW2Args a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int*) { return tile_varlen_k<BM, BN>(p.a.offsets, p.a.n, p.a.d, ti); }
-  static __device__ KOuterLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return kouter_loader<BM>(p.a.Ap, p.a.n, ti.m0, p.a.n, nullptr, ti.k_begin, ti.k_len);
+  static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
+    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.n, p.a.d, ti);
   }
-  static __device__ KOuterLoader<BN> make_n(const Params& p, const TileInfo& ti) {
-    return kouter_loader<BN>(p.a.dO, p.a.d, ti.n0, p.a.d, p.a.row_token, ti.k_begin, ti.k_len);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
+    s.init(p.a.Ap, p.a.n, nullptr, ti.k_begin, ti.k_len, p.a.n, ColOffset{ti.m0});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char*) {
-    store_weight_tile<BM, BN>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti, t);
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+    s.init(p.a.dO, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.n0});
+  }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
+    store_rows_bf16<Cfg>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti.m0, Cfg::BM, ti.n0, t);
   }
 };
 
 // dW1_e[d,2n] = gather(X)_e^T dH_e: M = d (X columns), N = 2n (dH columns)
-template <int BM_, int BN_>
+template <class Cfg_>
 struct OpDW1 {
-  static constexpr int BM = BM_, BN = BN_, kMinBlocks = 1;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW1Args a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int*) { return tile_varlen_k<BM, BN>(p.a.offsets, p.a.d, 2 * p.a.n, ti); }
-  static __device__ KOuterLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return kouter_loader<BM>(p.a.X, p.a.d, ti.m0, p.a.d, p.a.row_token, ti.k_begin, ti.k_len);
+  static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
+    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.d, 2 * p.a.n, ti);
   }
-  static __device__ KOuterLoader<BN> make_n(const Params& p, const TileInfo& ti) {
-    return kouter_loader<BN>(p.a.dH, 2 * p.a.n, ti.n0, 2 * p.a.n, nullptr, ti.k_begin, ti.k_len);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
+    s.init(p.a.X, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.m0});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char*) {
-    store_weight_tile<BM, BN>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti, t);
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+    s.init(p.a.dH, 2 * p.a.n, nullptr, ti.k_begin, ti.k_len, 2 * p.a.n, ColOffset{ti.n0});
+  }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
+    store_rows_bf16<Cfg>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, Cfg::BM, ti.n0, t);
   }
 };
 
 // dW_r[d,E] = X^T dL, split over token chunks into fp32 partials
-template <int BN_>
+template <class Cfg_>
 struct OpDWr {
-  static constexpr int BM = 128, BN = BN_, kMinBlocks = BN_ >= 256 ? 1 : 2;
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DWrArgs a; };
   static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
-    const int mtn = p.a.d / BM, ntn = (p.a.E + BN - 1) / BN;
+    const int mtn = p.a.d / Cfg::BM, ntn = (p.a.E + Cfg::BN - 1) / Cfg::BN;
     const int id = blockIdx.x;
     const int split = id / (mtn * ntn), rem = id % (mtn * ntn);
     ti.e = split;
-    ti.m0 = (rem / ntn) * BM;
-    ti.n0 = (rem % ntn) * BN;
-    ti.mrows = BM;
+    ti.m0 = (rem / ntn) * Cfg::BM;
+    ti.n0 = (rem % ntn) * Cfg::BN;
+    ti.mrows = Cfg::BM;
     ti.row_base = 0;
     const int chunk = (((p.a.T + p.a.splits - 1) / p.a.splits) + kBK - 1) / kBK * kBK;
     ti.k_begin = split * chunk;
     ti.k_len = max(0, min(chunk, p.a.T - ti.k_begin));
     return true;
   }
-  static __device__ KOuterLoader<BM> make_m(const Params& p, const TileInfo& ti) {
-    return kouter_loader<BM>(p.a.X, p.a.d, ti.m0, p.a.d, nullptr, ti.k_begin, ti.k_len);
+  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
+    s.init(p.a.X, p.a.d, nullptr, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.m0});
   }
-  static __device__ KOuterLoader<BN> make_n(const Params& p, const TileInfo& ti) {
-    return kouter_loader<BN>(p.a.dL, p.a.E, ti.n0, p.a.E, nullptr, ti.k_begin, ti.k_len);
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+    s.init(p.a.dL, p.a.E, nullptr, ti.k_begin, ti.k_len, p.a.E, ColOffset{ti.n0});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, MfmaTile<BM, BN>& t, char*) {
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
     float* out = p.a.part + (size_t)ti.e * p.a.d * p.a.E;
 #pragma unroll
-    for (int i = 0; i < t.RM; ++i) {
+    for (int i = 0; i < Cfg::RM; ++i) {
       const int m = t.m_of(i);
       float* o = out + (size_t)(ti.m0 + m) * p.a.E;
 #pragma unroll
-      for (int j = 0; j < t.RN; ++j)
+      for (int j = 0; j < Cfg::RN; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int col = ti.n0 + t.n_of(j, g);
@@ -447,7 +415,7 @@ struct OpDWr {
 template <class Op>
 static hipError_t run(const typename Op::Params& p, int grid, hipStream_t s) {
   if (grid <= 0) return hipSuccess;
-  grouped_gemm_kernel<Op><<<dim3(grid), dim3(256), 0, s>>>(p);
+  grouped_gemm_kernel<Op><<<dim3(grid), dim3(kThreads), 0, s>>>(p);
   return hipGetLastError();
 }
 
@@ -455,72 +423,73 @@ static int pad8(int g) { return (g + 7) & ~7; }
 // upper bound of sum_e ceil(count_e / BM) given sum_e count_e <= capacity
 static int mtiles_bound(int capacity, int E, int BM) { return capacity / BM + E; }
 
+// tile configurations <BM, BN, WM, WN, STAGES>; varlen-M GEMMs use BM = 256
+using C256x256 = GemmCfg<256, 256, 2, 4, 2>;
+using C256x128 = GemmCfg<256, 128, 4, 2, 3>;
+using C256x64 = GemmCfg<256, 64, 8, 1, 3>;
+using C128x256 = GemmCfg<128, 256, 2, 4, 3>;
+using C128x128 = GemmCfg<128, 128, 4, 2, 3>;
+using C128x64 = GemmCfg<128, 64, 4, 2, 3>;
+
 hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
-  const int mt = (a.T + 127) / 128;
-  if (a.E <= 64) return run<OpRouter<64>>({a}, mt, s);
-  if (a.E <= 128) return run<OpRouter<128>>({a}, mt, s);
-  return run<OpRouter<256>>({a}, mt * ((a.E + 255) / 256), s);
+  const int mt = (a.T + 255) / 256;
+  if (a.E <= 64) return run<OpRouter<C256x64>>({a}, mt, s);
+  if (a.E <= 128) return run<OpRouter<C256x128>>({a}, mt, s);
+  return run<OpRouter<C256x256>>({a}, mt * ((a.E + 255) / 256), s);
 }
 
 hipError_t launch_up(const UpArgs& a, hipStream_t s) {
   const int N = 2 * a.n;
-  if (a.n % 128 == 0) {
-    constexpr int BM = 256, BN = 256;
-    return run<OpUp<BM, BN>>({a}, pad8(mtiles_bound(a.capacity, a.E, BM) * (N / BN)), s);
-  }
-  constexpr int BM = 128, BN = 128;  // n = 64
-  return run<OpUp<BM, BN>>({a}, pad8(mtiles_bound(a.capacity, a.E, BM) * (N / BN)), s);
+  if (a.n % 128 == 0) return run<OpUp<C256x256>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (N / 256)), s);
+  return run<OpUp<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (N / 128)), s);  // n % 64
 }
 
 hipError_t launch_down(const DownArgs& a, hipStream_t s) {
-  if (a.d % 256 == 0) {
-    constexpr int BM = 256, BN = 256;
-    return run<OpDown<BM, BN>>({a}, pad8(mtiles_bound(a.capacity, a.E, BM) * (a.d / BN)), s);
-  }
-  constexpr int BM = 128, BN = 128;
-  return run<OpDown<BM, BN>>({a}, pad8(mtiles_bound(a.capacity, a.E, BM) * (a.d / BN)), s);
+  if (a.d % 256 == 0) return run<OpDown<C256x256>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
+  return run<OpDown<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 128)), s);
 }
 
 static int dh_bn(int n) { return n % 256 == 0 ? 256 : (n % 128 == 0 ? 128 : 64); }
 int dh_n_tiles(int n) { return n / dh_bn(n); }
 
 hipError_t launch_dh(const DHArgs& a, hipStream_t s) {
-  constexpr int BM = 128;
-  const int grid = pad8(mtiles_bound(a.capacity, a.E, BM) * dh_n_tiles(a.n));
+  const int grid = pad8(mtiles_bound(a.capacity, a.E, 256) * dh_n_tiles(a.n));
   switch (dh_bn(a.n)) {
-    case 256: return run<OpDH<BM, 256>>({a}, grid, s);
-    case 128: return run<OpDH<BM, 128>>({a}, grid, s);
-    default: return run<OpDH<BM, 64>>({a}, grid, s);
+    case 256: return run<OpDH<C256x256>>({a}, grid, s);
+    case 128: return run<OpDH<C256x128>>({a}, grid, s);
+    default: return run<OpDH<C256x64>>({a}, grid, s);
   }
 }
 
 hipError_t launch_dxt(const DXtArgs& a, hipStream_t s) {
-  if (a.d % 256 == 0) {
-    constexpr int BM = 256, BN = 256;
-    return run<OpDXt<BM, BN>>({a}, pad8(mtiles_bound(a.capacity, a.E, BM) * (a.d / BN)), s);
-  }
-  constexpr int BM = 128, BN = 128;
-  return run<OpDXt<BM, BN>>({a}, pad8(mtiles_bound(a.capacity, a.E, BM) * (a.d / BN)), s);
+  if (a.d % 256 == 0) return run<OpDXt<C256x256>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
+  return run<OpDXt<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 128)), s);
 }
+
+// varlen-K GEMMs gather their k rows: two stages (the row indices of the next
+// stage are fetched one step ahead into registers)
+using W256x256 = GemmCfg<256, 256, 2, 4, 2>;
+using W128x256 = GemmCfg<128, 256, 2, 4, 2>;
+using W64x256 = GemmCfg<64, 256, 2, 4, 2>;
+using W128x128 = GemmCfg<128, 128, 4, 2, 2>;
+using W64x128 = GemmCfg<64, 128, 2, 4, 2>;
 
 hipError_t launch_dw2(const DW2Args& a, hipStream_t s) {
   // M = n, N = d
-  if (a.n % 128 == 0 && a.d % 256 == 0) {
-    constexpr int BM = 128, BN = 256;
-    return run<OpDW2<BM, BN>>({a}, pad8(a.E * (a.n / BM) * (a.d / BN)), s);
+  if (a.d % 256 == 0) {
+    if (a.n % 256 == 0) return run<OpDW2<W256x256>>({a}, pad8(a.E * (a.n / 256) * (a.d / 256)), s);
+    if (a.n % 128 == 0) return run<OpDW2<W128x256>>({a}, pad8(a.E * (a.n / 128) * (a.d / 256)), s);
+    return run<OpDW2<W64x256>>({a}, pad8(a.E * (a.n / 64) * (a.d / 256)), s);
   }
-  constexpr int BM = 64, BN = 128;
-  return run<OpDW2<BM, BN>>({a}, pad8(a.E * (a.n / BM) * (a.d / BN)), s);
+  if (a.n % 128 == 0) return run<OpDW2<W128x128>>({a}, pad8(a.E * (a.n / 128) * (a.d / 128)), s);
+  return run<OpDW2<W64x128>>({a}, pad8(a.E * (a.n / 64) * (a.d / 128)), s);
 }
 
 hipError_t launch_dw1(const DW1Args& a, hipStream_t s) {
   // M = d, N = 2n
-  if (a.d % 256 == 0 && (2 * a.n) % 256 == 0) {
-    constexpr int BM = 256, BN = 256;
-    return run<OpDW1<BM, BN>>({a}, pad8(a.E * (a.d / BM) * (2 * a.n / BN)), s);
-  }
-  constexpr int BM = 128, BN = 128;
-  return run<OpDW1<BM, BN>>({a}, pad8(a.E * (a.d / BM) * (2 * a.n / BN)), s);
+  if (a.d % 256 == 0 && (2 * a.n) % 256 == 0)
+    return run<OpDW1<W256x256>>({a}, pad8(a.E * (a.d / 256) * (2 * a.n / 256)), s);
+  return run<OpDW1<W128x128>>({a}, pad8(a.E * (a.d / 128) * (2 * a.n / 128)), s);
 }
 
 int dwr_splits(int T, int d, int E) {
@@ -535,11 +504,11 @@ hipError_t launch_dwr(const DWrArgs& a, hipStream_t s) {
   hipError_t err;
   const int mtn = a.d / 128;
   if (a.E <= 64)
-    err = run<OpDWr<64>>({a}, a.splits * mtn, s);
+    err = run<OpDWr<C128x64>>({a}, a.splits * mtn, s);
   else if (a.E <= 128)
-    err = run<OpDWr<128>>({a}, a.splits * mtn, s);
+    err = run<OpDWr<C128x128>>({a}, a.splits * mtn, s);
   else
-    err = run<OpDWr<256>>({a}, a.splits * mtn * ((a.E + 255) / 256), s);
+    err = run<OpDWr<C128x256>>({a}, a.splits * mtn * ((a.E + 255) / 256), s);
   if (err != hipSuccess) return err;
   return launch_reduce_rows(a.part, a.dWr, a.d * a.E, a.splits, s);
 }
