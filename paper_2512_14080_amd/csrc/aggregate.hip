@@ -11,25 +11,43 @@
 
 namespace smoe {
 
+constexpr int kAggBatch = 8;  // rows whose loads are in flight together
+constexpr int kColRows = 128;  // tokens per chunk of the dbias column sum
+
 // One wave per token; lanes cover 8 consecutive bf16 (16 bytes) of the row.
+// The token's rows are taken kAggBatch at a time: all their loads are issued
+// before any is accumulated, so a lane keeps several HBM reads in flight.
 __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__ Y, const int32_t* __restrict__ tok_offsets,
                                                     const int32_t* __restrict__ tok_rows, const float* __restrict__ row_w,
                                                     uint16_t* __restrict__ O, int T, int d) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // wave-uniform token: row indices and weights become scalar loads
+  const int t = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = lane_id();
   const int j0 = tok_offsets[t], j1 = tok_offsets[t + 1];
   for (int c = lane * 8; c < d; c += 512) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = j0; j < j1; ++j) {
-      const int r = tok_rows[j];
-      const float w = row_w[r];
-      const u32x4 v = *(const u32x4*)(Y + (size_t)r * d + c);
+    for (int jb = j0; jb < j1; jb += kAggBatch) {
+      u32x4 v[kAggBatch];
+      float w[kAggBatch];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc[2 * q] += w * bf_lo(v[q]);
-        acc[2 * q + 1] += w * bf_hi(v[q]);
+      for (int u = 0; u < kAggBatch; ++u) {
+        if (jb + u < j1) {
+          const int r = tok_rows[jb + u];
+          w[u] = row_w[r];
+          v[u] = *(const u32x4*)(Y + (size_t)r * d + c);
+        } else {
+          w[u] = 0.f;
+          v[u] = u32x4{0u, 0u, 0u, 0u};
+        }
       }
+#pragma unroll
+      for (int u = 0; u < kAggBatch; ++u)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[2 * q] += w[u] * bf_lo(v[u][q]);
+          acc[2 * q + 1] += w[u] * bf_hi(v[u][q]);
+        }
     }
     u32x4 o;
 #pragma unroll
@@ -47,7 +65,8 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
                                                      const int32_t* __restrict__ row_expert,
                                                      const float* __restrict__ row_w, uint16_t* __restrict__ dX,
                                                      uint16_t* __restrict__ dL, int T, int d, int E) {
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  // wave-uniform token: row indices and weights become scalar loads
+  const int t = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = lane_id();
   const int j0 = tok_offsets[t], j1 = tok_offsets[t + 1];
@@ -59,20 +78,23 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
     }
   for (int c = lane * 8; c < d; c += 512) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = j0; j < j1; ++j) {
-      const int r = tok_rows[j];
-      const u32x4 v = *(const u32x4*)(dXt + (size_t)r * d + c);
+    for (int jb = j0; jb < j1; jb += kAggBatch) {
+      u32x4 v[kAggBatch];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        acc[2 * q] += bf_lo(v[q]);
-        acc[2 * q + 1] += bf_hi(v[q]);
-      }
+      for (int u = 0; u < kAggBatch; ++u)
+        v[u] = (jb + u < j1) ? *(const u32x4*)(dXt + (size_t)tok_rows[jb + u] * d + c) : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int u = 0; u < kAggBatch; ++u)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[2 * q] += bf_lo(v[u][q]);
+          acc[2 * q + 1] += bf_hi(v[u][q]);
+        }
     }
     if (WrT) {
       for (int j = j0; j < j1; ++j) {
         const int r = tok_rows[j];
-        const float w = row_w[r];
-        const float dl = w * (dS[r] - g);
+        const float dl = row_w[r] * (dS[r] - g);
         const float* wr = WrT + (size_t)row_expert[r] * d + c;
         const f32x4 a = *(const f32x4*)wr;
         const f32x4 b = *(const f32x4*)(wr + 4);
@@ -129,13 +151,26 @@ __global__ __launch_bounds__(256) void transpose_wr_kernel(const uint16_t* __res
   WrT[idx] = bf2f(Wr[(size_t)i * E + e]);
 }
 
-// dbias[e] = sum_t dL[t][e], one block per expert, fixed reduction tree
-__global__ __launch_bounds__(256) void colsum_kernel(const uint16_t* __restrict__ dL, float* __restrict__ out, int T,
-                                                     int E) {
+// dbias[e] = sum_t dL[t][e] in two fixed-order passes: per chunk of
+// kColRows tokens a column sum (reads of a row are contiguous across the
+// block), then one block per expert reduces the chunk sums with a fixed tree.
+__global__ __launch_bounds__(128) void colsum_rows_kernel(const uint16_t* __restrict__ dL, float* __restrict__ part,
+                                                          int T, int E) {
+  const int r0 = blockIdx.x * kColRows, r1 = min(T, r0 + kColRows);
+  for (int c = threadIdx.x; c < E; c += 128) {
+    float s = 0.f;
+#pragma unroll 8
+    for (int r = r0; r < r1; ++r) s += bf2f(dL[(size_t)r * E + c]);
+    part[(size_t)blockIdx.x * E + c] = s;
+  }
+}
+
+__global__ __launch_bounds__(256) void colsum_parts_kernel(const float* __restrict__ part, float* __restrict__ out,
+                                                           int chunks, int E) {
   __shared__ float red[4];
   const int e = blockIdx.x;
   float s = 0.f;
-  for (int t = threadIdx.x; t < T; t += 256) s += bf2f(dL[(size_t)t * E + e]);
+  for (int i = threadIdx.x; i < chunks; i += 256) s += part[(size_t)i * E + e];
   s = wave_sum(s);
   if (lane_id() == 0) red[threadIdx.x >> 6] = s;
   __syncthreads();
@@ -169,8 +204,12 @@ hipError_t launch_transpose_wr(const uint16_t* Wr, float* WrT, int d, int E, hip
   return hipGetLastError();
 }
 
-hipError_t launch_colsum_bf16(const uint16_t* dL, float* dbias, int T, int E, hipStream_t s) {
-  colsum_kernel<<<dim3(E), dim3(256), 0, s>>>(dL, dbias, T, E);
+int colsum_chunks(int T) { return (T + kColRows - 1) / kColRows; }
+
+hipError_t launch_colsum_bf16(const uint16_t* dL, float* part, float* dbias, int T, int E, hipStream_t s) {
+  const int chunks = colsum_chunks(T);
+  if (chunks > 0) colsum_rows_kernel<<<dim3(chunks), dim3(128), 0, s>>>(dL, part, T, E);
+  colsum_parts_kernel<<<dim3(E), dim3(256), 0, s>>>(part, dbias, chunks, E);
   return hipGetLastError();
 }
 

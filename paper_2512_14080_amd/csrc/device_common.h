@@ -23,9 +23,15 @@ __device__ __forceinline__ uint16_t f2bf(float x) {
   __bf16 h = (__bf16)x;
   return __builtin_bit_cast(uint16_t, h);
 }
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+// two fp32 -> packed bf16 pair (one v_cvt_pk_bf16_f32, round to nearest even)
 __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
-  return uint32_t(f2bf(lo)) | (uint32_t(f2bf(hi)) << 16);
+  const f32x2v v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
 }
+// logistic sigmoid with the hardware exp and reciprocal (about 1 ulp each)
+__device__ __forceinline__ float fast_sigmoid(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
@@ -53,6 +59,15 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
     if (l >= o) v += t;
   }
   return v;
+}
+
+// 64-bit value of lane l (wave-uniform l).  The readlane builtin works on
+// 32-bit ints: given a 64-bit argument it keeps only the sign-extended low
+// half, so the two halves are read separately.
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+  return ((uint64_t)hi << 32) | lo;
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt() {

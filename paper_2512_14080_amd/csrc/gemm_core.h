@@ -87,33 +87,39 @@ struct GemmCfg {
 };
 
 // ---------------------------------------------------------------- ROWS side
-// LDS: [R][64] bf16, chunk c of row r at r*128 + ((c ^ (r & 7)) << 4).
+// LDS: [R][64] bf16, chunk c of row r at r*128 + ((c ^ ((r >> 1) & 7)) << 4).
+// A fragment read (32 rows, one chunk each) then hits every bank once per
+// 16 lanes: even and odd rows fall in different bank halves and the eight
+// rows of each parity get eight different chunk slots.
 // DMA instruction q covers rows 8q..8q+7; lane l -> row 8q + l/8, physical
-// chunk l%8, logical chunk (l%8) ^ (l/8).
+// chunk l%8, logical chunk (l%8) ^ ((row >> 1) & 7).
 template <int R>
 struct RowsSide {
   static constexpr int Q = R / 64;  // instructions per wave
   const char* ptr[Q];               // row start (k = 0) of the row this lane loads, per instruction
   __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, const int32_t* idx, int row_base, int nrows) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int logical = (lane & 7) ^ (lane >> 3);
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
       const int q = wave + kWaves * j;
-      const int r = min(8 * q + (lane >> 3), nrows - 1);
+      const int lrow = 8 * q + (lane >> 3);
+      const int logical = (lane & 7) ^ ((lrow >> 1) & 7);
+      const int r = min(lrow, nrows - 1);
       const int64_t row = idx ? (int64_t)idx[row_base + r] : (int64_t)(row_base + r);
       ptr[j] = (const char*)(base + row * ld) + logical * 16;
     }
   }
-  __device__ __forceinline__ void issue(uint32_t lds_side, int k0) const {
+  // instructions j with j % parts == part (so a stage can be issued in pieces)
+  __device__ __forceinline__ void issue(uint32_t lds_side, int k0, int part = 0, int parts = 1) const {
     const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
-    for (int j = 0; j < Q; ++j) dma16(ptr[j] + k0 * 2, lds_side + (w + kWaves * j) * 1024);
+    for (int j = 0; j < Q; ++j)
+      if (j % parts == part) dma16(ptr[j] + k0 * 2, lds_side + (w + kWaves * j) * 1024);
   }
   static __device__ __forceinline__ bf16x8 frag(const char* lds_side, int r0, int s) {
     const int lane = threadIdx.x & 63;
     const int row = r0 + (lane & 31);
-    const int c = (2 * s + (lane >> 5)) ^ (row & 7);
+    const int c = (2 * s + (lane >> 5)) ^ ((row >> 1) & 7);
     return *(const bf16x8*)(lds_side + row * 128 + c * 16);
   }
 };
@@ -175,11 +181,12 @@ struct KOuterSide {
 #pragma unroll
     for (int j = 0; j < Q; ++j) asm volatile("" ::"v"(gnext[j]));
   }
-  __device__ __forceinline__ void issue(uint32_t lds_side, int k0) const {
+  __device__ __forceinline__ void issue(uint32_t lds_side, int k0, int part = 0, int parts = 1) const {
     const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
+      if (j % parts != part) continue;
       const int k = k0 + krow[j];
       const char* src;
       if (k < k_len && colb[j] >= 0) {
@@ -357,30 +364,45 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typenam
         wait_vm_barrier<0>();
       }
       const int knext = kt + S - 1;
-      if (knext < nk) {
-        const uint32_t st = lds0 + (knext % S) * Cfg::STAGE_BYTES;
+      const bool issue_next = knext < nk;
+      const uint32_t st_next = lds0 + (knext % S) * Cfg::STAGE_BYTES;
+      if (issue_next) {
         if constexpr (Op::M_MODE == KOUTER) ms.idx_ready();
         if constexpr (Op::N_MODE == KOUTER) ns.idx_ready();
-        ms.issue(st, knext * kBK);
-        ns.issue(st + Cfg::M_BYTES, knext * kBK);
-        if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * kBK);
-        if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * kBK);
       }
       const char* cur = smem + (kt % S) * Cfg::STAGE_BYTES;
       const char* lm = cur;
       const char* ln = cur + Cfg::M_BYTES;
+      // fragments of sub-step s+1 are read while the MFMAs of sub-step s issue
+      bf16x8 fm[2][Cfg::RM], fn[2][Cfg::RN];
+#pragma unroll
+      for (int i = 0; i < Cfg::RM; ++i) fm[0][i] = SideT<Op::M_MODE, BM>::type::frag(lm, wm0 + 32 * i, 0);
+#pragma unroll
+      for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = SideT<Op::N_MODE, BN>::type::frag(ln, wn0 + 32 * j, 0);
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        bf16x8 fm[Cfg::RM], fn[Cfg::RN];
+        // the next stage's DMA is spread over the four sub-steps so the
+        // vector-memory issue does not stall the MFMA stream in one burst
+        if (issue_next) {
+          ms.issue(st_next, knext * kBK, s, 4);
+          ns.issue(st_next + Cfg::M_BYTES, knext * kBK, s, 4);
+        }
+        const int cb = s & 1, nb = cb ^ 1;
+        if (s + 1 < 4) {
 #pragma unroll
-        for (int i = 0; i < Cfg::RM; ++i) fm[i] = SideT<Op::M_MODE, BM>::type::frag(lm, wm0 + 32 * i, s);
+          for (int i = 0; i < Cfg::RM; ++i) fm[nb][i] = SideT<Op::M_MODE, BM>::type::frag(lm, wm0 + 32 * i, s + 1);
 #pragma unroll
-        for (int j = 0; j < Cfg::RN; ++j) fn[j] = SideT<Op::N_MODE, BN>::type::frag(ln, wn0 + 32 * j, s);
+          for (int j = 0; j < Cfg::RN; ++j) fn[nb][j] = SideT<Op::N_MODE, BN>::type::frag(ln, wn0 + 32 * j, s + 1);
+        }
 #pragma unroll
         for (int i = 0; i < Cfg::RM; ++i)
 #pragma unroll
           for (int j = 0; j < Cfg::RN; ++j)
-            acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc.acc[i][j], 0, 0, 0);
+            acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[cb][j], fm[cb][i], acc.acc[i][j], 0, 0, 0);
+      }
+      if (issue_next) {
+        if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * kBK);
+        if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * kBK);
       }
     }
     barrier_lds();  // every wave done with the LDS stages before the epilogue reuses them

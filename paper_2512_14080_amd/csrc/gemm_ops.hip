@@ -15,7 +15,7 @@
 namespace smoe {
 
 __device__ __forceinline__ float silu_sig(float g, float* sig) {
-  const float s = 1.f / (1.f + __expf(-g));
+  const float s = fast_sigmoid(g);
   *sig = s;
   return g * s;
 }
@@ -243,29 +243,53 @@ struct OpDH {
     s.init(p.a.W2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, nullptr, ti.n0, Cfg::BN);
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* smem) {
+    constexpr int RM = Cfg::RM, RN = Cfg::RN;
     const int n = p.a.n;
     const int lane = threadIdx.x & 63;
     const int wn = t.wave_n();
     float* red = (float*)smem;  // [BM][WN]
+    // H values of one accumulator row block (gate and up halves) and the
+    // row's routing score, double-buffered: the loads of block i+1 are in
+    // flight while block i is computed and stored.
+    u32x2 hg[2][RN][4], hu[2][RN][4];
+    float sw[2];
+    auto load_block = [&](int i, int b) {
+      const int m = t.m_of(i);
+      const size_t row = (size_t)(ti.row_base + (m < ti.mrows ? m : 0));
+      const uint16_t* h = p.a.H + row * (2 * n);
+      sw[b] = p.a.row_w[row];
 #pragma unroll
-    for (int i = 0; i < Cfg::RM; ++i) {
+      for (int j = 0; j < RN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int col = ti.n0 + t.n_of(j, g);
+          hg[b][j][g] = *(const u32x2*)(h + col);
+          hu[b][j][g] = *(const u32x2*)(h + n + col);
+        }
+    };
+    load_block(0, 0);
+#pragma unroll
+    for (int i = 0; i < RM; ++i) {
+      const int b = i & 1;
+      if (i + 1 < RM) load_block(i + 1, b ^ 1);
       const int m = t.m_of(i);
       const bool valid = m < ti.mrows;
       const size_t row = (size_t)(ti.row_base + (valid ? m : 0));
-      const float s = valid ? p.a.row_w[row] : 0.f;
-      const uint16_t* h = p.a.H + row * (2 * n);
+      const float s = valid ? sw[b] : 0.f;
       uint16_t* dh = p.a.dH + row * (2 * n);
       uint16_t* ap = p.a.Ap + row * n;
       float part = 0.f;
       if (valid) {
 #pragma unroll
-        for (int j = 0; j < Cfg::RN; ++j)
+        for (int j = 0; j < RN; ++j)
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int col = ti.n0 + t.n_of(j, g);
-            float gv[4], uv[4], dg[4], du[4], apv[4];
-            load_bf16x4(h + col, gv);
-            load_bf16x4(h + n + col, uv);
+            const float gv[4] = {bf_lo(hg[b][j][g][0]), bf_hi(hg[b][j][g][0]), bf_lo(hg[b][j][g][1]),
+                                 bf_hi(hg[b][j][g][1])};
+            const float uv[4] = {bf_lo(hu[b][j][g][0]), bf_hi(hu[b][j][g][0]), bf_lo(hu[b][j][g][1]),
+                                 bf_hi(hu[b][j][g][1])};
+            float dg[4], du[4], apv[4];
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
               const float dap = t.acc[i][j][4 * g + r];

@@ -9,10 +9,10 @@
 namespace smoe {
 
 // routing
-hipError_t launch_softmax_topk(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
-                               int T, int E, int K, int do_softmax, hipStream_t s);
-hipError_t launch_build_mask(const int32_t* topk_idx, uint64_t* mask, int T, int E, int K, int W, hipStream_t s);
-hipError_t launch_metadata(const moe_routing& r, const float* scores, int T, int E, hipStream_t s);
+hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
+                             uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s);
+hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, hipStream_t s);
+hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, hipStream_t s);
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
                         hipStream_t s);
 
@@ -70,7 +70,9 @@ hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const float* WrT,
 hipError_t launch_reduce_rows(const float* part, float* out, int rows, int parts, hipStream_t s);
 hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s);
 hipError_t launch_transpose_wr(const uint16_t* Wr, float* WrT, int d, int E, hipStream_t s);
-hipError_t launch_colsum_bf16(const uint16_t* dL, float* dbias, int T, int E, hipStream_t s);
+// dbias = column sums of dL [T][E]; part holds colsum_chunks(T) * E floats
+int colsum_chunks(int T);
+hipError_t launch_colsum_bf16(const uint16_t* dL, float* part, float* dbias, int T, int E, hipStream_t s);
 
 // timing hooks (moe_abi.cpp)
 void prof_begin(int kernel_class, hipStream_t s);

@@ -86,6 +86,7 @@ struct BwdWs {
   uint16_t* dL;
   float* WrT;
   float* dWr_part;
+  float* dbias_part;
 };
 
 size_t carve(char* base, size_t off, size_t bytes, void** out) {
@@ -112,6 +113,7 @@ size_t bwd_layout(const moe_dims& m, int64_t cap, char* base, BwdWs* w) {
   off = carve(base, off, (size_t)m.T * m.E * 2, w ? (void**)&w->dL : nullptr);
   off = carve(base, off, (size_t)m.E * m.d * 4, w ? (void**)&w->WrT : nullptr);
   off = carve(base, off, (size_t)splits * m.d * m.E * 4, w ? (void**)&w->dWr_part : nullptr);
+  off = carve(base, off, (size_t)smoe::colsum_chunks(m.T) * m.E * 4, w ? (void**)&w->dbias_part : nullptr);
   return off;
 }
 
@@ -259,7 +261,7 @@ int moe_route(moe_dims m, const moe_bf16* X, const moe_bf16* Wr, const float* bi
   if (rc) return rc;
   rc = check_routing(m, r, (int64_t)m.T * m.K, "r");
   if (rc) return rc;
-  if (!r->topk_idx) return fail(MOE_ERR_INVALID_ARG, "r->topk_idx must not be null");
+  if (!r->topk_idx || !r->topk_w) return fail(MOE_ERR_INVALID_ARG, "r->topk_idx and r->topk_w must not be null");
   const bool scores_in = flags & MOE_ROUTE_SCORES_IN;
   if (!scores_in) {
     CHECK_PTR(X, 16);
@@ -274,23 +276,18 @@ int moe_route(moe_dims m, const moe_bf16* X, const moe_bf16* Wr, const float* bi
     return fail(MOE_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
   hipStream_t stream = (hipStream_t)stream_;
   float* scores_t = (flags & MOE_ROUTE_WRITE_SCORES_T) ? r->scores_t : nullptr;
+  const float* in = r->scores;
   if (!scores_in) {
     float* logits = (flags & MOE_ROUTE_WRITE_LOGITS) ? r->logits : r->scores;
     smoe::RouterGemmArgs a{X, Wr, bias, logits, m.T, m.d, m.E};
     LAUNCH(MOE_KC_ROUTER_GEMM, smoe::launch_router_gemm(a, stream), "router gemm");
-    LAUNCH(MOE_KC_TOPK,
-           smoe::launch_softmax_topk(logits, r->scores, scores_t, r->topk_idx, r->topk_w, m.T, m.E, m.K, 1, stream),
-           "softmax/top-K");
-  } else {
-    LAUNCH(MOE_KC_TOPK,
-           smoe::launch_softmax_topk(r->scores, r->scores, scores_t, r->topk_idx, r->topk_w, m.T, m.E, m.K, 0, stream),
-           "top-K");
+    in = logits;
   }
-  smoe::prof_begin(MOE_KC_META, stream);
-  hipError_t e = smoe::launch_build_mask(r->topk_idx, r->mask, m.T, m.E, m.K, r->words, stream);
-  if (e == hipSuccess) e = smoe::launch_metadata(*r, r->scores, m.T, m.E, stream);
-  smoe::prof_end(MOE_KC_META, stream);
-  if (e != hipSuccess) return hip_fail(e, "routing metadata");
+  LAUNCH(MOE_KC_TOPK,
+         smoe::launch_topk_route(in, r->scores, scores_t, r->topk_idx, r->topk_w, r->mask, m.T, m.E, m.K, r->words,
+                                 scores_in ? 0 : 1, stream),
+         "softmax/top-K");
+  LAUNCH(MOE_KC_META, smoe::launch_tc_metadata(*r, m.T, m.E, m.K, stream), "routing metadata");
   return MOE_OK;
 }
 
@@ -311,7 +308,7 @@ int moe_round_tokens(moe_dims m, int32_t m_tile, int mode, const float* u, const
   hipStream_t stream = (hipStream_t)stream_;
   smoe::prof_begin(MOE_KC_ROUND, stream);
   hipError_t e = smoe::launch_round(*tc, *tr, u, m.T, m.E, m_tile, mode, stream);
-  if (e == hipSuccess) e = smoe::launch_metadata(*tr, tc->scores, m.T, m.E, stream);
+  if (e == hipSuccess) e = smoe::launch_metadata(*tr, tc->scores_t, m.T, m.E, stream);
   smoe::prof_end(MOE_KC_ROUND, stream);
   if (e != hipSuccess) return hip_fail(e, "token rounding");
   return MOE_OK;
@@ -386,7 +383,7 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
     const int splits = smoe::dwr_splits(m.T, m.d, m.E);
     LAUNCH(MOE_KC_DWR, smoe::launch_dwr({X, w.dL, w.dWr_part, dWr, m.T, m.d, m.E, splits}, stream), "dW_r");
   }
-  if (dbias) HIP_TRY(smoe::launch_colsum_bf16(w.dL, dbias, m.T, m.E, stream), "dbias");
+  if (dbias) HIP_TRY(smoe::launch_colsum_bf16(w.dL, w.dbias_part, dbias, m.T, m.E, stream), "dbias");
   return MOE_OK;
 }
 

@@ -4,7 +4,7 @@
 // The paper describes the method as a two-step sort (TC top-K, then a sort of
 // each expert's tokens by router score with TC tokens preferred).  Only the
 // last tile changes, so instead of sorting all T tokens per expert this code
-// selects the at most m_tile-1 tokens that change with a 4-pass 8-bit radix
+// selects the at most m_tile-1 tokens that change with a bitwise (32-pass)
 // select on an order-preserving integer image of the fp32 score, then breaks
 // ties on the threshold value by token index.  The result is the same set the
 // full sort would give.
@@ -72,14 +72,19 @@ constexpr int kSelThreads = 1024;
 //   drop (dir < 0): the need worst TC tokens by (score asc, token desc).
 // Both become "the need largest keys" with key = score_key for pads and
 // ~score_key for drops, ties preferring low tokens for pads, high for drops.
+//
+// Token t is owned by thread t % 1024 as its slot t / 1024.  With KPT > 0 the
+// block holds all T <= 1024*KPT keys in registers (read once; KPT <= 32 keeps
+// them within the 128 VGPRs a 1024-thread block allows); KPT == 0 is the
+// any-T form that re-reads the scores from memory on every pass.
+template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* __restrict__ tc_mask,
                                                                 uint64_t* __restrict__ tr_mask,
                                                                 const float* __restrict__ scores_t,
                                                                 const int32_t* __restrict__ round_dir,
                                                                 const int32_t* __restrict__ need_arr, int T, int W) {
-  __shared__ int hist[256];
-  __shared__ int sh[4];
-  __shared__ int lds[16];
+  constexpr int kWaves = kSelThreads / 64;
+  __shared__ int lds[kWaves];
   const int e = blockIdx.x;
   const uint64_t* src = tc_mask + (size_t)e * W;
   uint64_t* dst = tr_mask + (size_t)e * W;
@@ -91,82 +96,123 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
   }
   const float* S = scores_t + (size_t)e * T;
   const bool want_set = dir < 0;  // candidates: TC tokens for drops, non-TC for pads
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int slots = (T + kSelThreads - 1) / kSelThreads;
+
+  // key of slot i of this thread; cand tells whether the token is a candidate
+  auto load_key = [&](int i, bool& cand) -> uint32_t {
+    const int t = i * kSelThreads + threadIdx.x;
+    cand = false;
+    if (t >= T) return 0u;
+    cand = (((src[t >> 6] >> (t & 63)) & 1ull) != 0) == want_set;
+    if (!cand) return 0u;
+    const uint32_t k = score_key(S[t]);
+    return dir < 0 ? ~k : k;
+  };
+  uint32_t keys[KPT > 0 ? KPT : 1];
+  uint64_t cmask = 0;
+  if constexpr (KPT > 0) {
+    // scores and mask words are requested 16 slots at a time before any is used
+    constexpr int kBatch = KPT < 16 ? KPT : 16;
+#pragma unroll
+    for (int i0 = 0; i0 < KPT; i0 += kBatch) {
+      uint64_t words[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = i0 + u;
+        const int t = i * kSelThreads + threadIdx.x;
+        const int w = __builtin_amdgcn_readfirstlane(i * kWaves + wave);  // the wave's word: a scalar load
+        keys[i] = t < T ? __float_as_uint(S[t]) : 0u;
+        words[u] = w < W ? src[w] : 0ull;
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = i0 + u;
+        const int t = i * kSelThreads + threadIdx.x;
+        const bool c = t < T && ((((words[u] >> lane) & 1ull) != 0) == want_set);
+        const uint32_t k = score_key(__uint_as_float(keys[i]));
+        keys[i] = c ? (dir < 0 ? ~k : k) : 0u;
+        cmask |= (uint64_t)c << i;
+      }
+      asm volatile("" ::: "memory");  // keep the next batch's loads after this one
+    }
+  }
+  // number of candidates in the block whose key k has (k >> sh) == v
+  auto count_eq = [&](uint32_t v, int sh) -> int {
+    int cnt = 0;
+    if constexpr (KPT > 0) {
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) cnt += __popcll(__ballot(((cmask >> i) & 1ull) && (keys[i] >> sh) == v));
+    } else {
+      for (int i = 0; i < slots; ++i) {
+        bool c;
+        const uint32_t k = load_key(i, c);
+        cnt += __popcll(__ballot(c && (k >> sh) == v));
+      }
+    }
+    if (lane == 0) lds[wave] = cnt;
+    __syncthreads();
+    int total = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) total += lds[q];
+    __syncthreads();
+    return total;
+  };
+
+  // Bitwise select (MSB first) of tau, the need-th largest candidate key:
+  // keep a bit set when the candidates extending the prefix with a 1 still
+  // hold `remaining` keys, else count them as taken and clear it.
   uint32_t prefix = 0;
   int remaining = need;
-  for (int pass = 3; pass >= 0; --pass) {
-    for (int i = threadIdx.x; i < 256; i += kSelThreads) hist[i] = 0;
-    __syncthreads();
-    const int sh_hi = 8 * (pass + 1);
-    for (int t = threadIdx.x; t < T; t += kSelThreads) {
-      const bool in_tc = (src[t >> 6] >> (t & 63)) & 1ull;
-      if (in_tc != want_set) continue;
-      uint32_t k = score_key(S[t]);
-      if (dir < 0) k = ~k;
-      if (pass == 3 || (k >> sh_hi) == prefix) atomicAdd(&hist[(k >> (8 * pass)) & 255], 1);
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      int cum = 0, dsel = 0;
-      for (int dgt = 255; dgt >= 0; --dgt) {
-        if (cum + hist[dgt] >= remaining) {
-          dsel = dgt;
-          break;
-        }
-        cum += hist[dgt];
-      }
-      sh[0] = dsel;
-      sh[1] = remaining - cum;
-    }
-    __syncthreads();
-    prefix = (prefix << 8) | (uint32_t)sh[0];
-    remaining = sh[1];
-    __syncthreads();
+  for (int bit = 31; bit >= 0; --bit) {
+    const int total = count_eq((prefix >> bit) | 1u, bit);
+    if (total >= remaining)
+      prefix |= 1u << bit;
+    else
+      remaining -= total;
   }
   const uint32_t tau = prefix;
-  // marking pass over words, in preferred token order (ascending for pads,
-  // descending for drops); ties on tau are taken until `remaining` are used
+  const int nties = count_eq(tau, 0);
+
+  // Marking pass in ascending token order: slot i of wave w is word 16i + w.
+  // Every candidate with key > tau flips; of the nties ties on tau, the
+  // `remaining` first ones flip for pads and the last ones for drops.  A
+  // tie's ascending rank comes from ballots, a scan over the waves and a
+  // carry over slots.
+  const int first_tie = dir > 0 ? 0 : nties - remaining;
+  const int last_tie = dir > 0 ? remaining : nties;  // flip ranks in [first_tie, last_tie)
   int carry = 0;
-  for (int c0 = 0; c0 < W; c0 += kSelThreads) {
-    const int idx = c0 + threadIdx.x;
-    const int w = dir > 0 ? idx : W - 1 - idx;
-    uint64_t word = 0;
-    int ties = 0;
-    const bool valid = idx < W;
-    if (valid) {
-      word = src[w];
-      for (int b = 0; b < 64; ++b) {
-        const int t = w * 64 + b;
-        if (t >= T) break;
-        const bool in_tc = (word >> b) & 1ull;
-        if (in_tc != want_set) continue;
-        uint32_t k = score_key(S[t]);
-        if (dir < 0) k = ~k;
-        ties += (k == tau);
-      }
+  auto mark = [&](int i, bool cand, uint32_t k) {
+    const int w = i * kWaves + wave;
+    const bool gt = cand && k > tau;
+    const bool tie = cand && k == tau;
+    const uint64_t ties = __ballot(tie);
+    if (lane == 0) lds[wave] = __popcll(ties);
+    __syncthreads();
+    int base = carry, total = 0;
+#pragma unroll
+    for (int q = 0; q < kWaves; ++q) {
+      const int c = lds[q];
+      if (q < wave) base += c;
+      total += c;
     }
-    int total;
-    const int before = carry + block_excl_scan<kSelThreads>(ties, &total, lds);
-    if (valid) {
-      uint64_t out = word;
-      int rank = before;
-      for (int bb = 0; bb < 64; ++bb) {
-        const int b = dir > 0 ? bb : 63 - bb;
-        const int t = w * 64 + b;
-        if (t >= T) continue;
-        const bool in_tc = (word >> b) & 1ull;
-        if (in_tc != want_set) continue;
-        uint32_t k = score_key(S[t]);
-        if (dir < 0) k = ~k;
-        bool flip = k > tau;
-        if (k == tau) {
-          flip = rank < remaining;
-          ++rank;
-        }
-        if (flip) out ^= (1ull << b);
-      }
-      dst[w] = out;
-    }
+    const int rank = base + __popcll(ties & lanemask_lt());
+    const bool flip = gt || (tie && rank >= first_tie && rank < last_tie);
+    const uint64_t flips = __ballot(flip);
+    if (w < W && lane == 0) dst[w] = src[w] ^ flips;
     carry += total;
+    __syncthreads();
+  };
+  if constexpr (KPT > 0) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i)
+      if (i < slots) mark(i, (cmask >> i) & 1ull, keys[i]);
+  } else {
+    for (int i = 0; i < slots; ++i) {
+      bool c;
+      const uint32_t k = load_key(i, c);
+      mark(i, c, k);
+    }
   }
 }
 
@@ -174,8 +220,18 @@ hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, 
                         hipStream_t s) {
   int32_t* need = tr.scratch;
   tr_decide_kernel<<<dim3(1), dim3(256), 0, s>>>(tc.counts, u, tr.round_dir, need, T, E, M, mode);
-  tr_select_kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, T,
-                                                         tr.words);
+  const int slots = (T + kSelThreads - 1) / kSelThreads;
+  auto select = [&](auto kernel) {
+    kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, T, tr.words);
+  };
+  if (slots <= 4)
+    select(tr_select_kernel<4>);
+  else if (slots <= 16)
+    select(tr_select_kernel<16>);
+  else if (slots <= 32)
+    select(tr_select_kernel<32>);
+  else
+    select(tr_select_kernel<0>);
   return hipGetLastError();
 }
 

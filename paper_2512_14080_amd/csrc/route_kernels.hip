@@ -6,147 +6,148 @@
 // the top-K kernel in Appendix D (equal scores go to the lower expert index).
 // Unlike that kernel, the expert index is not packed into the low mantissa
 // bits: the comparison uses the exact (score, index) pair, so no score is
-// perturbed.  One wave64 handles one token; the K winners are found by K
-// rounds of a wave-wide arg-max over (score desc, index asc).
+// perturbed.  One wave64 handles one token at a time; the K winners are found
+// by K rounds of a wave-wide arg-max over (score desc, index asc).  A
+// workgroup owns 64 consecutive tokens, i.e. one 64-bit word of every
+// expert's membership bitmap, which it assembles in LDS.
 #include "device_common.h"
 #include "launch.h"
 
 namespace smoe {
 
-template <int EPL>
-// `in` and `scores` may alias (logits overwritten in place by the scores).
-__global__ __launch_bounds__(256) void softmax_topk_kernel(const float* in, float* scores,
-                                                           float* __restrict__ scores_t, int32_t* __restrict__ topk_idx,
-                                                           float* __restrict__ topk_w, int T, int E, int K,
-                                                           int do_softmax) {
-  const int wave = threadIdx.x >> 6;
+constexpr int kTopkWaves = 16;
+
+// Workgroup = 64 tokens (one membership word).  `in` and `scores` may alias
+// (logits overwritten in place by the scores).  With STASH, the scores are
+// staged in LDS and written transposed (scores_t[e][t]) in 64-token runs.
+template <int EPL, bool STASH>
+__global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float* scores, float* __restrict__ scores_t,
+                                                         int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
+                                                         uint64_t* __restrict__ mask, int T, int E, int K, int W,
+                                                         int do_softmax) {
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
+  unsigned long long* mword = (unsigned long long*)dyn;      // [E]
+  float* st = (float*)(dyn + ((E * 8 + 15) & ~15));           // [E][64] when STASH
+  const int w = blockIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = lane_id();
-  const int t = blockIdx.x * 4 + wave;
-  if (t >= T) return;
-  const float* row = in + (size_t)t * E;
-  float v[EPL];
-#pragma unroll
-  for (int j = 0; j < EPL; ++j) {
-    const int e = lane + 64 * j;
-    v[j] = e < E ? row[e] : -INFINITY;
-  }
-  if (do_softmax) {
-    float m = -INFINITY;
-#pragma unroll
-    for (int j = 0; j < EPL; ++j) m = fmaxf(m, v[j]);
-    m = wave_max(m);
-    float s = 0.f;
+  for (int e = threadIdx.x; e < E; e += kTopkWaves * 64) mword[e] = 0ull;
+  __syncthreads();
+  for (int i = wave; i < 64; i += kTopkWaves) {
+    const int t = w * 64 + i;
+    if (t >= T) break;
+    const float* row = in + (size_t)t * E;
+    float v[EPL];
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
       const int e = lane + 64 * j;
-      v[j] = e < E ? expf(v[j] - m) : 0.f;
-      s += v[j];
+      v[j] = e < E ? row[e] : -INFINITY;
     }
-    s = wave_sum(s);
+    if (do_softmax) {
+      float m = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < EPL; ++j) {
-      const int e = lane + 64 * j;
-      if (e < E) {
-        v[j] = v[j] / s;
-        scores[(size_t)t * E + e] = v[j];
-      }
-    }
-  }
-  if (scores_t) {
-#pragma unroll
-    for (int j = 0; j < EPL; ++j) {
-      const int e = lane + 64 * j;
-      if (e < E) scores_t[(size_t)e * T + t] = v[j];
-    }
-  }
-  // K rounds of wave arg-max over (value desc, expert asc)
-  uint32_t taken = 0;
-  int sel_e[16];
-  float sel_v[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) {
-    sel_e[k] = 0;
-    sel_v[k] = 0.f;
-    if (k < K) {
-      float bv = -INFINITY;
-      int be = 0x7fffffff;
+      for (int j = 0; j < EPL; ++j) m = fmaxf(m, v[j]);
+      m = wave_max(m);
+      float s = 0.f;
 #pragma unroll
       for (int j = 0; j < EPL; ++j) {
         const int e = lane + 64 * j;
-        if (e < E && !((taken >> j) & 1u)) {
-          if (be == 0x7fffffff || v[j] > bv || (v[j] == bv && e < be)) {
-            bv = v[j];
-            be = e;
+        v[j] = e < E ? expf(v[j] - m) : 0.f;
+        s += v[j];
+      }
+      s = wave_sum(s);
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) {
+        const int e = lane + 64 * j;
+        if (e < E) {
+          v[j] = v[j] / s;
+          scores[(size_t)t * E + e] = v[j];
+        }
+      }
+    }
+    if (scores_t) {
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) {
+        const int e = lane + 64 * j;
+        if (e < E) {
+          if (STASH)
+            st[e * 64 + i] = v[j];
+          else
+            scores_t[(size_t)e * T + t] = v[j];
+        }
+      }
+    }
+    // K rounds of wave arg-max over (value desc, expert asc)
+    uint32_t taken = 0;
+    int sel_e[16];
+    float sel_v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      sel_e[k] = 0;
+      sel_v[k] = 0.f;
+      if (k < K) {
+        float bv = -INFINITY;
+        int be = 0x7fffffff;
+#pragma unroll
+        for (int j = 0; j < EPL; ++j) {
+          const int e = lane + 64 * j;
+          if (e < E && !((taken >> j) & 1u)) {
+            if (be == 0x7fffffff || v[j] > bv || (v[j] == bv && e < be)) {
+              bv = v[j];
+              be = e;
+            }
           }
         }
-      }
 #pragma unroll
-      for (int o = 32; o > 0; o >>= 1) {
-        const float ov = __shfl_xor(bv, o, kWave);
-        const int oe = __shfl_xor(be, o, kWave);
-        // candidates without a valid expert carry index INT_MAX and lose
-        const bool better = (oe != 0x7fffffff) && (be == 0x7fffffff || ov > bv || (ov == bv && oe < be));
-        if (better) {
-          bv = ov;
-          be = oe;
+        for (int o = 32; o > 0; o >>= 1) {
+          const float ov = __shfl_xor(bv, o, kWave);
+          const int oe = __shfl_xor(be, o, kWave);
+          // candidates without a valid expert carry index INT_MAX and lose
+          const bool better = (oe != 0x7fffffff) && (be == 0x7fffffff || ov > bv || (ov == bv && oe < be));
+          if (better) {
+            bv = ov;
+            be = oe;
+          }
         }
+        if ((be & 63) == lane) taken |= 1u << (be >> 6);
+        sel_e[k] = be;
+        sel_v[k] = bv;
       }
-      if ((be & 63) == lane) taken |= 1u << (be >> 6);
-      sel_e[k] = be;
-      sel_v[k] = bv;
+    }
+    // renormalisation denominator: selected scores summed in ascending expert order
+    float denom = 0.f;
+    int last = -1;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      if (r < K) {
+        int nxt = 0x7fffffff;
+        float nv = 0.f;
+#pragma unroll
+        for (int k = 0; k < 16; ++k)
+          if (k < K && sel_e[k] > last && sel_e[k] < nxt) {
+            nxt = sel_e[k];
+            nv = sel_v[k];
+          }
+        denom += nv;
+        last = nxt;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      if (k < K && lane == k) {
+        topk_idx[(size_t)t * K + k] = sel_e[k];
+        topk_w[(size_t)t * K + k] = sel_v[k] / denom;
+        atomicOr(&mword[sel_e[k]], 1ull << i);
+      }
     }
   }
-  // renormalisation denominator: selected scores summed in ascending expert order
-  float denom = 0.f;
-  int last = -1;
-#pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    if (r < K) {
-      int nxt = 0x7fffffff;
-      float nv = 0.f;
-#pragma unroll
-      for (int k = 0; k < 16; ++k)
-        if (k < K && sel_e[k] > last && sel_e[k] < nxt) {
-          nxt = sel_e[k];
-          nv = sel_v[k];
-        }
-      denom += nv;
-      last = nxt;
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += kTopkWaves * 64) mask[(size_t)e * W + w] = mword[e];
+  if (STASH && scores_t) {
+    for (int idx = threadIdx.x; idx < E * 64; idx += kTopkWaves * 64) {
+      const int e = idx >> 6, i = idx & 63;
+      if (w * 64 + i < T) scores_t[(size_t)e * T + w * 64 + i] = st[idx];
     }
-  }
-#pragma unroll
-  for (int k = 0; k < 16; ++k) {
-    if (k < K && lane == k) {
-      topk_idx[(size_t)t * K + k] = sel_e[k];
-      if (topk_w) topk_w[(size_t)t * K + k] = sel_v[k] / denom;
-    }
-  }
-}
-
-// One wave per 64-token word: bit (t % 64) of mask[e][t / 64] is set iff
-// expert e is among token t's selected experts.
-__global__ __launch_bounds__(256) void build_mask_kernel(const int32_t* __restrict__ topk_idx,
-                                                         uint64_t* __restrict__ mask, int T, int E, int K, int W) {
-  const int wave = threadIdx.x >> 6;
-  const int lane = lane_id();
-  const int w = blockIdx.x * 4 + wave;
-  if (w >= W) return;
-  const int t = w * 64 + lane;
-  int ex[16];
-#pragma unroll
-  for (int k = 0; k < 16; ++k) ex[k] = (k < K && t < T) ? topk_idx[(size_t)t * K + k] : -1;
-  for (int e0 = 0; e0 < E; e0 += 64) {
-    uint64_t mine = 0;
-    const int lim = min(64, E - e0);
-    for (int i = 0; i < lim; ++i) {
-      const int e = e0 + i;
-      bool hit = false;
-#pragma unroll
-      for (int k = 0; k < 16; ++k) hit |= (ex[k] == e);
-      const uint64_t b = __ballot(hit);
-      if (lane == i) mine = b;
-    }
-    if (lane < lim) mask[(size_t)(e0 + lane) * W + w] = mine;
   }
 }
 
@@ -170,78 +171,186 @@ __global__ __launch_bounds__(256) void expert_scan_kernel(const uint64_t* __rest
   if (threadIdx.x == 0) counts[e] = running;
 }
 
-// offsets[0..n] = exclusive scan of cnt[0..n-1] (one block of 1024 threads).
+// out[0..n] = exclusive scan of cnt[0..n-1] (one block of 1024 threads, four
+// values per thread per pass).
 __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ cnt, int32_t* __restrict__ out,
                                                     int n) {
   __shared__ int lds[16];
   int running = 0;
-  for (int c0 = 0; c0 < n; c0 += 1024) {
-    const int i = c0 + threadIdx.x;
-    const int v = i < n ? cnt[i] : 0;
+  for (int c0 = 0; c0 < n; c0 += 4096) {
+    const int i0 = c0 + threadIdx.x * 4;
+    int v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = i0 + q < n ? cnt[i0 + q] : 0;
+    const int sum = v[0] + v[1] + v[2] + v[3];
     int total;
-    const int ex = block_excl_scan<1024>(v, &total, lds);
-    if (i < n) out[i] = running + ex;
+    int ex = block_excl_scan<1024>(sum, &total, lds) + running;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (i0 + q < n) out[i0 + q] = ex;
+      ex += v[q];
+    }
     running += total;
   }
   if (threadIdx.x == 0) out[n] = running;
 }
 
-// Per token: number of selected experts and the renormalisation denominator
-// (selected scores summed in ascending expert order, fp32).
-__global__ __launch_bounds__(256) void token_count_kernel(const uint64_t* __restrict__ mask,
-                                                          const float* __restrict__ scores, int32_t* __restrict__ cnt,
-                                                          float* __restrict__ denom, int T, int E, int W) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= T) return;
-  const int w = t >> 6, b = t & 63;
-  int c = 0;
-  float s = 0.f;
-  for (int e = 0; e < E; ++e) {
-    const uint64_t word = mask[(size_t)e * W + w];
-    if ((word >> b) & 1ull) {
-      ++c;
-      s += scores[(size_t)t * E + e];
-    }
-  }
-  cnt[t] = c;
-  denom[t] = s;
+__device__ __forceinline__ int expert_row(const uint64_t* __restrict__ mask, const int32_t* __restrict__ prefix,
+                                          const int32_t* __restrict__ offsets, int e, int W, int w, uint64_t below) {
+  const uint64_t word = mask[(size_t)e * W + w];
+  return offsets[e] + prefix[(size_t)e * W + w] + __popcll(word & below);
 }
 
-// Per token: place its rows (expert-major index of each pair), the
-// token-major list and the renormalised weights.
-__global__ __launch_bounds__(256) void token_place_kernel(
-    const uint64_t* __restrict__ mask, const int32_t* __restrict__ prefix, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tok_offsets, const float* __restrict__ scores, const float* __restrict__ denom,
-    int32_t* __restrict__ tok_rows, int32_t* __restrict__ row_token, int32_t* __restrict__ row_expert,
-    float* __restrict__ row_w, int T, int E, int W) {
+// Token-choice placement: every token has exactly K rows, so the token-major
+// offsets are t*K.  Each token's experts are visited in ascending order.
+__global__ __launch_bounds__(256) void tc_place_kernel(const int32_t* __restrict__ topk_idx,
+                                                       const float* __restrict__ topk_w,
+                                                       const uint64_t* __restrict__ mask,
+                                                       const int32_t* __restrict__ prefix,
+                                                       const int32_t* __restrict__ offsets,
+                                                       int32_t* __restrict__ tok_offsets, int32_t* __restrict__ tok_count,
+                                                       int32_t* __restrict__ tok_rows, int32_t* __restrict__ row_token,
+                                                       int32_t* __restrict__ row_expert, float* __restrict__ row_w, int T,
+                                                       int K, int W) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
   const int w = t >> 6, b = t & 63;
   const uint64_t below = b ? (~0ull >> (64 - b)) : 0ull;
-  int j = tok_offsets[t];
-  const float dn = denom[t];
-  for (int e = 0; e < E; ++e) {
-    const uint64_t word = mask[(size_t)e * W + w];
-    if ((word >> b) & 1ull) {
-      const int r = offsets[e] + prefix[(size_t)e * W + w] + __popcll(word & below);
-      tok_rows[j++] = r;
-      row_token[r] = t;
-      row_expert[r] = e;
-      row_w[r] = scores[(size_t)t * E + e] / dn;
+  int ex[16];
+  float wt[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    ex[k] = k < K ? topk_idx[(size_t)t * K + k] : 0x7fffffff;
+    wt[k] = k < K ? topk_w[(size_t)t * K + k] : 0.f;
+  }
+  int last = -1;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    if (r < K) {
+      int e = 0x7fffffff;
+      float wv = 0.f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k)
+        if (ex[k] > last && ex[k] < e) {
+          e = ex[k];
+          wv = wt[k];
+        }
+      last = e;
+      const int row = expert_row(mask, prefix, offsets, e, W, w, below);
+      tok_rows[(size_t)t * K + r] = row;
+      row_token[row] = t;
+      row_expert[row] = e;
+      row_w[row] = wv;
+    }
+  }
+  tok_offsets[t] = t * K;
+  tok_count[t] = K;
+  if (t == T - 1) tok_offsets[T] = T * K;
+}
+
+// General placement (any membership, e.g. after token rounding), one wave per
+// 64-token word.  Pass 1: per-token expert count and renormalisation
+// denominator (selected scores summed in ascending expert order, fp32).
+// The wave first loads the mask words of 64 experts at once (lane i holds
+// expert c + i), then walks the experts in ascending order, taking each word
+// from its lane with a readlane; the score loads of 8 experts are issued
+// before any is summed.
+constexpr int kMetaBatch = 8;
+
+__global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restrict__ mask,
+                                                         const float* __restrict__ scores_t, int32_t* __restrict__ cnt,
+                                                         float* __restrict__ denom, int T, int E, int W) {
+  const int w = blockIdx.x;
+  const int lane = lane_id();
+  const int t = w * 64 + lane;
+  const bool live = t < T;
+  int c = 0;
+  float s = 0.f;
+  for (int c0 = 0; c0 < E; c0 += 64) {
+    const uint64_t words = c0 + lane < E ? mask[(size_t)(c0 + lane) * W + w] : 0ull;
+    const int n = min(64, E - c0);
+    for (int j0 = 0; j0 < n; j0 += kMetaBatch) {
+      float v[kMetaBatch];
+#pragma unroll
+      for (int u = 0; u < kMetaBatch; ++u) {
+        const uint64_t word = readlane_u64(words, j0 + u);  // 0 past n
+        const bool hit = live && ((word >> lane) & 1ull);
+        v[u] = hit ? scores_t[(size_t)(c0 + j0 + u) * T + t] : 0.f;
+        c += hit;
+      }
+      // adding +0 for a miss leaves the sum unchanged (it is never -0)
+#pragma unroll
+      for (int u = 0; u < kMetaBatch; ++u) s += v[u];
+    }
+  }
+  if (live) {
+    cnt[t] = c;
+    denom[t] = s;
+  }
+}
+
+// Pass 2: rows of every token (expert ascending), renormalised weights.
+__global__ __launch_bounds__(64) void token_place_kernel(
+    const uint64_t* __restrict__ mask, const int32_t* __restrict__ prefix, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ tok_offsets, const float* __restrict__ scores_t, const float* __restrict__ denom,
+    int32_t* __restrict__ tok_rows, int32_t* __restrict__ row_token, int32_t* __restrict__ row_expert,
+    float* __restrict__ row_w, int T, int E, int W) {
+  const int w = blockIdx.x;
+  const int lane = lane_id();
+  const int t = w * 64 + lane;
+  const bool live = t < T;
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  int j = live ? tok_offsets[t] : 0;
+  const float dn = live ? denom[t] : 1.f;
+  for (int c0 = 0; c0 < E; c0 += 64) {
+    const int el = c0 + lane;
+    const uint64_t words = el < E ? mask[(size_t)el * W + w] : 0ull;
+    const int bases = el < E ? offsets[el] + prefix[(size_t)el * W + w] : 0;
+    const int n = min(64, E - c0);
+    for (int j0 = 0; j0 < n; j0 += kMetaBatch) {
+      float v[kMetaBatch];
+      bool hit[kMetaBatch];
+#pragma unroll
+      for (int u = 0; u < kMetaBatch; ++u) {
+        const uint64_t word = readlane_u64(words, j0 + u);
+        hit[u] = live && ((word >> lane) & 1ull);
+        v[u] = hit[u] ? scores_t[(size_t)(c0 + j0 + u) * T + t] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kMetaBatch; ++u) {
+        if (hit[u]) {
+          const int e = c0 + j0 + u;
+          const uint64_t word = readlane_u64(words, j0 + u);
+          const int r = __builtin_amdgcn_readlane(bases, j0 + u) + __popcll(word & below);
+          tok_rows[j++] = r;
+          row_token[r] = t;
+          row_expert[r] = e;
+          row_w[r] = v[u] / dn;
+        }
+      }
     }
   }
 }
 
 // ---------------------------------------------------------------- launchers
 
-hipError_t launch_softmax_topk(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
-                               int T, int E, int K, int do_softmax, hipStream_t s) {
-  const dim3 grid((T + 3) / 4), block(256);
+static size_t topk_lds_bytes(int E, bool stash) { return ((E * 8 + 15) & ~15) + (stash ? (size_t)E * 64 * 4 : 0); }
+
+hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
+                             uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s) {
+  const dim3 grid(W), block(kTopkWaves * 64);
   const int epl = (E + 63) / 64;
-#define SMOE_TOPK(N)                                                                                    \
-  if (epl <= N) {                                                                                       \
-    softmax_topk_kernel<N><<<grid, block, 0, s>>>(in, scores, scores_t, topk_idx, topk_w, T, E, K, do_softmax); \
-    return hipGetLastError();                                                                           \
+  // the transposed-score stash must fit the default 64 KB of dynamic LDS
+  const bool stash = scores_t && topk_lds_bytes(E, true) <= 65536;
+#define SMOE_TOPK(N)                                                                                               \
+  if (epl <= N) {                                                                                                  \
+    if (stash)                                                                                                     \
+      topk_route_kernel<N, true><<<grid, block, topk_lds_bytes(E, true), s>>>(in, scores, scores_t, topk_idx,      \
+                                                                               topk_w, mask, T, E, K, W, do_softmax); \
+    else                                                                                                           \
+      topk_route_kernel<N, false><<<grid, block, topk_lds_bytes(E, false), s>>>(in, scores, scores_t, topk_idx,    \
+                                                                                 topk_w, mask, T, E, K, W, do_softmax); \
+    return hipGetLastError();                                                                                      \
   }
   SMOE_TOPK(1)
   SMOE_TOPK(2)
@@ -254,19 +363,24 @@ hipError_t launch_softmax_topk(const float* in, float* scores, float* scores_t, 
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_build_mask(const int32_t* topk_idx, uint64_t* mask, int T, int E, int K, int W, hipStream_t s) {
-  build_mask_kernel<<<dim3((W + 3) / 4), dim3(256), 0, s>>>(topk_idx, mask, T, E, K, W);
-  return hipGetLastError();
-}
-
-hipError_t launch_metadata(const moe_routing& r, const float* scores, int T, int E, hipStream_t s) {
+hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, hipStream_t s) {
   const int W = r.words;
   expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
   scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.counts, r.offsets, E);
-  const dim3 tg((T + 255) / 256), tb(256);
-  token_count_kernel<<<tg, tb, 0, s>>>(r.mask, scores, r.tok_count, r.tok_denom, T, E, W);
+  tc_place_kernel<<<dim3((T + 255) / 256), dim3(256), 0, s>>>(r.topk_idx, r.topk_w, r.mask, r.mask_prefix, r.offsets,
+                                                              r.tok_offsets, r.tok_count, r.tok_rows, r.row_token,
+                                                              r.row_expert, r.row_w, T, K, W);
+  return hipGetLastError();
+}
+
+hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, hipStream_t s) {
+  const int W = r.words;
+  expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
+  scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.counts, r.offsets, E);
+  const dim3 wg(W), wb(64);
+  token_count_kernel<<<wg, wb, 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, T, E, W);
   scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.tok_count, r.tok_offsets, T);
-  token_place_kernel<<<tg, tb, 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_offsets, scores, r.tok_denom,
+  token_place_kernel<<<wg, wb, 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_offsets, scores_t, r.tok_denom,
                                        r.tok_rows, r.row_token, r.row_expert, r.row_w, T, E, W);
   return hipGetLastError();
 }

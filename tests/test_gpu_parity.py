@@ -46,12 +46,10 @@ def mask_bits(member):
     """Oracle membership -> the device's [E, ceil(T/64)] uint64 bitmap."""
     T, E = member.shape
     Wd = (T + 63) // 64
-    out = np.zeros((E, Wd), np.uint64)
-    for e in range(E):
-        for w in range(Wd):
-            seg = member[w * 64:(w + 1) * 64, e]
-            out[e, w] = np.uint64(sum(int(b) << i for i, b in enumerate(seg)))
-    return out
+    bits = np.zeros((E, Wd * 64), np.uint64)
+    bits[:, :T] = member.T.astype(np.uint64)
+    weights = np.left_shift(np.uint64(1), np.arange(64, dtype=np.uint64))
+    return (bits.reshape(E, Wd, 64) * weights).sum(axis=2, dtype=np.uint64)
 
 
 def check_routing(layer, R, idx=None, rdir=None):
@@ -196,3 +194,27 @@ def test_no_router_grad_path():
     fw = oracle.forward(X, W1, W2, R)
     bw = oracle.backward(dO, X, fw["H"], W1, W2, None, R)
     assert rel_err(layer.dX.float().cpu().numpy(), bw["dX"]) <= TOL
+
+
+ROUTE_ONLY = W.MoEConfig("route", T=3000, d=128, n=128, E=16, K=4, m_tile=128)
+
+
+@pytest.mark.parametrize("T", [3000, 9000, 20000, 40000])
+@pytest.mark.parametrize("quantised", [False, True])
+def test_rounding_selection_sizes_and_ties(T, quantised):
+    """Token sizes spanning every form of the device's rounding selection
+    (register-resident keys up to 32 per thread, then the re-reading form),
+    with real-valued scores and with scores on a coarse grid, where most
+    candidates tie on the threshold and the token-order tie break decides."""
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    inp = W.make_inputs(ROUTE_ONLY, 11, T=T)
+    _, S = oracle_scores(inp)
+    if quantised:
+        S = (np.round(S * 16.0) / 16.0).astype(np.float32)
+    for mode in ("up", "down", "nearest"):
+        layer = DeviceLayer(inp, round_mode=mode, scores_in=S)
+        layer.route()
+        torch.cuda.synchronize()
+        idx, rdir, R = oracle_routing(S, ROUTE_ONLY.K, mode, ROUTE_ONLY.m_tile)
+        check_routing(layer, R, idx, rdir)
