@@ -175,11 +175,14 @@ struct KOuterSide {
       gnext[j] = k < k_len ? gidx[k_begin + k] : 0;
     }
   }
-  // make the compiler complete the index loads before the DMA asm below
-  __device__ __forceinline__ void idx_ready() {
-    if (!gidx) return;
+  // Called where the index loads are known to be complete (after a
+  // vmcnt(0) wait).  The empty asm redefines the registers, so the compiler
+  // sees no pending load behind them later on; otherwise it places its own
+  // vmcnt(0) before every use, which also waits for the DMA (invisible to
+  // it) issued in between.
+  __device__ __forceinline__ void idx_commit() {
 #pragma unroll
-    for (int j = 0; j < Q; ++j) asm volatile("" ::"v"(gnext[j]));
+    for (int j = 0; j < Q; ++j) asm volatile("" : "+v"(gnext[j]));
   }
   __device__ __forceinline__ void issue(uint32_t lds_side, int k0, int part = 0, int parts = 1) const {
     const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -256,18 +259,11 @@ struct Acc {
   __device__ __forceinline__ static int wave_n() { return (threadIdx.x >> 6) / Cfg::WM; }
 };
 
-// XCD-aware remap of the flat workgroup id: workgroups are dispatched to the
-// 8 XCDs round-robin, so consecutive logical tiles are handed to the same XCD
-// (and share its L2) by mapping id -> (id % 8) * (G / 8) + id / 8.
-__device__ __forceinline__ int xcd_remap(int id, int G) {
-  if ((G & 7) != 0) return id;
-  return (id & 7) * (G >> 3) + (id >> 3);
-}
-
 // For varlen-M scheduling: find the expert e and its local m-tile for the
 // global m-tile index mt, where expert e owns ceil(count_e / BM) tiles.
-// Runs on wave 0; result broadcast through LDS.  Returns false if mt is past
-// the last tile.
+// Runs on wave 0; result broadcast through sh[0..3] (LDS).  Returns false if
+// mt is past the last tile.  The barrier waits for LDS only, so DMA loads in
+// flight stay in flight.
 template <int BM>
 __device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets, int E, int mt, int* sh, TileInfo& ti) {
   if (threadIdx.x < 64) {
@@ -303,7 +299,7 @@ __device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets,
       sh[3] = found_off;
     }
   }
-  __syncthreads();
+  barrier_lds();
   ti.e = sh[0];
   if (ti.e < 0) return false;
   ti.m0 = sh[1];
@@ -312,73 +308,146 @@ __device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets,
   return true;
 }
 
+// Number of varlen-M m-tiles, sum_e ceil(count_e / BM), from wave 0 through sh[0].
+template <int BM>
+__device__ __forceinline__ int count_m_tiles(const int32_t* __restrict__ offsets, int E, int* sh) {
+  if (threadIdx.x < 64) {
+    int total = 0;
+    for (int e = threadIdx.x; e < E; e += 64) total += (offsets[e + 1] - offsets[e] + BM - 1) / BM;
+    total = wave_sum(total);
+    if (threadIdx.x == 0) sh[0] = total;
+  }
+  barrier_lds();
+  return sh[0];
+}
+
+// Persistent schedule.  The grid holds one workgroup per CU, a multiple of 8,
+// and workgroup b runs on XCD b % 8 (round-robin dispatch).  The ntiles
+// logical tiles are cut into 8 contiguous ranges, one per XCD; the G/8
+// workgroups of an XCD take its range round-robin.  Tiles that run at the
+// same time on one XCD are then neighbours in the logical order (same
+// expert, shared operand rows in that XCD's L2), and every XCD gets the same
+// number of real tiles.
+struct Sched {
+  int ntiles, per_xcd, gx, x, slot;
+  __device__ __forceinline__ void init(int n) {
+    ntiles = n;
+    per_xcd = (n + 7) >> 3;
+    gx = gridDim.x >> 3;
+    x = blockIdx.x & 7;
+    slot = blockIdx.x >> 3;
+  }
+  // logical id of this workgroup's k-th tile, or -1 when it has no more
+  __device__ __forceinline__ int id(int k) const {
+    const int local = slot + k * gx;
+    if (local >= per_xcd) return -1;
+    const int l = x * per_xcd + local;
+    return l < ntiles ? l : -1;
+  }
+};
+
 // The main loop shared by every GEMM.  Op supplies:
-//   using Cfg = GemmCfg<...>;  static constexpr int M_MODE, N_MODE;
-//   bool tile(const Params&, TileInfo&, int* sh)          -- scheduling
+//   using Cfg = GemmCfg<...>;  static constexpr int M_MODE, N_MODE, EPI_LDS;
+//   int  count(const Params&, int* sh)                     -- number of tiles
+//   bool tile(const Params&, int id, TileInfo&, int* sh)   -- tile id -> TileInfo
 //   void init_m(const Params&, const TileInfo&, Side&)      -- operand sides
 //   void init_n(const Params&, const TileInfo&, Side&)
-//   void epilogue(const Params&, const TileInfo&, Acc<Cfg>&, char* smem)
+//   void epilogue(const Params&, const TileInfo&, Acc<Cfg>&, char* epi_lds)
+// Each workgroup is persistent over its tiles.  For tile k it looks up tile
+// k+1 and sets up its operand sides while tile k's first stages are in
+// flight; after tile k's k loop it issues tile k+1's prologue DMA and only
+// then runs tile k's epilogue, so the epilogue's stores and arithmetic
+// overlap the next tile's first loads.  The epilogue gets its own LDS
+// (EPI_LDS bytes) since the stage buffers are being refilled meanwhile.
 template <class Op>
 __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typename Op::Params p) {
   using Cfg = typename Op::Cfg;
+  using MSide = typename SideT<Op::M_MODE, Cfg::BM>::type;
+  using NSide = typename SideT<Op::N_MODE, Cfg::BN>::type;
   constexpr int BM = Cfg::BM, BN = Cfg::BN, S = Cfg::STAGES;
-  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES];
-  __shared__ int sh[8];
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES + (Op::EPI_LDS > 0 ? Op::EPI_LDS : 16)];
+  __shared__ int sh[16];  // [0..3], [4..7]: tile lookups of even / odd k; [8]: tile count
+  Sched sched;
+  sched.init(Op::count(p, sh + 8));
+  const int id = sched.id(0);
   TileInfo ti;
-  if (!Op::tile(p, ti, sh)) return;
-  typename SideT<Op::M_MODE, BM>::type ms;
-  typename SideT<Op::N_MODE, BN>::type ns;
+  // tile() may synchronise the workgroup: ids are workgroup-uniform
+  if (id < 0 || !Op::tile(p, id, ti, sh)) return;
+  MSide ms, ms_next;
+  NSide ns, ns_next;
   Op::init_m(p, ti, ms);
   Op::init_n(p, ti, ns);
-  Acc<Cfg> acc;
-  acc.zero();
-  const int nk = (ti.k_len + kBK - 1) / kBK;
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
   const int wave = threadIdx.x >> 6;
   const int wm0 = (wave % Cfg::WM) * (BM / Cfg::WM);
   const int wn0 = (wave / Cfg::WM) * (BN / Cfg::WN);
   constexpr int kPerStage = Cfg::QM + Cfg::QN;  // DMA ops per wave per stage
 
-  if (nk > 0) {
-    // prologue: stages 0 .. S-2
+  // stages 0 .. S-2 of a tile, and the row indices of stage S-1 (gathered k)
+  auto prologue = [&](const TileInfo& t, MSide& a, NSide& b) {
+    const int nk = (t.k_len + kBK - 1) / kBK;
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) {
       if (st < nk) {
-        if constexpr (Op::M_MODE == KOUTER) { ms.prefetch_idx(st * kBK); ms.idx_ready(); }
-        if constexpr (Op::N_MODE == KOUTER) { ns.prefetch_idx(st * kBK); ns.idx_ready(); }
-        ms.issue(lds0 + st * Cfg::STAGE_BYTES, st * kBK);
-        ns.issue(lds0 + st * Cfg::STAGE_BYTES + Cfg::M_BYTES, st * kBK);
+        if constexpr (Op::M_MODE == KOUTER) a.prefetch_idx(st * kBK);
+        if constexpr (Op::N_MODE == KOUTER) b.prefetch_idx(st * kBK);
+        if constexpr (Op::M_MODE == KOUTER || Op::N_MODE == KOUTER) {
+          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          if constexpr (Op::M_MODE == KOUTER) a.idx_commit();
+          if constexpr (Op::N_MODE == KOUTER) b.idx_commit();
+        }
+        a.issue(lds0 + st * Cfg::STAGE_BYTES, st * kBK);
+        b.issue(lds0 + st * Cfg::STAGE_BYTES + Cfg::M_BYTES, st * kBK);
       }
     }
-    if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((S - 1) * kBK);
-    if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((S - 1) * kBK);
+    if constexpr (Op::M_MODE == KOUTER) a.prefetch_idx((S - 1) * kBK);
+    if constexpr (Op::N_MODE == KOUTER) b.prefetch_idx((S - 1) * kBK);
+  };
+
+  Acc<Cfg> acc;
+  acc.zero();
+  prologue(ti, ms, ns);
+  for (int k = 0;; ++k) {
+    // next tile: lookup and side setup overlap this tile's first DMA
+    int idn = sched.id(k + 1);
+    TileInfo tn;
+    if (idn >= 0 && !Op::tile(p, idn, tn, sh + 4 * ((k + 1) & 1))) idn = -1;
+    if (idn >= 0) {
+      Op::init_m(p, tn, ms_next);
+      Op::init_n(p, tn, ns_next);
+    }
+    const int nk = (ti.k_len + kBK - 1) / kBK;
+    // gathered k rows: their index loads are younger than the DMA, so only a
+    // full drain covers them
+    bool gathered = false;
+    if constexpr (Op::M_MODE == KOUTER) gathered = gathered || ms.gidx != nullptr;
+    if constexpr (Op::N_MODE == KOUTER) gathered = gathered || ns.gidx != nullptr;
     for (int kt = 0; kt < nk; ++kt) {
       // stage kt is complete when at most (stages issued after it) * kPerStage ops remain
       const int ahead = min(S - 2, nk - 1 - kt);
       if constexpr (S == 3) {
-        if (ahead >= 1)
+        if (ahead >= 1 && kt > 0 && !gathered)
           wait_vm_barrier<kPerStage>();
         else
-          wait_vm_barrier<0>();
+          wait_vm_barrier<0>();  // at kt = 0 the previous epilogue's stores are younger than stage 0
       } else {
         wait_vm_barrier<0>();
       }
+      // with gathered k rows the wait above was a full drain, index loads included
+      if constexpr (Op::M_MODE == KOUTER) ms.idx_commit();
+      if constexpr (Op::N_MODE == KOUTER) ns.idx_commit();
       const int knext = kt + S - 1;
       const bool issue_next = knext < nk;
       const uint32_t st_next = lds0 + (knext % S) * Cfg::STAGE_BYTES;
-      if (issue_next) {
-        if constexpr (Op::M_MODE == KOUTER) ms.idx_ready();
-        if constexpr (Op::N_MODE == KOUTER) ns.idx_ready();
-      }
       const char* cur = smem + (kt % S) * Cfg::STAGE_BYTES;
       const char* lm = cur;
       const char* ln = cur + Cfg::M_BYTES;
       // fragments of sub-step s+1 are read while the MFMAs of sub-step s issue
       bf16x8 fm[2][Cfg::RM], fn[2][Cfg::RN];
 #pragma unroll
-      for (int i = 0; i < Cfg::RM; ++i) fm[0][i] = SideT<Op::M_MODE, BM>::type::frag(lm, wm0 + 32 * i, 0);
+      for (int i = 0; i < Cfg::RM; ++i) fm[0][i] = MSide::frag(lm, wm0 + 32 * i, 0);
 #pragma unroll
-      for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = SideT<Op::N_MODE, BN>::type::frag(ln, wn0 + 32 * j, 0);
+      for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = NSide::frag(ln, wn0 + 32 * j, 0);
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         // the next stage's DMA is spread over the four sub-steps so the
@@ -390,9 +459,9 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typenam
         const int cb = s & 1, nb = cb ^ 1;
         if (s + 1 < 4) {
 #pragma unroll
-          for (int i = 0; i < Cfg::RM; ++i) fm[nb][i] = SideT<Op::M_MODE, BM>::type::frag(lm, wm0 + 32 * i, s + 1);
+          for (int i = 0; i < Cfg::RM; ++i) fm[nb][i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
 #pragma unroll
-          for (int j = 0; j < Cfg::RN; ++j) fn[nb][j] = SideT<Op::N_MODE, BN>::type::frag(ln, wn0 + 32 * j, s + 1);
+          for (int j = 0; j < Cfg::RN; ++j) fn[nb][j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
         }
 #pragma unroll
         for (int i = 0; i < Cfg::RM; ++i)
@@ -405,9 +474,17 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typenam
         if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * kBK);
       }
     }
-    barrier_lds();  // every wave done with the LDS stages before the epilogue reuses them
+    barrier_lds();  // every wave is done with the stage buffers
+    if (idn >= 0) {
+      ms = ms_next;
+      ns = ns_next;
+      prologue(tn, ms, ns);
+    }
+    Op::epilogue(p, ti, acc, smem + Cfg::LDS_BYTES);
+    if (idn < 0) break;
+    ti = tn;
+    acc.zero();
   }
-  Op::epilogue(p, ti, acc, smem);
 }
 
 }  // namespace smoe

@@ -9,6 +9,8 @@
 //   dwr        dW_r = X^T dL             (split-K)    router weight gradient
 // varlen-M GEMMs schedule (expert, m-tile) pairs from the device-side expert
 // offsets, so no host synchronisation is needed for the ragged row counts.
+#include <algorithm>
+
 #include "gemm_core.h"
 #include "launch.h"
 
@@ -36,10 +38,12 @@ __device__ __forceinline__ void load_bf16x4(const uint16_t* src, float* out) {
 }
 
 // ---------------------------------------------------------------- scheduling
+// Logical tile ids are m-tile-major: id = mt * (N / BN) + nt, so neighbouring
+// ids share the rows of one m-tile and the weights of one expert.
 template <int BM, int BN>
-__device__ __forceinline__ bool tile_varlen_m(const int32_t* offsets, int E, int N, int K, int* sh, TileInfo& ti) {
+__device__ __forceinline__ bool tile_varlen_m(const int32_t* offsets, int E, int N, int K, int id, int* sh,
+                                              TileInfo& ti) {
   const int nnt = N / BN;
-  const int id = xcd_remap(blockIdx.x, gridDim.x);
   const int mt = id / nnt, nt = id % nnt;
   if (!find_m_tile<BM>(offsets, E, mt, sh, ti)) return false;
   ti.n0 = nt * BN;
@@ -49,9 +53,13 @@ __device__ __forceinline__ bool tile_varlen_m(const int32_t* offsets, int E, int
 }
 
 template <int BM, int BN>
-__device__ __forceinline__ bool tile_plain_m(int M, int N, int K, TileInfo& ti) {
+__device__ __forceinline__ int count_varlen_m(const int32_t* offsets, int E, int N, int* sh) {
+  return count_m_tiles<BM>(offsets, E, sh) * (N / BN);
+}
+
+template <int BM, int BN>
+__device__ __forceinline__ bool tile_plain_m(int M, int N, int K, int id, TileInfo& ti) {
   const int nnt = (N + BN - 1) / BN;
-  const int id = blockIdx.x;
   const int mt = id / nnt, nt = id % nnt;
   ti.e = 0;
   ti.m0 = mt * BM;
@@ -66,9 +74,8 @@ __device__ __forceinline__ bool tile_plain_m(int M, int N, int K, TileInfo& ti) 
 
 // varlen-K: one tile per (expert, m-tile, n-tile); k = the expert's rows
 template <int BM, int BN>
-__device__ __forceinline__ bool tile_varlen_k(const int32_t* offsets, int M, int N, TileInfo& ti) {
+__device__ __forceinline__ bool tile_varlen_k(const int32_t* offsets, int M, int N, int id, TileInfo& ti) {
   const int mtn = M / BM, ntn = N / BN;
-  const int id = xcd_remap(blockIdx.x, gridDim.x);
   ti.e = id / (mtn * ntn);
   const int rem = id % (mtn * ntn);
   ti.m0 = (rem / ntn) * BM;
@@ -90,9 +97,13 @@ template <class Cfg_>
 struct OpRouter {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
+  static constexpr int EPI_LDS = 0;
   struct Params { RouterGemmArgs a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
-    return tile_plain_m<Cfg::BM, Cfg::BN>(p.a.T, p.a.E, p.a.d, ti);
+  static __device__ int count(const Params& p, int*) {
+    return ((p.a.T + Cfg::BM - 1) / Cfg::BM) * ((p.a.E + Cfg::BN - 1) / Cfg::BN);
+  }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
+    return tile_plain_m<Cfg::BM, Cfg::BN>(p.a.T, p.a.E, p.a.d, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
     s.init(p.a.X, p.a.d, nullptr, ti.row_base, ti.mrows);
@@ -140,8 +151,12 @@ struct OpUp {
       return q < Wn / 2 ? j0 + wn * (Wn / 2) + q : n + j0 + wn * (Wn / 2) + (q - Wn / 2);
     }
   };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, p.a.d, sh, ti);
+  static constexpr int EPI_LDS = 0;
+  static __device__ int count(const Params& p, int* sh) {
+    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, sh);
+  }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, p.a.d, id, sh, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
     s.init(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
@@ -208,8 +223,12 @@ struct OpDown {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
   struct Params { DownArgs a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, p.a.n, sh, ti);
+  static constexpr int EPI_LDS = 0;
+  static __device__ int count(const Params& p, int* sh) {
+    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
+  }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, p.a.n, id, sh, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
     s.init(p.a.A, p.a.n, nullptr, ti.row_base, ti.mrows);
@@ -232,8 +251,12 @@ struct OpDH {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DHArgs a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, p.a.d, sh, ti);
+  static constexpr int EPI_LDS = Cfg::BM * Cfg::WN * 4;  // dS partial sums [BM][WN]
+  static __device__ int count(const Params& p, int* sh) {
+    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, sh);
+  }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, p.a.d, id, sh, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
     s.init(p.a.dO, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
@@ -247,7 +270,7 @@ struct OpDH {
     const int n = p.a.n;
     const int lane = threadIdx.x & 63;
     const int wn = t.wave_n();
-    float* red = (float*)smem;  // [BM][WN]
+    float* red = (float*)smem;  // [BM][WN], the epilogue's own LDS
     // H values of one accumulator row block (gate and up halves) and the
     // row's routing score, double-buffered: the loads of block i+1 are in
     // flight while block i is computed and stored.
@@ -310,7 +333,7 @@ struct OpDH {
       part += __shfl_xor(part, 32, kWave);
       if (lane < 32) red[m * Cfg::WN + wn] = part;
     }
-    __syncthreads();
+    barrier_lds();
     const int nnt = n / Cfg::BN;
     const int nt = ti.n0 / Cfg::BN;
     for (int m = threadIdx.x; m < ti.mrows; m += kThreads) {
@@ -332,8 +355,12 @@ struct OpDXt {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DXtArgs a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, 2 * p.a.n, sh, ti);
+  static constexpr int EPI_LDS = 0;
+  static __device__ int count(const Params& p, int* sh) {
+    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
+  }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, 2 * p.a.n, id, sh, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
     s.init(p.a.dH, 2 * p.a.n, nullptr, ti.row_base, ti.mrows);
@@ -354,8 +381,10 @@ struct OpDW2 {
   using Cfg = Cfg_;
   static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW2Args a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
-    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.n, p.a.d, ti);
+  static constexpr int EPI_LDS = 0;
+  static __device__ int count(const Params& p, int*) { return p.a.E * (p.a.n / Cfg::BM) * (p.a.d / Cfg::BN); }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
+    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.n, p.a.d, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
     s.init(p.a.Ap, p.a.n, nullptr, ti.k_begin, ti.k_len, p.a.n, ColOffset{ti.m0});
@@ -374,8 +403,10 @@ struct OpDW1 {
   using Cfg = Cfg_;
   static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW1Args a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
-    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.d, 2 * p.a.n, ti);
+  static constexpr int EPI_LDS = 0;
+  static __device__ int count(const Params& p, int*) { return p.a.E * (p.a.d / Cfg::BM) * (2 * p.a.n / Cfg::BN); }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
+    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.d, 2 * p.a.n, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
     s.init(p.a.X, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.m0});
@@ -393,10 +424,13 @@ template <class Cfg_>
 struct OpDWr {
   using Cfg = Cfg_;
   static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
+  static constexpr int EPI_LDS = 0;
   struct Params { DWrArgs a; };
-  static __device__ bool tile(const Params& p, TileInfo& ti, int*) {
+  static __device__ int count(const Params& p, int*) {
+    return p.a.splits * (p.a.d / Cfg::BM) * ((p.a.E + Cfg::BN - 1) / Cfg::BN);
+  }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
     const int mtn = p.a.d / Cfg::BM, ntn = (p.a.E + Cfg::BN - 1) / Cfg::BN;
-    const int id = blockIdx.x;
     const int split = id / (mtn * ntn), rem = id % (mtn * ntn);
     ti.e = split;
     ti.m0 = (rem / ntn) * Cfg::BM;
@@ -436,9 +470,24 @@ struct OpDWr {
 };
 
 // ================================================================== launchers
+// One persistent workgroup per CU (the grid is a multiple of 8 for the XCD
+// split), fewer when there are fewer tiles than CUs.
+static int cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 template <class Op>
-static hipError_t run(const typename Op::Params& p, int grid, hipStream_t s) {
-  if (grid <= 0) return hipSuccess;
+static hipError_t run(const typename Op::Params& p, int tiles_bound, hipStream_t s) {
+  if (tiles_bound <= 0) return hipSuccess;
+  const int grid = (std::min(tiles_bound, cu_count()) + 7) & ~7;
   grouped_gemm_kernel<Op><<<dim3(grid), dim3(kThreads), 0, s>>>(p);
   return hipGetLastError();
 }
