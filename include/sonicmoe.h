@@ -126,6 +126,11 @@ enum {
  *   X     [T,d] bf16;  Wr [d,E] bf16 (unused with MOE_ROUTE_SCORES_IN)
  *   bias  [E] fp32, nullable
  * r->capacity must be >= T*K.
+ * Scores are compared through the order-preserving image of their fp32 bit
+ * pattern, which is the float order for numbers (+0 = -0) and extends it to
+ * NaN (sign clear: above +Inf; sign set: below -Inf), so non-finite scores
+ * still select K distinct experts per token (their weights are then not
+ * finite).  Token rounding orders scores the same way.
  */
 int moe_route(moe_dims dims, const moe_bf16 *X, const moe_bf16 *Wr, const float *bias, int flags,
               moe_routing *r, void *stream);

@@ -3,30 +3,31 @@
 //
 // The paper builds its whole MoE computation from one grouped GEMM with
 // modular fusion plus an aggregation kernel (Section 3.1).  This core is that
-// grouped GEMM written for CDNA4.  A 512-thread workgroup (8 wave64, two per
-// SIMD) computes a BM x BN tile of C[M,N] = sum_k Mside[m,k] * Nside[n,k].
+// grouped GEMM written for CDNA4.  A workgroup of 4 or 8 wave64 computes a
+// BM x BN tile of C[M,N] = sum_k Mside[m,k] * Nside[n,k]; with 4 waves two
+// workgroups share a CU, so one's epilogue overlaps the other's k loop.
 //
 // Operands never pass through registers on their way to LDS:
 // global_load_lds_dwordx4 writes 16 bytes per lane straight into LDS.  The
 // LDS layout of a stage is chosen per operand:
 //   ROWS   : operand rows with k contiguous in memory (X, dO, A, dH, W rows).
-//            LDS tile [rows][64 k], 128-byte rows, 16-byte chunk index
-//            XOR-swizzled by (row & 7).  Rows may be gathered through an index
+//            LDS tile [rows][BK k], 16-byte chunk index XOR-swizzled by the
+//            row so fragment reads are bank-conflict free.  Rows may be gathered through an index
 //            list -- the token gather of Section 4.1.1 fused into the load.
 //            MFMA fragments are read with ds_read_b128.
 //   KOUTER : k is the outer index in memory, m/n contiguous (W1/W2 in the
 //            forward, every operand of the weight gradients).  LDS tile
-//            [64 k][R], stored as in memory with a 16-byte chunk XOR swizzle
+//            [BK k][R], stored as in memory with a 16-byte chunk XOR swizzle
 //            on the k row.  MFMA fragments (8 consecutive k of one column)
 //            are read with the CDNA4 transposing load ds_read_b64_tr_b16, so
 //            no register transpose is needed.  k rows may be gathered
 //            (varlen-K weight gradients over an expert's tokens) and rows past
 //            the end of the reduction read a zero page.
 //
-// The k loop keeps STAGES LDS buffers; each step waits for its own stage
-// (s_waitcnt vmcnt + s_barrier), then issues the DMA for the stage
-// STAGES-1 ahead, then runs the MFMAs, so loads overlap a full stage of
-// compute with one barrier per step.  The DMA and the wait are inline
+// The k loop keeps STAGES LDS buffers of BK (32 or 64) k each; each step
+// waits for its own stage (s_waitcnt vmcnt + s_barrier), then issues the DMA
+// for the stage STAGES-1 ahead, then runs the MFMAs, so up to STAGES-1 stages
+// of loads are in flight behind the compute, with one barrier per step.  The DMA and the wait are inline
 // assembly so the compiler's conservative LDS-DMA tracking does not serialise
 // the pipeline; every wait that orders DMA data is explicit here.
 //
@@ -38,9 +39,7 @@
 
 namespace smoe {
 
-constexpr int kThreads = 512;
-constexpr int kWaves = kThreads / 64;
-constexpr int kBK = 64;
+constexpr int kBK = 64;  // default k depth of a stage
 
 enum SrcMode { ROWS = 0, KOUTER = 1 };
 
@@ -72,38 +71,50 @@ __device__ __forceinline__ void wait_vm_barrier() {
 }
 __device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_>
+// BM x BN tile, WM x WN waves (each BM/WM x BN/WN), STAGES LDS buffers of BK
+// k, OCC workgroups per CU.
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_ = kBK, int OCC_ = 1>
 struct GemmCfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, BK = BK_, OCC = OCC_;
+  static constexpr int NW = WM * WN, THREADS = NW * 64;
   static constexpr int RM = BM / WM / 32, RN = BN / WN / 32;
-  static constexpr int M_BYTES = BM * kBK * 2, N_BYTES = BN * kBK * 2;
+  static constexpr int SUB = BK / 16;  // MFMA k steps per stage
+  static constexpr int M_BYTES = BM * BK * 2, N_BYTES = BN * BK * 2;
   static constexpr int STAGE_BYTES = M_BYTES + N_BYTES;
   static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
-  static constexpr int QM = BM / 64, QN = BN / 64;  // DMA instructions per wave per stage
-  static_assert(WM * WN == kWaves, "8 waves");
+  static constexpr int QM = BM * BK / (NW * 512), QN = BN * BK / (NW * 512);  // DMA instructions per wave per stage
+  static_assert(BK == 32 || BK == 64, "stage depth");
+  static_assert(STAGES >= 2 && STAGES <= 4, "stages");
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  static_assert(OCC * LDS_BYTES <= 160 * 1024, "LDS of the co-resident workgroups");
   static_assert(RM >= 1 && RN >= 1 && BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "wave tile");
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile multiple of 64");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 };
 
 // ---------------------------------------------------------------- ROWS side
-// LDS: [R][64] bf16, chunk c of row r at r*128 + ((c ^ ((r >> 1) & 7)) << 4).
-// A fragment read (32 rows, one chunk each) then hits every bank once per
-// 16 lanes: even and odd rows fall in different bank halves and the eight
-// rows of each parity get eight different chunk slots.
-// DMA instruction q covers rows 8q..8q+7; lane l -> row 8q + l/8, physical
-// chunk l%8, logical chunk (l%8) ^ ((row >> 1) & 7).
-template <int R>
+// LDS: [R][BK] bf16, C = BK/8 chunks of 16 bytes per row; chunk c of row r at
+// r*2BK + ((c ^ swz(r)) << 4) with swz(r) = (r >> 1) & 7 for BK = 64 and
+// (r >> 2) & 3 for BK = 32.  A fragment read (32 rows, one chunk each) is
+// served 16 lanes at a time; with this swizzle those 16 lanes hit 16
+// different 16-byte bank groups.
+// DMA instruction q covers rows (64/C)q .. (64/C)q + 64/C - 1; lane l -> row
+// (64/C)q + l/C, physical chunk l%C, logical chunk (l%C) ^ swz(row).
+template <int R, int BK, int NW>
 struct RowsSide {
-  static constexpr int Q = R / 64;  // instructions per wave
+  static constexpr int C = BK / 8;              // chunks per row
+  static constexpr int RPI = 64 / C;            // rows per DMA instruction
+  static constexpr int Q = R * BK / (NW * 512);  // instructions per wave
+  static_assert(Q >= 1 && Q * NW * 512 == R * BK, "rows x k of a stage must be whole DMA instructions per wave");
+  static __device__ __forceinline__ int swz(int r) { return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3); }
   const char* ptr[Q];               // row start (k = 0) of the row this lane loads, per instruction
   __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, const int32_t* idx, int row_base, int nrows) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
-      const int q = wave + kWaves * j;
-      const int lrow = 8 * q + (lane >> 3);
-      const int logical = (lane & 7) ^ ((lrow >> 1) & 7);
+      const int q = wave + NW * j;
+      const int lrow = RPI * q + lane / C;
+      const int logical = (lane % C) ^ swz(lrow);
       const int r = min(lrow, nrows - 1);
       const int64_t row = idx ? (int64_t)idx[row_base + r] : (int64_t)(row_base + r);
       ptr[j] = (const char*)(base + row * ld) + logical * 16;
@@ -114,27 +125,28 @@ struct RowsSide {
     const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int j = 0; j < Q; ++j)
-      if (j % parts == part) dma16(ptr[j] + k0 * 2, lds_side + (w + kWaves * j) * 1024);
+      if (j % parts == part) dma16(ptr[j] + k0 * 2, lds_side + (w + NW * j) * 1024);
   }
   static __device__ __forceinline__ bf16x8 frag(const char* lds_side, int r0, int s) {
     const int lane = threadIdx.x & 63;
     const int row = r0 + (lane & 31);
-    const int c = (2 * s + (lane >> 5)) ^ ((row >> 1) & 7);
-    return *(const bf16x8*)(lds_side + row * 128 + c * 16);
+    const int c = (2 * s + (lane >> 5)) ^ swz(row);
+    return *(const bf16x8*)(lds_side + row * (2 * BK) + c * 16);
   }
 };
 
 // --------------------------------------------------------------- KOUTER side
-// LDS: [64 k][R] bf16 (2R bytes per k row, L = R/8 chunks), chunk c of row k
+// LDS: [BK k][R] bf16 (2R bytes per k row, L = R/8 chunks), chunk c of row k
 // at k*2R + ((c ^ x(k)) << 4) with x(k) = 4*(k%4) for L >= 16 and
 // 4*((k/2)%2) for L = 8; with it, the 8 k rows x 64 bytes one transposing
 // read touches spread over all banks.
-template <int R>
+template <int R, int BK, int NW>
 struct KOuterSide {
   static constexpr int L = R / 8;
-  static constexpr int RPI = 512 / R;  // k rows per DMA instruction
-  static constexpr int Q = R / 64;     // instructions per wave
+  static constexpr int RPI = 512 / R;            // k rows per DMA instruction
+  static constexpr int Q = R * BK / (NW * 512);  // instructions per wave
   static_assert(L >= 8, "R >= 64");
+  static_assert(Q >= 1 && Q * NW * 512 == R * BK, "k x columns of a stage must be whole DMA instructions per wave");
   static __device__ __forceinline__ int swz(int k) { return L >= 16 ? 4 * (k & 3) : 4 * ((k >> 1) & 1); }
 
   const char* base;      // matrix base (bytes)
@@ -157,7 +169,7 @@ struct KOuterSide {
     k_len = kl;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
-      const int q = wave + kWaves * j;
+      const int q = wave + NW * j;
       const int row = q * RPI + lane / L;
       const int phys = lane % L;
       const int logical = phys ^ swz(row);
@@ -198,7 +210,7 @@ struct KOuterSide {
       } else {
         src = (const char*)g_zero_page + lane * 16;
       }
-      dma16(src, lds_side + (w + kWaves * j) * 1024);
+      dma16(src, lds_side + (w + NW * j) * 1024);
     }
   }
   static __device__ __forceinline__ bf16x8 frag(const char* lds_side, int c0, int s) {
@@ -224,15 +236,15 @@ struct KOuterSide {
   }
 };
 
-template <int MODE, int R>
+template <int MODE, int R, int BK, int NW>
 struct SideT;
-template <int R>
-struct SideT<ROWS, R> {
-  using type = RowsSide<R>;
+template <int R, int BK, int NW>
+struct SideT<ROWS, R, BK, NW> {
+  using type = RowsSide<R, BK, NW>;
 };
-template <int R>
-struct SideT<KOUTER, R> {
-  using type = KOuterSide<R>;
+template <int R, int BK, int NW>
+struct SideT<KOUTER, R, BK, NW> {
+  using type = KOuterSide<R, BK, NW>;
 };
 
 template <class Cfg>
@@ -360,11 +372,11 @@ struct Sched {
 // overlap the next tile's first loads.  The epilogue gets its own LDS
 // (EPI_LDS bytes) since the stage buffers are being refilled meanwhile.
 template <class Op>
-__global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typename Op::Params p) {
+__global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_kernel(const typename Op::Params p) {
   using Cfg = typename Op::Cfg;
-  using MSide = typename SideT<Op::M_MODE, Cfg::BM>::type;
-  using NSide = typename SideT<Op::N_MODE, Cfg::BN>::type;
-  constexpr int BM = Cfg::BM, BN = Cfg::BN, S = Cfg::STAGES;
+  using MSide = typename SideT<Op::M_MODE, Cfg::BM, Cfg::BK, Cfg::NW>::type;
+  using NSide = typename SideT<Op::N_MODE, Cfg::BN, Cfg::BK, Cfg::NW>::type;
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, S = Cfg::STAGES, BK = Cfg::BK, SUB = Cfg::SUB;
   __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES + (Op::EPI_LDS > 0 ? Op::EPI_LDS : 16)];
   __shared__ int sh[16];  // [0..3], [4..7]: tile lookups of even / odd k; [8]: tile count
   Sched sched;
@@ -385,23 +397,23 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typenam
 
   // stages 0 .. S-2 of a tile, and the row indices of stage S-1 (gathered k)
   auto prologue = [&](const TileInfo& t, MSide& a, NSide& b) {
-    const int nk = (t.k_len + kBK - 1) / kBK;
+    const int nk = (t.k_len + BK - 1) / BK;
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) {
       if (st < nk) {
-        if constexpr (Op::M_MODE == KOUTER) a.prefetch_idx(st * kBK);
-        if constexpr (Op::N_MODE == KOUTER) b.prefetch_idx(st * kBK);
+        if constexpr (Op::M_MODE == KOUTER) a.prefetch_idx(st * BK);
+        if constexpr (Op::N_MODE == KOUTER) b.prefetch_idx(st * BK);
         if constexpr (Op::M_MODE == KOUTER || Op::N_MODE == KOUTER) {
           asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
           if constexpr (Op::M_MODE == KOUTER) a.idx_commit();
           if constexpr (Op::N_MODE == KOUTER) b.idx_commit();
         }
-        a.issue(lds0 + st * Cfg::STAGE_BYTES, st * kBK);
-        b.issue(lds0 + st * Cfg::STAGE_BYTES + Cfg::M_BYTES, st * kBK);
+        a.issue(lds0 + st * Cfg::STAGE_BYTES, st * BK);
+        b.issue(lds0 + st * Cfg::STAGE_BYTES + Cfg::M_BYTES, st * BK);
       }
     }
-    if constexpr (Op::M_MODE == KOUTER) a.prefetch_idx((S - 1) * kBK);
-    if constexpr (Op::N_MODE == KOUTER) b.prefetch_idx((S - 1) * kBK);
+    if constexpr (Op::M_MODE == KOUTER) a.prefetch_idx((S - 1) * BK);
+    if constexpr (Op::N_MODE == KOUTER) b.prefetch_idx((S - 1) * BK);
   };
 
   Acc<Cfg> acc;
@@ -416,23 +428,23 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typenam
       Op::init_m(p, tn, ms_next);
       Op::init_n(p, tn, ns_next);
     }
-    const int nk = (ti.k_len + kBK - 1) / kBK;
+    const int nk = (ti.k_len + BK - 1) / BK;
     // gathered k rows: their index loads are younger than the DMA, so only a
     // full drain covers them
     bool gathered = false;
     if constexpr (Op::M_MODE == KOUTER) gathered = gathered || ms.gidx != nullptr;
     if constexpr (Op::N_MODE == KOUTER) gathered = gathered || ns.gidx != nullptr;
     for (int kt = 0; kt < nk; ++kt) {
-      // stage kt is complete when at most (stages issued after it) * kPerStage ops remain
-      const int ahead = min(S - 2, nk - 1 - kt);
-      if constexpr (S == 3) {
-        if (ahead >= 1 && kt > 0 && !gathered)
-          wait_vm_barrier<kPerStage>();
-        else
-          wait_vm_barrier<0>();  // at kt = 0 the previous epilogue's stores are younger than stage 0
-      } else {
+      // stage kt is complete when at most (stages issued after it) * kPerStage
+      // ops remain.  At kt = 0 the previous epilogue's stores are younger than
+      // stage 0, and gathered index loads are younger than the DMA: full drain.
+      const int ahead = (kt == 0 || gathered) ? 0 : min(S - 2, nk - 1 - kt);
+      if (ahead >= 2)
+        wait_vm_barrier<(S >= 4 ? 2 : 0) * kPerStage>();
+      else if (ahead == 1)
+        wait_vm_barrier<(S >= 3 ? 1 : 0) * kPerStage>();
+      else
         wait_vm_barrier<0>();
-      }
       // with gathered k rows the wait above was a full drain, index loads included
       if constexpr (Op::M_MODE == KOUTER) ms.idx_commit();
       if constexpr (Op::N_MODE == KOUTER) ns.idx_commit();
@@ -449,15 +461,15 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typenam
 #pragma unroll
       for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = NSide::frag(ln, wn0 + 32 * j, 0);
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        // the next stage's DMA is spread over the four sub-steps so the
+      for (int s = 0; s < SUB; ++s) {
+        // the next stage's DMA is spread over the sub-steps so the
         // vector-memory issue does not stall the MFMA stream in one burst
         if (issue_next) {
-          ms.issue(st_next, knext * kBK, s, 4);
-          ns.issue(st_next + Cfg::M_BYTES, knext * kBK, s, 4);
+          ms.issue(st_next, knext * BK, s, SUB);
+          ns.issue(st_next + Cfg::M_BYTES, knext * BK, s, SUB);
         }
         const int cb = s & 1, nb = cb ^ 1;
-        if (s + 1 < 4) {
+        if (s + 1 < SUB) {
 #pragma unroll
           for (int i = 0; i < Cfg::RM; ++i) fm[nb][i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
 #pragma unroll
@@ -470,8 +482,8 @@ __global__ __launch_bounds__(kThreads, 1) void grouped_gemm_kernel(const typenam
             acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[cb][j], fm[cb][i], acc.acc[i][j], 0, 0, 0);
       }
       if (issue_next) {
-        if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * kBK);
-        if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * kBK);
+        if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * BK);
+        if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * BK);
       }
     }
     barrier_lds();  // every wave is done with the stage buffers

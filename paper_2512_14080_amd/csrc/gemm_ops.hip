@@ -105,10 +105,10 @@ struct OpRouter {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
     return tile_plain_m<Cfg::BM, Cfg::BN>(p.a.T, p.a.E, p.a.d, id, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.X, p.a.d, nullptr, ti.row_base, ti.mrows);
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.Wr, p.a.E, nullptr, 0, p.a.d, p.a.E, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
@@ -158,10 +158,10 @@ struct OpUp {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, p.a.d, id, sh, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     const uint16_t* w = p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n);
     s.init(w, 2 * p.a.n, nullptr, 0, p.a.d, 2 * p.a.n, ColMap{(ti.n0 / Cfg::BN) * (Cfg::BN / 2), p.a.n});
   }
@@ -230,10 +230,10 @@ struct OpDown {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, p.a.n, id, sh, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.A, p.a.n, nullptr, ti.row_base, ti.mrows);
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     const uint16_t* w = p.a.W2 + (size_t)ti.e * p.a.n * p.a.d;
     s.init(w, p.a.d, nullptr, 0, p.a.n, p.a.d, ColOffset{ti.n0});
   }
@@ -258,10 +258,10 @@ struct OpDH {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, p.a.d, id, sh, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dO, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, RowsSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, RowsSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     // rows of W2_e [n][d] are the n columns of dA', with d contiguous
     s.init(p.a.W2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, nullptr, ti.n0, Cfg::BN);
   }
@@ -336,7 +336,7 @@ struct OpDH {
     barrier_lds();
     const int nnt = n / Cfg::BN;
     const int nt = ti.n0 / Cfg::BN;
-    for (int m = threadIdx.x; m < ti.mrows; m += kThreads) {
+    for (int m = threadIdx.x; m < ti.mrows; m += Cfg::THREADS) {
       float v = 0.f;
 #pragma unroll
       for (int w = 0; w < Cfg::WN; ++w) v += red[m * Cfg::WN + w];
@@ -362,10 +362,10 @@ struct OpDXt {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, 2 * p.a.n, id, sh, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dH, 2 * p.a.n, nullptr, ti.row_base, ti.mrows);
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, RowsSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, RowsSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     // rows of W1_e [d][2n] are the d columns of dX~, with 2n contiguous
     s.init(p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, nullptr, ti.n0, Cfg::BN);
   }
@@ -386,10 +386,10 @@ struct OpDW2 {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
     return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.n, p.a.d, id, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.Ap, p.a.n, nullptr, ti.k_begin, ti.k_len, p.a.n, ColOffset{ti.m0});
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dO, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
@@ -408,10 +408,10 @@ struct OpDW1 {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
     return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.d, 2 * p.a.n, id, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.X, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.m0});
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dH, 2 * p.a.n, nullptr, ti.k_begin, ti.k_len, 2 * p.a.n, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
@@ -437,15 +437,15 @@ struct OpDWr {
     ti.n0 = (rem % ntn) * Cfg::BN;
     ti.mrows = Cfg::BM;
     ti.row_base = 0;
-    const int chunk = (((p.a.T + p.a.splits - 1) / p.a.splits) + kBK - 1) / kBK * kBK;
+    const int chunk = (((p.a.T + p.a.splits - 1) / p.a.splits) + Cfg::BK - 1) / Cfg::BK * Cfg::BK;
     ti.k_begin = split * chunk;
     ti.k_len = max(0, min(chunk, p.a.T - ti.k_begin));
     return true;
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.X, p.a.d, nullptr, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.m0});
   }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN>& s) {
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dL, p.a.E, nullptr, ti.k_begin, ti.k_len, p.a.E, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
@@ -487,8 +487,9 @@ static int cu_count() {
 template <class Op>
 static hipError_t run(const typename Op::Params& p, int tiles_bound, hipStream_t s) {
   if (tiles_bound <= 0) return hipSuccess;
-  const int grid = (std::min(tiles_bound, cu_count()) + 7) & ~7;
-  grouped_gemm_kernel<Op><<<dim3(grid), dim3(kThreads), 0, s>>>(p);
+  using Cfg = typename Op::Cfg;
+  const int grid = (std::min(tiles_bound, cu_count() * Cfg::OCC) + 7) & ~7;
+  grouped_gemm_kernel<Op><<<dim3(grid), dim3(Cfg::THREADS), 0, s>>>(p);
   return hipGetLastError();
 }
 

@@ -17,6 +17,16 @@ namespace smoe {
 
 constexpr int kTopkWaves = 16;
 
+// Order-preserving integer image of an fp32 score (+0 and -0 map to one key).
+// Comparisons go through it so the selection order is total even for NaN
+// scores (a NaN never compares greater or smaller as a float, which would let
+// the lanes of a wave disagree on the winner and pick an expert twice).
+__device__ __forceinline__ uint32_t topk_key(float x) {
+  uint32_t b = __float_as_uint(x);
+  if (b == 0x80000000u) b = 0;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
 // Workgroup = 64 tokens (one membership word).  `in` and `scores` may alias
 // (logits overwritten in place by the scores).  With STASH, the scores are
 // staged in LDS and written transposed (scores_t[e][t]) in 64-token runs.
@@ -86,14 +96,17 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
       sel_e[k] = 0;
       sel_v[k] = 0.f;
       if (k < K) {
-        float bv = -INFINITY;
+        float bv = 0.f;
+        uint32_t bk = 0;
         int be = 0x7fffffff;
 #pragma unroll
         for (int j = 0; j < EPL; ++j) {
           const int e = lane + 64 * j;
           if (e < E && !((taken >> j) & 1u)) {
-            if (be == 0x7fffffff || v[j] > bv || (v[j] == bv && e < be)) {
+            const uint32_t kj = topk_key(v[j]);
+            if (be == 0x7fffffff || kj > bk || (kj == bk && e < be)) {
               bv = v[j];
+              bk = kj;
               be = e;
             }
           }
@@ -101,11 +114,13 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) {
           const float ov = __shfl_xor(bv, o, kWave);
+          const uint32_t ok = (uint32_t)__shfl_xor((int)bk, o, kWave);
           const int oe = __shfl_xor(be, o, kWave);
           // candidates without a valid expert carry index INT_MAX and lose
-          const bool better = (oe != 0x7fffffff) && (be == 0x7fffffff || ov > bv || (ov == bv && oe < be));
+          const bool better = (oe != 0x7fffffff) && (be == 0x7fffffff || ok > bk || (ok == bk && oe < be));
           if (better) {
             bv = ov;
+            bk = ok;
             be = oe;
           }
         }
@@ -236,6 +251,7 @@ __global__ __launch_bounds__(256) void tc_place_kernel(const int32_t* __restrict
           wv = wt[k];
         }
       last = e;
+      if (e == 0x7fffffff) break;  // fewer than K distinct experts: cannot happen with a valid top-K
       const int row = expert_row(mask, prefix, offsets, e, W, w, below);
       tok_rows[(size_t)t * K + r] = row;
       row_token[row] = t;

@@ -218,3 +218,45 @@ def test_rounding_selection_sizes_and_ties(T, quantised):
         torch.cuda.synchronize()
         idx, rdir, R = oracle_routing(S, ROUTE_ONLY.K, mode, ROUTE_ONLY.m_tile)
         check_routing(layer, R, idx, rdir)
+
+
+def test_routing_with_nonfinite_scores():
+    """Scores holding NaN and +-Inf (a diverged router, or caller-supplied
+    scores) still give every token K distinct experts in [0, E), consistent
+    counts/offsets/rows, and a rounded routing within capacity; the layer then
+    runs on it.  Selection follows the total order of the fp32 bit patterns,
+    which is the float order wherever both operands are numbers."""
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    cfg = W.MoEConfig("nonfinite", T=700, d=128, n=128, E=64, K=6, m_tile=64)
+    inp = W.make_inputs(cfg, 12)
+    _, S = oracle_scores(inp)
+    rng = np.random.default_rng(5)
+    S = S.copy()
+    flat = S.reshape(-1)
+    pick = rng.choice(flat.size, flat.size // 20, replace=False)
+    flat[pick[0::3]] = np.nan
+    flat[pick[1::3]] = np.inf
+    flat[pick[2::3]] = -np.inf
+    S[3, :] = np.nan  # a token whose every score is NaN
+    for mode in (None, "nearest"):
+        layer = DeviceLayer(inp, round_mode=mode, scores_in=S)
+        layer.step()
+        torch.cuda.synchronize()
+        tc = {k: v.cpu().numpy() for k, v in layer.tc.arrays().items() if v is not None}
+        idx = tc["topk_idx"]
+        assert idx.shape == (cfg.T, cfg.K)
+        assert ((idx >= 0) & (idx < cfg.E)).all()
+        assert all(len(set(r)) == cfg.K for r in idx)
+        np.testing.assert_array_equal(tc["counts"], np.bincount(idx.ravel(), minlength=cfg.E))
+        # finite-score tokens keep the oracle's choice
+        ok = np.isfinite(S).all(axis=1)
+        ref = oracle.topk_select(S[ok], cfg.K)
+        np.testing.assert_array_equal(idx[ok], ref)
+        a = {k: (v.cpu().numpy() if v is not None else None) for k, v in layer.routing.arrays().items()}
+        P = int(a["offsets"][-1])
+        assert P == int(a["counts"].sum()) <= layer.routing.capacity
+        assert (np.diff(a["offsets"]) == a["counts"]).all()
+        rt, re_ = a["row_token"][:P], a["row_expert"][:P]
+        assert ((rt >= 0) & (rt < cfg.T)).all() and ((re_ >= 0) & (re_ < cfg.E)).all()
+        assert sorted(a["tok_rows"][:P].tolist()) == list(range(P))
