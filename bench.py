@@ -23,10 +23,122 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_7b_tr128.md")
+
+# kernel-name fragment -> kernel class (as in the library's timing classes)
+KERNEL_CLASS_OF = [("OpUp<", "up_proj"), ("OpDown<", "down_proj"), ("OpDH<", "dH"), ("OpDW2<", "dW2"),
+                   ("OpDXt<", "dXtilde"), ("OpDW1<", "dW1"), ("OpDWr<", "dWr"), ("OpRouter<", "router_gemm"),
+                   ("agg_o_kernel", "aggregate_O"), ("agg_dx_kernel", "aggregate_dX"),
+                   ("topk_route_kernel", "topk"), ("tr_select_kernel", "tr_select")]
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    """sha256 over the HIP/C++ sources of the library (sorted by file name)."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2512_14080_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h", ".cpp")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+def _pmc_per_dispatch(run_dir, counter):
+    """Mean of a rocprofv3 counter per dispatch, by kernel name (KiB for *_SIZE)."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {run_dir}")
+    tot, disp = {}, {}
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                k = r["Kernel_Name"]
+                tot[k] = tot.get(k, 0.0) + float(r["Counter_Value"])
+                disp.setdefault(k, set()).add(r["Dispatch_Id"])
+    return {k: tot[k] / len(disp[k]) for k in tot}
+
+
+def traffic_report(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_bytes):
+    """Markdown summary of measured HBM traffic per launch and kernel class.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by what the same
+    counter reads for a plain device copy of copy_bytes (read once, written once)."""
+    cf = _pmc_per_dispatch(copy_fetch_dir, "FETCH_SIZE")
+    cw = _pmc_per_dispatch(copy_write_dir, "WRITE_SIZE")
+    ck = [k for k in cf if "copyBuffer" in k]
+    if not ck:
+        raise RuntimeError("no copy kernel in the calibration run")
+    f_scale = copy_bytes / (cf[ck[0]] * 1024.0)
+    w_scale = copy_bytes / (cw[ck[0]] * 1024.0)
+    fetch = _pmc_per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = _pmc_per_dispatch(write_dir, "WRITE_SIZE")
+    rows = []
+    for frag, cls in KERNEL_CLASS_OF:
+        ks = [k for k in fetch if frag in k]
+        if not ks:
+            continue
+        f = sum(fetch[k] for k in ks) / len(ks)
+        w = sum(write.get(k, 0.0) for k in ks) / len(ks)
+        rows.append((cls, f, w, f * 1024 * f_scale + w * 1024 * w_scale))
+    lines = [
+        "# HBM traffic per launch: 7B layer step (T=32768, d=1536, n=256, E=128, K=8), token rounding "
+        "M_tile=128 nearest",
+        "",
+        "Commands (repository root, one MI355X; each counter in a run of its own):",
+        "",
+        "```",
+        "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- "
+        "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- "
+        "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/copy_fetch -o run -- "
+        f"python3 bench.py --copy-calibration {copy_bytes}",
+        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/copy_write -o run -- "
+        f"python3 bench.py --copy-calibration {copy_bytes}",
+        "python3 bench.py --traffic-report gpurun_out/pmc_fetch gpurun_out/pmc_write gpurun_out/copy_fetch "
+        f"gpurun_out/copy_write {copy_bytes}",
+        "```",
+        "",
+        f"Calibration: a device copy of {copy_bytes} bytes reads FETCH_SIZE = {cf[ck[0]]:.1f} KiB and "
+        f"WRITE_SIZE = {cw[ck[0]]:.1f} KiB per dispatch, so fetch scale = {f_scale:.4f} and write scale = "
+        f"{w_scale:.4f} (bytes per counted byte).",
+        "",
+        "| kernel class | FETCH_SIZE KiB/launch | WRITE_SIZE KiB/launch | scaled HBM bytes/launch |",
+        "|---|---|---|---|",
+    ]
+    for cls, f, w, b in rows:
+        lines.append(f"| {cls} | {f:.1f} | {w:.1f} | {b:.0f} |")
+    lines += ["", f"kernel sources sha256: {kernel_source_hash()}", ""]
+    return "\n".join(lines)
+
+
+def measured_traffic(kernel_class):
+    """Scaled HBM bytes per launch from the committed profile, if the kernels are unchanged since."""
+    try:
+        with open(TRAFFIC_PROFILE) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    if f"kernel sources sha256: {kernel_source_hash()}" not in text:
+        return None
+    for line in text.splitlines():
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) == 4 and cells[0] == kernel_class:
+            try:
+                return float(cells[3])
+            except ValueError:
+                return None
+    return None
 
 
 def kernel_work(cls, cfg, P, T):
@@ -97,13 +209,31 @@ def main():
     ap.add_argument("--round", default="nearest", help="rounding mode, or 'none' for token-choice routing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="also time every kernel class")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run one plain device copy of BYTES (HBM counter calibration) and exit")
+    ap.add_argument("--traffic-report", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
+                                                          "COPY_WRITE_DIR", "COPY_BYTES"),
+                    help="print the HBM-traffic markdown summary from rocprofv3 counter runs and exit")
     args = ap.parse_args()
+    if args.traffic_report:
+        fd, wd, cfd, cwd, nb = args.traffic_report
+        print(traffic_report(fd, wd, cfd, cwd, int(nb)))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the layer is built and measured on a "
               f"single MI355X; multi-GPU sharding is a design note, not part of this build.", file=sys.stderr)
         sys.exit(2)
 
     import torch
+
+    if args.copy_calibration:
+        a = torch.ones(args.copy_calibration, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"[bench] copied {args.copy_calibration} bytes once")
+        return
 
     from paper_2512_14080_amd import binding as B
     from paper_2512_14080_amd import workloads as W
@@ -176,7 +306,7 @@ def main():
         "tokens_per_s": round(cfg.T / (ms_step * 1e-3), 1),
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "roofline": {"kernel": dominant, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
-                     "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                     "unit": unit, "frac": round(achieved / peak, 4), "traffic": measured_traffic(dominant),
                      "launch_ms": round(dom_avg, 5), "launches": dom_n},
         "kernel_ms": {c: round(t, 5) for c, t in per.items()},
     }

@@ -13,6 +13,9 @@ then up columns), down-projection W2[E,n,d], top-K routing.
 from __future__ import annotations
 
 import dataclasses
+import concurrent.futures
+import os
+
 import numpy as np
 
 
@@ -57,10 +60,12 @@ CONFIGS = {
 
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
-    """Round fp32 values to bf16 (round-to-nearest-even) and return raw uint16 bits."""
+    """Round finite fp32 values to bf16 (round-to-nearest-even) and return raw
+    uint16 bits.  The uint32 sum cannot wrap for finite inputs (largest bit
+    pattern 0xFF7FFFFF + 0x8000 < 2^32)."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    b = x.view(np.uint32).astype(np.uint64)
-    r = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    b = x.view(np.uint32)
+    r = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return r.astype(np.uint16)
 
 
@@ -86,31 +91,62 @@ class MoEInputs:
         return f32_from_bf16_bits(getattr(self, name))
 
 
+_ROW_BLOCK = 2048  # rows (tokens) or experts per independent normal stream
+
+
+def _normal_blocks(ss: np.random.SeedSequence, shape, scale: float, block: int) -> np.ndarray:
+    """Standard normals * scale, rounded to bf16 bits, drawn block by block along
+    axis 0: block i of ``block`` leading indices uses its own Philox stream
+    seeded by the child SeedSequence (entropy of ``ss``, spawn key + (i,)).
+    Blocks are filled on a thread pool; the values do not depend on it, and a
+    prefix along axis 0 reproduces the first blocks exactly."""
+    out = np.empty(shape, np.uint16)
+    nb = (shape[0] + block - 1) // block
+
+    def fill(i):
+        child = np.random.SeedSequence(ss.entropy, spawn_key=tuple(ss.spawn_key) + (i,))
+        g = np.random.Generator(np.random.Philox(child))
+        lo, hi = i * block, min(shape[0], (i + 1) * block)
+        x = g.standard_normal((hi - lo,) + tuple(shape[1:]), dtype=np.float32)
+        x *= np.float32(scale)
+        out[lo:hi] = bf16_bits_from_f32(x)
+
+    workers = max(1, min(16, os.cpu_count() or 1, nb))
+    if workers == 1:
+        for i in range(nb):
+            fill(i)
+    else:
+        with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill, range(nb)))
+    return out
+
+
 def make_inputs(cfg: MoEConfig, seed: int = 0, T: int | None = None) -> MoEInputs:
     """Draw the layer's inputs from a fixed seed.
 
     Streams are spawned from one SeedSequence in the fixed order
-    [X, W_r, W1, W2, dO, bias-permutation].  Draws are fp32, then rounded to
-    bf16.  ``T`` overrides the token count (the first T rows of the X/dO
-    streams are the same as for the full config, so a sample is a prefix).
+    [X, W_r, W1, W2, dO, bias-permutation]; X and dO are drawn in blocks of
+    2048 tokens and W1/W2 in blocks of 2048 experts' leading index (one child
+    stream per block, see _normal_blocks).  Draws are fp32, then rounded to
+    bf16.  ``T`` overrides the token count (the first T rows of X and dO are
+    the same as for the full config, so a sample is a prefix).
     """
     T = cfg.T if T is None else T
     ss = np.random.SeedSequence(seed)
-    gx, gr, g1, g2, gd, gb = [np.random.Generator(np.random.Philox(s)) for s in ss.spawn(6)]
+    sx, sr, s1, s2, sd, sb = ss.spawn(6)
     d, n, E = cfg.d, cfg.n, cfg.E
-    X = gx.standard_normal((T, d), dtype=np.float32) * np.float32(cfg.w_std)
     r_std = cfg.w_std if cfg.router == "w_std" else 1.0 / (cfg.w_std * np.sqrt(d))
-    Wr = gr.standard_normal((d, E), dtype=np.float32) * np.float32(r_std)
-    W1 = g1.standard_normal((E, d, 2 * n), dtype=np.float32) * np.float32(cfg.w_std)
-    W2 = g2.standard_normal((E, n, d), dtype=np.float32) * np.float32(cfg.w_std)
-    dO = gd.standard_normal((T, d), dtype=np.float32)
+    X = _normal_blocks(sx, (T, d), cfg.w_std, _ROW_BLOCK)
+    Wr = _normal_blocks(sr, (d, E), r_std, d)
+    W1 = _normal_blocks(s1, (E, d, 2 * n), cfg.w_std, 1)
+    W2 = _normal_blocks(s2, (E, n, d), cfg.w_std, 1)
+    dO = _normal_blocks(sd, (T, d), 1.0, _ROW_BLOCK)
     bias = None
     if cfg.zipf_s > 0:
+        gb = np.random.Generator(np.random.Philox(sb))
         rank = gb.permutation(E) + 1  # expert e gets popularity rank rank[e]
         bias = (-cfg.zipf_s * np.log(rank.astype(np.float64))).astype(np.float32)
-    return MoEInputs(cfg, seed, bf16_bits_from_f32(X), bf16_bits_from_f32(Wr),
-                     bf16_bits_from_f32(W1), bf16_bits_from_f32(W2),
-                     bf16_bits_from_f32(dO), bias)
+    return MoEInputs(cfg, seed, X, Wr, W1, W2, dO, bias)
 
 
 def scaled(cfg: MoEConfig, **kw) -> MoEConfig:
