@@ -22,20 +22,41 @@ __device__ __forceinline__ float silu_sig(float g, float* sig) {
   return g * s;
 }
 
-__device__ __forceinline__ void store_bf16x4(uint16_t* dst, float a, float b, float c, float d) {
-  u32x2 v;
-  v[0] = pack_bf2(a, b);
-  v[1] = pack_bf2(c, d);
-  *(u32x2*)dst = v;
+
+// One 32-column accumulator block of a row, as bf16: v[g] holds columns
+// 8g + 4*(lane/32) + [0, 4) (the MFMA output layout).  One lane-pair swap per
+// dword (v_permlane32_swap exchanges the upper half of its first operand with
+// the lower half of its second) leaves every lane with 8 consecutive
+// columns, so each lane stores 16 bytes: lane < 32 columns 8g .. 8g+7 and
+// lane >= 32 columns 8g+8 .. 8g+15, for g = 0, 2.
+__device__ __forceinline__ void store_block_bf16(uint16_t* row_block, const u32x2 (&v)[4]) {
+  const int hi = (threadIdx.x >> 5) & 1;
+#pragma unroll
+  for (int g = 0; g < 4; g += 2) {
+    const auto a = __builtin_amdgcn_permlane32_swap(v[g][0], v[g + 1][0], false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(v[g][1], v[g + 1][1], false, false);
+    *(u32x4*)(row_block + 8 * g + 8 * hi) = u32x4{a[0], b[0], a[1], b[1]};
+  }
 }
 
-__device__ __forceinline__ void load_bf16x4(const uint16_t* src, float* out) {
-  const u32x2 v = *(const u32x2*)src;
-  out[0] = bf_lo(v[0]);
-  out[1] = bf_hi(v[0]);
-  out[2] = bf_lo(v[1]);
-  out[3] = bf_hi(v[1]);
+// The inverse: 16-byte loads of a 32-column block, returned in the
+// accumulator layout of store_block_bf16 (the swap is its own inverse).
+__device__ __forceinline__ void load_block_bf16(const uint16_t* row_block, u32x2 (&v)[4]) {
+  const int hi = (threadIdx.x >> 5) & 1;
+#pragma unroll
+  for (int g = 0; g < 4; g += 2) {
+    const u32x4 x = *(const u32x4*)(row_block + 8 * g + 8 * hi);
+    const auto a = __builtin_amdgcn_permlane32_swap(x[0], x[2], false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(x[1], x[3], false, false);
+    v[g] = u32x2{a[0], b[0]};
+    v[g + 1] = u32x2{a[1], b[1]};
+  }
 }
+
+__device__ __forceinline__ u32x2 pack_bf16x4(float a, float b, float c, float d) {
+  return u32x2{pack_bf2(a, b), pack_bf2(c, d)};
+}
+
 
 // ---------------------------------------------------------------- scheduling
 // Logical tile ids are m-tile-major: id = mt * (N / BN) + nt, so neighbouring
@@ -178,11 +199,11 @@ struct OpUp {
       uint16_t* h = p.a.H + row * (2 * n);
       uint16_t* a = p.a.A + row * n;
 #pragma unroll
-      for (int j = 0; j < RN / 2; ++j)
+      for (int j = 0; j < RN / 2; ++j) {
+        const int col = j0 + wn * (Wn / 2) + 32 * j;  // first column of the 32-column block
+        u32x2 hg[4], hu[4], ha[4];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int q = t.n_of(j, g) - wn * Wn;
-          const int col = j0 + wn * (Wn / 2) + q;
           float gv[4], uv[4], av[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -191,10 +212,14 @@ struct OpUp {
             float sg;
             av[r] = silu_sig(gv[r], &sg) * uv[r];
           }
-          store_bf16x4(h + col, gv[0], gv[1], gv[2], gv[3]);
-          store_bf16x4(h + n + col, uv[0], uv[1], uv[2], uv[3]);
-          store_bf16x4(a + col, av[0], av[1], av[2], av[3]);
+          hg[g] = pack_bf16x4(gv[0], gv[1], gv[2], gv[3]);
+          hu[g] = pack_bf16x4(uv[0], uv[1], uv[2], uv[3]);
+          ha[g] = pack_bf16x4(av[0], av[1], av[2], av[3]);
         }
+        store_block_bf16(h + col, hg);
+        store_block_bf16(h + n + col, hu);
+        store_block_bf16(a + col, ha);
+      }
     }
   }
 };
@@ -208,12 +233,13 @@ __device__ __forceinline__ void store_rows_bf16(uint16_t* out, int64_t ld, int r
     if (m >= mrows) continue;
     uint16_t* y = out + (size_t)(row_base + m) * ld + n0;
 #pragma unroll
-    for (int j = 0; j < Cfg::RN; ++j)
+    for (int j = 0; j < Cfg::RN; ++j) {
+      u32x2 v[4];
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int c = t.n_of(j, g);
-        store_bf16x4(y + c, t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
-      }
+      for (int g = 0; g < 4; ++g)
+        v[g] = pack_bf16x4(t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
+      store_block_bf16(y + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1), v);
+    }
   }
 }
 
@@ -282,13 +308,11 @@ struct OpDH {
       const uint16_t* h = p.a.H + row * (2 * n);
       sw[b] = p.a.row_w[row];
 #pragma unroll
-      for (int j = 0; j < RN; ++j)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int col = ti.n0 + t.n_of(j, g);
-          hg[b][j][g] = *(const u32x2*)(h + col);
-          hu[b][j][g] = *(const u32x2*)(h + n + col);
-        }
+      for (int j = 0; j < RN; ++j) {
+        const int col = ti.n0 + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1);  // first column of the block
+        load_block_bf16(h + col, hg[b][j]);
+        load_block_bf16(h + n + col, hu[b][j]);
+      }
     };
     load_block(0, 0);
 #pragma unroll
@@ -304,10 +328,11 @@ struct OpDH {
       float part = 0.f;
       if (valid) {
 #pragma unroll
-        for (int j = 0; j < RN; ++j)
+        for (int j = 0; j < RN; ++j) {
+          const int col = ti.n0 + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1);
+          u32x2 vg[4], vu[4], va[4];
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
-            const int col = ti.n0 + t.n_of(j, g);
             const float gv[4] = {bf_lo(hg[b][j][g][0]), bf_hi(hg[b][j][g][0]), bf_lo(hg[b][j][g][1]),
                                  bf_hi(hg[b][j][g][1])};
             const float uv[4] = {bf_lo(hu[b][j][g][0]), bf_hi(hu[b][j][g][0]), bf_lo(hu[b][j][g][1]),
@@ -325,10 +350,14 @@ struct OpDH {
               du[r] = da * sl;
               apv[r] = s * av;
             }
-            store_bf16x4(dh + col, dg[0], dg[1], dg[2], dg[3]);
-            store_bf16x4(dh + n + col, du[0], du[1], du[2], du[3]);
-            store_bf16x4(ap + col, apv[0], apv[1], apv[2], apv[3]);
+            vg[g] = pack_bf16x4(dg[0], dg[1], dg[2], dg[3]);
+            vu[g] = pack_bf16x4(du[0], du[1], du[2], du[3]);
+            va[g] = pack_bf16x4(apv[0], apv[1], apv[2], apv[3]);
           }
+          store_block_bf16(dh + col, vg);
+          store_block_bf16(dh + n + col, vu);
+          store_block_bf16(ap + col, va);
+        }
       }
       part += __shfl_xor(part, 32, kWave);
       if (lane < 32) red[m * Cfg::WN + wn] = part;
