@@ -13,54 +13,82 @@ namespace smoe {
 
 constexpr int kAggBatch = 8;  // rows whose loads are in flight together
 constexpr int kColRows = 128;  // tokens per chunk of the dbias column sum
+static_assert(kAggBatch == 8, "lane & 7 picks a batch slot");
 
-// One wave per token; lanes cover 8 consecutive bf16 (16 bytes) of the row.
-// The token's rows are taken kAggBatch at a time: all their loads are issued
-// before any is accumulated, so a lane keeps several HBM reads in flight.
+__device__ __forceinline__ int bcast_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ float bcast_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// One wave per token; lanes cover 8 consecutive bf16 (16 bytes) of the row,
+// in NC chunks of 512 columns starting at column c0.  The token's rows are taken kAggBatch at a time
+// without branches: lanes 0..7 fetch the batch's row indices and weights
+// (padding slots clamped to the token's last row, weight 0) and broadcast
+// them, then the row loads of every chunk are issued before any is
+// accumulated, so a lane keeps NC * kAggBatch HBM reads in flight.
+template <int NC>
 __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__ Y, const int32_t* __restrict__ tok_offsets,
                                                     const int32_t* __restrict__ tok_rows, const float* __restrict__ row_w,
-                                                    uint16_t* __restrict__ O, int T, int d) {
+                                                    uint16_t* __restrict__ O, int T, int d, int c0) {
   // wave-uniform token: row indices and weights become scalar loads
   const int t = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = lane_id();
   const int j0 = tok_offsets[t], j1 = tok_offsets[t + 1];
-  for (int c = lane * 8; c < d; c += 512) {
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int jb = j0; jb < j1; jb += kAggBatch) {
-      u32x4 v[kAggBatch];
-      float w[kAggBatch];
+  float acc[NC][8];
 #pragma unroll
-      for (int u = 0; u < kAggBatch; ++u) {
-        if (jb + u < j1) {
-          const int r = tok_rows[jb + u];
-          w[u] = row_w[r];
-          v[u] = *(const u32x4*)(Y + (size_t)r * d + c);
-        } else {
-          w[u] = 0.f;
-          v[u] = u32x4{0u, 0u, 0u, 0u};
-        }
-      }
+  for (int ci = 0; ci < NC; ++ci)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) acc[ci][q] = 0.f;
+  for (int jb = j0; jb < j1; jb += kAggBatch) {
+    const int slot = jb + (lane & 7);
+    const int rl = tok_rows[min(slot, j1 - 1)];
+    const float wl = slot < j1 ? row_w[rl] : 0.f;
+    int r[kAggBatch];
+    float w[kAggBatch];
+#pragma unroll
+    for (int u = 0; u < kAggBatch; ++u) {
+      r[u] = bcast_i(rl, u);
+      w[u] = bcast_f(wl, u);
+    }
+    u32x4 v[NC][kAggBatch];
+#pragma unroll
+    for (int ci = 0; ci < NC; ++ci) {
+      const int c = min(c0 + lane * 8 + 512 * ci, d - 8);  // lanes past the row end re-read its last chunk
+#pragma unroll
+      for (int u = 0; u < kAggBatch; ++u) v[ci][u] = *(const u32x4*)(Y + (size_t)r[u] * d + c);
+    }
+#pragma unroll
+    for (int ci = 0; ci < NC; ++ci)
 #pragma unroll
       for (int u = 0; u < kAggBatch; ++u)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          acc[2 * q] += w[u] * bf_lo(v[u][q]);
-          acc[2 * q + 1] += w[u] * bf_hi(v[u][q]);
+          acc[ci][2 * q] += w[u] * bf_lo(v[ci][u][q]);
+          acc[ci][2 * q + 1] += w[u] * bf_hi(v[ci][u][q]);
         }
-    }
-    u32x4 o;
+  }
 #pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[2 * q], acc[2 * q + 1]);
-    *(u32x4*)(O + (size_t)t * d + c) = o;
+  for (int ci = 0; ci < NC; ++ci) {
+    const int c = c0 + lane * 8 + 512 * ci;
+    if (c < d) {
+      u32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[ci][2 * q], acc[ci][2 * q + 1]);
+      *(u32x4*)(O + (size_t)t * d + c) = o;
+    }
   }
 }
 
 // dX_t = sum over the token's rows of dX~ + sum_j dl_j W_r[:, e_j], with the
 // router gradient on the token's selected set dl_j = s_j (dS_j - sum_k s_k dS_k).
 // Also writes the dense router-logit gradient row dL[t, :] (bf16) for dW_r.
+// W_r^T [E][d] is a bf16 copy (exact: W_r is bf16), so each row term is one
+// 16-byte load per lane; a batch's dX~ rows and W_r^T rows are all requested
+// before any is accumulated.
 __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict__ dXt, const float* __restrict__ dS,
-                                                     const float* __restrict__ WrT, const int32_t* __restrict__ tok_offsets,
+                                                     const uint16_t* __restrict__ WrT,
+                                                     const int32_t* __restrict__ tok_offsets,
                                                      const int32_t* __restrict__ tok_rows,
                                                      const int32_t* __restrict__ row_expert,
                                                      const float* __restrict__ row_w, uint16_t* __restrict__ dX,
@@ -79,29 +107,39 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
   for (int c = lane * 8; c < d; c += 512) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int jb = j0; jb < j1; jb += kAggBatch) {
+      // slot lane&7 of the batch: one vector load per level, then broadcast
+      const int slot = jb + (lane & 7);
+      const int rl = tok_rows[min(slot, j1 - 1)];
+      const int el = WrT ? row_expert[rl] : 0;
+      const float dll = (WrT && slot < j1) ? row_w[rl] * (dS[rl] - g) : 0.f;
+      int r[kAggBatch];
+#pragma unroll
+      for (int u = 0; u < kAggBatch; ++u) r[u] = bcast_i(rl, u);
       u32x4 v[kAggBatch];
 #pragma unroll
-      for (int u = 0; u < kAggBatch; ++u)
-        v[u] = (jb + u < j1) ? *(const u32x4*)(dXt + (size_t)tok_rows[jb + u] * d + c) : u32x4{0u, 0u, 0u, 0u};
+      for (int u = 0; u < kAggBatch; ++u) v[u] = *(const u32x4*)(dXt + (size_t)r[u] * d + c);
+      float keep[kAggBatch];
+#pragma unroll
+      for (int u = 0; u < kAggBatch; ++u) keep[u] = jb + u < j1 ? 1.f : 0.f;  // padding slots re-read the last row
 #pragma unroll
       for (int u = 0; u < kAggBatch; ++u)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          acc[2 * q] += bf_lo(v[u][q]);
-          acc[2 * q + 1] += bf_hi(v[u][q]);
+          acc[2 * q] += keep[u] * bf_lo(v[u][q]);
+          acc[2 * q + 1] += keep[u] * bf_hi(v[u][q]);
         }
-    }
-    if (WrT) {
-      for (int j = j0; j < j1; ++j) {
-        const int r = tok_rows[j];
-        const float dl = row_w[r] * (dS[r] - g);
-        const float* wr = WrT + (size_t)row_expert[r] * d + c;
-        const f32x4 a = *(const f32x4*)wr;
-        const f32x4 b = *(const f32x4*)(wr + 4);
+      if (WrT) {
+        u32x4 wv[kAggBatch];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[q] += dl * a[q];
-          acc[4 + q] += dl * b[q];
+        for (int u = 0; u < kAggBatch; ++u) wv[u] = *(const u32x4*)(WrT + (size_t)bcast_i(el, u) * d + c);
+#pragma unroll
+        for (int u = 0; u < kAggBatch; ++u) {
+          const float dl = bcast_f(dll, u);  // 0 for padding slots
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            acc[2 * q] += dl * bf_lo(wv[u][q]);
+            acc[2 * q + 1] += dl * bf_hi(wv[u][q]);
+          }
         }
       }
     }
@@ -142,13 +180,13 @@ __global__ __launch_bounds__(256) void reduce_rowparts_kernel(const float* __res
   out[i] = s;
 }
 
-// WrT[e][i] = W_r[i][e] as fp32
-__global__ __launch_bounds__(256) void transpose_wr_kernel(const uint16_t* __restrict__ Wr, float* __restrict__ WrT, int d,
-                                                           int E) {
+// WrT[e][i] = W_r[i][e] (bf16 copy)
+__global__ __launch_bounds__(256) void transpose_wr_kernel(const uint16_t* __restrict__ Wr, uint16_t* __restrict__ WrT,
+                                                           int d, int E) {
   const int idx = blockIdx.x * 256 + threadIdx.x;
   if (idx >= d * E) return;
   const int e = idx / d, i = idx % d;
-  WrT[idx] = bf2f(Wr[(size_t)i * E + e]);
+  WrT[idx] = Wr[(size_t)i * E + e];
 }
 
 // dbias[e] = sum_t dL[t][e] in two fixed-order passes: per chunk of
@@ -178,11 +216,18 @@ __global__ __launch_bounds__(256) void colsum_parts_kernel(const float* __restri
 }
 
 hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s) {
-  agg_o_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>(Y, r.tok_offsets, r.tok_rows, r.row_w, O, T, d);
+  const dim3 grid((T + 3) / 4), block(256);
+  const int nc = (d + 511) / 512;
+  if (nc <= 1) agg_o_kernel<1><<<grid, block, 0, s>>>(Y, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, 0);
+  else if (nc == 2) agg_o_kernel<2><<<grid, block, 0, s>>>(Y, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, 0);
+  else if (nc == 3) agg_o_kernel<3><<<grid, block, 0, s>>>(Y, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, 0);
+  else  // rows wider than 1536: 2048-column slices, one launch each
+    for (int c0 = 0; c0 < d; c0 += 2048)
+      agg_o_kernel<4><<<grid, block, 0, s>>>(Y, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, c0);
   return hipGetLastError();
 }
 
-hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const float* WrT, const moe_routing& r, uint16_t* dX,
+hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const uint16_t* WrT, const moe_routing& r, uint16_t* dX,
                          uint16_t* dL, int T, int d, int E, hipStream_t s) {
   agg_dx_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>(dXt, dS, WrT, r.tok_offsets, r.tok_rows, r.row_expert, r.row_w,
                                                         dX, dL, T, d, E);
@@ -199,7 +244,7 @@ hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int p
   return hipGetLastError();
 }
 
-hipError_t launch_transpose_wr(const uint16_t* Wr, float* WrT, int d, int E, hipStream_t s) {
+hipError_t launch_transpose_wr(const uint16_t* Wr, uint16_t* WrT, int d, int E, hipStream_t s) {
   transpose_wr_kernel<<<dim3((d * E + 255) / 256), dim3(256), 0, s>>>(Wr, WrT, d, E);
   return hipGetLastError();
 }

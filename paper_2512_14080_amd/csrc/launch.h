@@ -65,11 +65,11 @@ hipError_t launch_dwr(const DWrArgs& a, hipStream_t s);
 
 // aggregation and small kernels
 hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s);
-hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const float* WrT, const moe_routing& r, uint16_t* dX,
+hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const uint16_t* WrT, const moe_routing& r, uint16_t* dX,
                          uint16_t* dL, int T, int d, int E, hipStream_t s);
 hipError_t launch_reduce_rows(const float* part, float* out, int rows, int parts, hipStream_t s);
 hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s);
-hipError_t launch_transpose_wr(const uint16_t* Wr, float* WrT, int d, int E, hipStream_t s);
+hipError_t launch_transpose_wr(const uint16_t* Wr, uint16_t* WrT, int d, int E, hipStream_t s);
 // dbias = column sums of dL [T][E]; part holds colsum_chunks(T) * E floats
 int colsum_chunks(int T);
 hipError_t launch_colsum_bf16(const uint16_t* dL, float* part, float* dbias, int T, int E, hipStream_t s);

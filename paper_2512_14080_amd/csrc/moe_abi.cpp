@@ -84,7 +84,7 @@ struct BwdWs {
   float* dS;
   float* dS_part;
   uint16_t* dL;
-  float* WrT;
+  uint16_t* WrT;
   float* dWr_part;
   float* dbias_part;
 };
@@ -111,7 +111,7 @@ size_t bwd_layout(const moe_dims& m, int64_t cap, char* base, BwdWs* w) {
   off = carve(base, off, (size_t)cap * 4, w ? (void**)&w->dS : nullptr);
   off = carve(base, off, nnt > 1 ? (size_t)cap * nnt * 4 : 0, w ? (void**)&w->dS_part : nullptr);
   off = carve(base, off, (size_t)m.T * m.E * 2, w ? (void**)&w->dL : nullptr);
-  off = carve(base, off, (size_t)m.E * m.d * 4, w ? (void**)&w->WrT : nullptr);
+  off = carve(base, off, (size_t)m.E * m.d * 2, w ? (void**)&w->WrT : nullptr);
   off = carve(base, off, (size_t)splits * m.d * m.E * 4, w ? (void**)&w->dWr_part : nullptr);
   off = carve(base, off, (size_t)smoe::colsum_chunks(m.T) * m.E * 4, w ? (void**)&w->dbias_part : nullptr);
   return off;
