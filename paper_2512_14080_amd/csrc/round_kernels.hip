@@ -85,6 +85,7 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
                                                                 const int32_t* __restrict__ need_arr, int T, int W) {
   constexpr int kWaves = kSelThreads / 64;
   __shared__ int lds[kWaves];
+  __shared__ int cnt_lds[2][kWaves];  // per-wave counts of a pass, double-buffered by pass parity
   const int e = blockIdx.x;
   const uint64_t* src = tc_mask + (size_t)e * W;
   uint64_t* dst = tr_mask + (size_t)e * W;
@@ -137,7 +138,11 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
       asm volatile("" ::: "memory");  // keep the next batch's loads after this one
     }
   }
-  // number of candidates in the block whose key k has (k >> sh) == v
+  // number of candidates in the block whose key k has (k >> sh) == v.  One
+  // barrier per call: the counts of consecutive calls go to alternating slots,
+  // and a slot is only rewritten after the next call's barrier, which every
+  // wave reaches after reading it.
+  int parity = 0;
   auto count_eq = [&](uint32_t v, int sh) -> int {
     int cnt = 0;
     if constexpr (KPT > 0) {
@@ -150,12 +155,12 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
         cnt += __popcll(__ballot(c && (k >> sh) == v));
       }
     }
-    if (lane == 0) lds[wave] = cnt;
+    if (lane == 0) cnt_lds[parity][wave] = cnt;
     __syncthreads();
     int total = 0;
 #pragma unroll
-    for (int q = 0; q < kWaves; ++q) total += lds[q];
-    __syncthreads();
+    for (int q = 0; q < kWaves; ++q) total += cnt_lds[parity][q];
+    parity ^= 1;
     return total;
   };
 
@@ -164,15 +169,63 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
   // hold `remaining` keys, else count them as taken and clear it.
   uint32_t prefix = 0;
   int remaining = need;
-  for (int bit = 31; bit >= 0; --bit) {
-    const int total = count_eq((prefix >> bit) | 1u, bit);
-    if (total >= remaining)
-      prefix |= 1u << bit;
-    else
-      remaining -= total;
+  int nties;
+  if constexpr (KPT > 0) {
+    // Register form: bit i of `alive` marks key i as a candidate that still
+    // matches the prefix.  After the first few bits (sign, exponent) only a
+    // few keys survive, and slots dead in the whole wave are skipped.
+    uint32_t alive = (uint32_t)cmask;
+    auto block_total = [&](int cnt) {
+      if (lane == 0) cnt_lds[parity][wave] = cnt;
+      __syncthreads();
+      int total = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) total += cnt_lds[parity][q];
+      parity ^= 1;
+      return total;
+    };
+    auto wave_alive = [&]() {
+      uint32_t x = alive;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) x |= (uint32_t)__shfl_xor((int)x, o, kWave);
+      return (uint32_t)__builtin_amdgcn_readfirstlane((int)x);
+    };
+    for (int bit = 31; bit >= 0; --bit) {
+      const uint32_t any = wave_alive();
+      int cnt = 0;
+      uint32_t hit = 0;
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        if ((any >> i) & 1u) {
+          const bool h = ((alive >> i) & 1u) && ((keys[i] >> bit) & 1u);
+          cnt += __popcll(__ballot(h));
+          hit |= (uint32_t)h << i;
+        }
+      }
+      const int total = block_total(cnt);
+      if (total >= remaining) {
+        prefix |= 1u << bit;
+        alive &= hit;
+      } else {
+        remaining -= total;
+        alive &= ~hit;
+      }
+    }
+    int cnt = 0;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) cnt += __popcll(__ballot((alive >> i) & 1u));
+    nties = block_total(cnt);  // the survivors are exactly the keys equal to tau
+  } else {
+    for (int bit = 31; bit >= 0; --bit) {
+      const int total = count_eq((prefix >> bit) | 1u, bit);
+      if (total >= remaining)
+        prefix |= 1u << bit;
+      else
+        remaining -= total;
+    }
+    nties = count_eq(prefix, 0);
   }
   const uint32_t tau = prefix;
-  const int nties = count_eq(tau, 0);
 
   // Marking pass in ascending token order: slot i of wave w is word 16i + w.
   // Every candidate with key > tau flips; of the nties ties on tau, the
@@ -204,9 +257,34 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     __syncthreads();
   };
   if constexpr (KPT > 0) {
+    // Register form: all tie counts first (flat index slot * waves + wave),
+    // one block scan for every tie's rank base, then all flips.
+    __shared__ int tie_base[KPT * kWaves];
 #pragma unroll
-    for (int i = 0; i < KPT; ++i)
-      if (i < slots) mark(i, (cmask >> i) & 1ull, keys[i]);
+    for (int i = 0; i < KPT; ++i) {
+      const bool tie = ((cmask >> i) & 1ull) && keys[i] == tau;
+      const uint64_t ties = __ballot(tie);
+      if (lane == 0) tie_base[i * kWaves + wave] = __popcll(ties);
+    }
+    __syncthreads();
+    const int cnt = threadIdx.x < KPT * kWaves ? tie_base[threadIdx.x] : 0;
+    int all_ties;
+    const int ex = block_excl_scan<kSelThreads>(cnt, &all_ties, lds);
+    if (threadIdx.x < KPT * kWaves) tie_base[threadIdx.x] = ex;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      if (i >= slots) break;
+      const int w = i * kWaves + wave;
+      const bool cand = (cmask >> i) & 1ull;
+      const bool gt = cand && keys[i] > tau;
+      const bool tie = cand && keys[i] == tau;
+      const uint64_t ties = __ballot(tie);
+      const int rank = tie_base[w] + __popcll(ties & lanemask_lt());
+      const bool flip = gt || (tie && rank >= first_tie && rank < last_tie);
+      const uint64_t flips = __ballot(flip);
+      if (w < W && lane == 0) dst[w] = src[w] ^ flips;
+    }
   } else {
     for (int i = 0; i < slots; ++i) {
       bool c;

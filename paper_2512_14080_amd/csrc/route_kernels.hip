@@ -26,6 +26,10 @@ __device__ __forceinline__ uint32_t topk_key(float x) {
   if (b == 0x80000000u) b = 0;
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
+// inverse of topk_key (-0 comes back as +0)
+__device__ __forceinline__ float topk_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
 
 // Workgroup = 64 tokens (one membership word).  `in` and `scores` may alias
 // (logits overwritten in place by the scores).  With STASH, the scores are
@@ -96,34 +100,27 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
       sel_e[k] = 0;
       sel_v[k] = 0.f;
       if (k < K) {
-        float bv = 0.f;
-        uint32_t bk = 0;
-        int be = 0x7fffffff;
+        // (key, ~expert) packed in 64 bits: its maximum is the first expert by
+        // (score desc, expert asc); 0 marks "no candidate" (a real candidate's
+        // low word ~e is never 0)
+        uint64_t best = 0;
 #pragma unroll
         for (int j = 0; j < EPL; ++j) {
           const int e = lane + 64 * j;
           if (e < E && !((taken >> j) & 1u)) {
-            const uint32_t kj = topk_key(v[j]);
-            if (be == 0x7fffffff || kj > bk || (kj == bk && e < be)) {
-              bv = v[j];
-              bk = kj;
-              be = e;
-            }
+            const uint64_t c = ((uint64_t)topk_key(v[j]) << 32) | (uint32_t)~(uint32_t)e;
+            best = c > best ? c : best;
           }
         }
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) {
-          const float ov = __shfl_xor(bv, o, kWave);
-          const uint32_t ok = (uint32_t)__shfl_xor((int)bk, o, kWave);
-          const int oe = __shfl_xor(be, o, kWave);
-          // candidates without a valid expert carry index INT_MAX and lose
-          const bool better = (oe != 0x7fffffff) && (be == 0x7fffffff || ok > bk || (ok == bk && oe < be));
-          if (better) {
-            bv = ov;
-            bk = ok;
-            be = oe;
-          }
+          const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)best, o, kWave);
+          const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(best >> 32), o, kWave);
+          const uint64_t other = ((uint64_t)hi << 32) | lo;
+          best = other > best ? other : best;
         }
+        const int be = best ? (int)~(uint32_t)best : 0x7fffffff;
+        const float bv = topk_value((uint32_t)(best >> 32));
         if ((be & 63) == lane) taken |= 1u << (be >> 6);
         sel_e[k] = be;
         sel_v[k] = bv;
