@@ -61,6 +61,41 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
+// Wave reductions with DPP (no LDS): quad swaps, half-row and row mirrors,
+// then the row broadcasts; lane 63 ends with the result, which is read back
+// as a wave-uniform value.  Lanes that receive no value keep their own.
+template <int CTRL, int ROW_MASK, class T>
+__device__ __forceinline__ T dpp_mov(T v) {
+  if constexpr (sizeof(T) == 8) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const int lo = (int)(uint32_t)u, hi = (int)(uint32_t)(u >> 32);
+    const uint32_t nlo = (uint32_t)__builtin_amdgcn_update_dpp(lo, lo, CTRL, ROW_MASK, 0xf, false);
+    const uint32_t nhi = (uint32_t)__builtin_amdgcn_update_dpp(hi, hi, CTRL, ROW_MASK, 0xf, false);
+    return __builtin_bit_cast(T, ((uint64_t)nhi << 32) | nlo);
+  } else {
+    const int b = __builtin_bit_cast(int, v);
+    return __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(b, b, CTRL, ROW_MASK, 0xf, false));
+  }
+}
+
+template <class T, class Op>
+__device__ __forceinline__ T dpp_reduce(T x, Op op) {
+  x = op(x, dpp_mov<0xB1, 0xf>(x));   // quad_perm [1,0,3,2]
+  x = op(x, dpp_mov<0x4E, 0xf>(x));   // quad_perm [2,3,0,1]
+  x = op(x, dpp_mov<0x141, 0xf>(x));  // row_half_mirror
+  x = op(x, dpp_mov<0x140, 0xf>(x));  // row_mirror: every lane holds its row's value
+  x = op(x, dpp_mov<0x142, 0xa>(x));  // row_bcast:15 into rows 1 and 3
+  x = op(x, dpp_mov<0x143, 0xc>(x));  // row_bcast:31 into rows 2 and 3
+  if constexpr (sizeof(T) == 8) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, x);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+    return __builtin_bit_cast(T, ((uint64_t)hi << 32) | lo);
+  } else {
+    return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), 63));
+  }
+}
+
 // 64-bit value of lane l (wave-uniform l).  The readlane builtin works on
 // 32-bit ints: given a 64-bit argument it keeps only the sign-extended low
 // half, so the two halves are read separately.

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
       float m = -INFINITY;
 #pragma unroll
       for (int j = 0; j < EPL; ++j) m = fmaxf(m, v[j]);
-      m = wave_max(m);
+      m = dpp_reduce(m, [](float a, float b) { return fmaxf(a, b); });
       float s = 0.f;
 #pragma unroll
       for (int j = 0; j < EPL; ++j) {
@@ -69,7 +69,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
         v[j] = e < E ? expf(v[j] - m) : 0.f;
         s += v[j];
       }
-      s = wave_sum(s);
+      s = dpp_reduce(s, [](float a, float b) { return a + b; });
 #pragma unroll
       for (int j = 0; j < EPL; ++j) {
         const int e = lane + 64 * j;
@@ -112,13 +112,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
             best = c > best ? c : best;
           }
         }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)best, o, kWave);
-          const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(best >> 32), o, kWave);
-          const uint64_t other = ((uint64_t)hi << 32) | lo;
-          best = other > best ? other : best;
-        }
+        best = dpp_reduce(best, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
         const int be = best ? (int)~(uint32_t)best : 0x7fffffff;
         const float bv = topk_value((uint32_t)(best >> 32));
         if ((be & 63) == lane) taken |= 1u << (be >> 6);
@@ -126,22 +120,16 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
         sel_v[k] = bv;
       }
     }
-    // renormalisation denominator: selected scores summed in ascending expert order
+    // renormalisation denominator: selected scores summed in ascending expert
+    // order (expert 64j + l is value j of lane l; ballots list them in order)
     float denom = 0.f;
-    int last = -1;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      if (r < K) {
-        int nxt = 0x7fffffff;
-        float nv = 0.f;
-#pragma unroll
-        for (int k = 0; k < 16; ++k)
-          if (k < K && sel_e[k] > last && sel_e[k] < nxt) {
-            nxt = sel_e[k];
-            nv = sel_v[k];
-          }
-        denom += nv;
-        last = nxt;
+    for (int j = 0; j < EPL; ++j) {
+      uint64_t sel = __ballot((taken >> j) & 1u);
+      while (sel) {
+        const int l = __ffsll((unsigned long long)sel) - 1;
+        denom += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[j]), l));
+        sel &= sel - 1;
       }
     }
 #pragma unroll
