@@ -290,24 +290,43 @@ __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restr
   }
 }
 
-// Pass 2: rows of every token (expert ascending), renormalised weights.
-__global__ __launch_bounds__(64) void token_place_kernel(
+// Pass 2: rows of every token (expert ascending), renormalised weights.  The
+// kPlaceWaves waves of a workgroup share one word: wave q places experts
+// [q*Ew, (q+1)*Ew); it first counts its experts per token, and the counts of
+// the lower ranges (exchanged through LDS) give each token's first slot.
+constexpr int kPlaceWaves = 4;
+
+__global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
     const uint64_t* __restrict__ mask, const int32_t* __restrict__ prefix, const int32_t* __restrict__ offsets,
     const int32_t* __restrict__ tok_offsets, const float* __restrict__ scores_t, const float* __restrict__ denom,
     int32_t* __restrict__ tok_rows, int32_t* __restrict__ row_token, int32_t* __restrict__ row_expert,
     float* __restrict__ row_w, int T, int E, int W) {
+  __shared__ int cnt[kPlaceWaves][64];
   const int w = blockIdx.x;
   const int lane = lane_id();
+  const int q = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int t = w * 64 + lane;
   const bool live = t < T;
   const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
-  int j = live ? tok_offsets[t] : 0;
-  const float dn = live ? denom[t] : 1.f;
-  for (int c0 = 0; c0 < E; c0 += 64) {
+  const int ew = (E + kPlaceWaves - 1) / kPlaceWaves;
+  const int e_lo = min(E, q * ew), e_hi = min(E, e_lo + ew);
+  int c = 0;
+  for (int c0 = e_lo; c0 < e_hi; c0 += 64) {
     const int el = c0 + lane;
-    const uint64_t words = el < E ? mask[(size_t)el * W + w] : 0ull;
-    const int bases = el < E ? offsets[el] + prefix[(size_t)el * W + w] : 0;
-    const int n = min(64, E - c0);
+    const uint64_t words = el < e_hi ? mask[(size_t)el * W + w] : 0ull;
+    const int n = min(64, e_hi - c0);
+    for (int u = 0; u < n; ++u) c += (int)((readlane_u64(words, u) >> lane) & 1ull);
+  }
+  cnt[q][lane] = c;
+  __syncthreads();
+  int j = live ? tok_offsets[t] : 0;
+  for (int p = 0; p < q; ++p) j += cnt[p][lane];
+  const float dn = live ? denom[t] : 1.f;
+  for (int c0 = e_lo; c0 < e_hi; c0 += 64) {
+    const int el = c0 + lane;
+    const uint64_t words = el < e_hi ? mask[(size_t)el * W + w] : 0ull;
+    const int bases = el < e_hi ? offsets[el] + prefix[(size_t)el * W + w] : 0;
+    const int n = min(64, e_hi - c0);
     for (int j0 = 0; j0 < n; j0 += kMetaBatch) {
       float v[kMetaBatch];
       bool hit[kMetaBatch];
@@ -381,7 +400,7 @@ hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, i
   const dim3 wg(W), wb(64);
   token_count_kernel<<<wg, wb, 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, T, E, W);
   scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.tok_count, r.tok_offsets, T);
-  token_place_kernel<<<wg, wb, 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_offsets, scores_t, r.tok_denom,
+  token_place_kernel<<<wg, dim3(64 * kPlaceWaves), 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_offsets, scores_t, r.tok_denom,
                                        r.tok_rows, r.row_token, r.row_expert, r.row_w, T, E, W);
   return hipGetLastError();
 }
