@@ -537,6 +537,8 @@ using C128x64 = GemmCfg<128, 64, 4, 2, 3>;
 hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
   const int mt = (a.T + 255) / 256;
   if (a.E <= 64) return run<OpRouter<C256x64>>({a}, mt, s);
+  // 128-row tiles while 256-row tiles would leave CUs idle
+  if (a.E <= 128 && mt < 2 * cu_count()) return run<OpRouter<C128x128>>({a}, (a.T + 127) / 128, s);
   if (a.E <= 128) return run<OpRouter<C256x128>>({a}, mt, s);
   return run<OpRouter<C256x256>>({a}, mt * ((a.E + 255) / 256), s);
 }
@@ -597,7 +599,7 @@ hipError_t launch_dw1(const DW1Args& a, hipStream_t s) {
 
 int dwr_splits(int T, int d, int E) {
   const int tiles = (d / 128) * ((E + 127) / 128);
-  int s = (512 + tiles - 1) / tiles;  // aim for ~512 workgroups
+  int s = (256 + tiles - 1) / tiles;  // aim for one tile per CU
   const int max_s = (T + 255) / 256;  // at least 256 tokens per split
   if (s > max_s) s = max_s;
   return s < 1 ? 1 : s;

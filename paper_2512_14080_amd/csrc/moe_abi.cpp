@@ -159,7 +159,7 @@ size_t routing_layout(const moe_dims& m, int64_t cap, int flags, char* base, moe
   o->tok_denom = (float*)p;
   take((size_t)m.E * 4, &p);
   o->round_dir = (int32_t*)p;
-  take((size_t)(m.E + 64) * 4, &p);
+  take((size_t)(m.E + 64 + 2 * (W + 1)) * 4, &p);  // rounding needs [E], then per-word token sums and bases
   o->scratch = (int32_t*)p;
   o->capacity = (int32_t)cap;
   o->words = W;

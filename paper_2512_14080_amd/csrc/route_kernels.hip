@@ -260,7 +260,8 @@ constexpr int kMetaBatch = 8;
 
 __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restrict__ mask,
                                                          const float* __restrict__ scores_t, int32_t* __restrict__ cnt,
-                                                         float* __restrict__ denom, int T, int E, int W) {
+                                                         float* __restrict__ denom, int32_t* __restrict__ word_sum,
+                                                         int T, int E, int W) {
   const int w = blockIdx.x;
   const int lane = lane_id();
   const int t = w * 64 + lane;
@@ -288,6 +289,8 @@ __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restr
     cnt[t] = c;
     denom[t] = s;
   }
+  const int total = wave_sum(live ? c : 0);
+  if (lane == 0) word_sum[w] = total;  // rows of the word's 64 tokens
 }
 
 // Pass 2: rows of every token (expert ascending), renormalised weights.  The
@@ -298,9 +301,10 @@ constexpr int kPlaceWaves = 4;
 
 __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
     const uint64_t* __restrict__ mask, const int32_t* __restrict__ prefix, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tok_offsets, const float* __restrict__ scores_t, const float* __restrict__ denom,
-    int32_t* __restrict__ tok_rows, int32_t* __restrict__ row_token, int32_t* __restrict__ row_expert,
-    float* __restrict__ row_w, int T, int E, int W) {
+    const int32_t* __restrict__ tok_count, const int32_t* __restrict__ word_base, int32_t* __restrict__ tok_offsets,
+    const float* __restrict__ scores_t, const float* __restrict__ denom, int32_t* __restrict__ tok_rows,
+    int32_t* __restrict__ row_token, int32_t* __restrict__ row_expert, float* __restrict__ row_w, int T, int E,
+    int W) {
   __shared__ int cnt[kPlaceWaves][64];
   const int w = blockIdx.x;
   const int lane = lane_id();
@@ -319,7 +323,15 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
   }
   cnt[q][lane] = c;
   __syncthreads();
-  int j = live ? tok_offsets[t] : 0;
+  // token t's first row: the word's base (scan of the word sums) plus the
+  // rows of the word's earlier tokens; wave 0 also writes tok_offsets
+  const int ct = live ? tok_count[t] : 0;
+  const int tok_first = word_base[w] + wave_incl_scan(ct) - ct;
+  if (q == 0) {
+    if (live) tok_offsets[t] = tok_first;
+    if (w == W - 1 && lane == 0) tok_offsets[T] = word_base[W];
+  }
+  int j = tok_first;
   for (int p = 0; p < q; ++p) j += cnt[p][lane];
   const float dn = live ? denom[t] : 1.f;
   for (int c0 = e_lo; c0 < e_hi; c0 += 64) {
@@ -395,13 +407,15 @@ hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, hipStre
 
 hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, hipStream_t s) {
   const int W = r.words;
+  int32_t* word_sum = r.scratch + E + 64;  // [W]
+  int32_t* word_base = word_sum + W + 1;   // [W + 1]
   expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
   scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.counts, r.offsets, E);
-  const dim3 wg(W), wb(64);
-  token_count_kernel<<<wg, wb, 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, T, E, W);
-  scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.tok_count, r.tok_offsets, T);
-  token_place_kernel<<<wg, dim3(64 * kPlaceWaves), 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_offsets, scores_t, r.tok_denom,
-                                       r.tok_rows, r.row_token, r.row_expert, r.row_w, T, E, W);
+  token_count_kernel<<<dim3(W), dim3(64), 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, word_sum, T, E, W);
+  scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(word_sum, word_base, W);
+  token_place_kernel<<<dim3(W), dim3(64 * kPlaceWaves), 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_count, word_base,
+                                                                r.tok_offsets, scores_t, r.tok_denom, r.tok_rows,
+                                                                r.row_token, r.row_expert, r.row_w, T, E, W);
   return hipGetLastError();
 }
 
