@@ -17,11 +17,11 @@ layer) and in fp64 when ``dtype=np.float64`` is passed (used by the pins).
 from .routing import (router_logits, softmax_scores, topk_select, tc_membership,
                       routing_from_membership, round_tokens, route)
 from .layer import (swiglu, dswiglu, forward, backward, forward_tokens, backward_tokens,
-                    cached_bytes)
+                    weight_grad_columns, cached_bytes)
 
 __all__ = [
     "router_logits", "softmax_scores", "topk_select", "tc_membership",
     "routing_from_membership", "round_tokens", "route",
     "swiglu", "dswiglu", "forward", "backward", "forward_tokens", "backward_tokens",
-    "cached_bytes",
+    "weight_grad_columns", "cached_bytes",
 ]

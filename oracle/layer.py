@@ -200,6 +200,41 @@ def backward_tokens(dO, X, W1, W2, Wr, R, tokens, dtype=np.float32):
     return dX, rows_out, dS_out, dl_out
 
 
+def weight_grad_columns(dO, X, W1, W2, R, e, cols, dtype=np.float32):
+    """Columns of expert e's weight gradients from its routed rows only (for
+    sampled checks at sizes where the full backward is too slow).
+
+    For each j in cols (0 <= j < n), over the expert's rows (token t, score s):
+    h = [x_t W1_e[:, j], x_t W1_e[:, n+j]] (gate, up), a = SwiGLU(h),
+    dA'_j = dO_t W2_e[j, :]^T, dH = dSwiGLU(s dA'_j, h) -- the down-projection
+    backward of Section 3 and the up-projection backward of Appendix E
+    restricted to one column pair -- then
+    dW1_e[:, j] = X_e^T dH_gate, dW1_e[:, n+j] = X_e^T dH_up and
+    dW2_e[j, :] = (s a)^T dO_e.
+    Returns (dW1 columns [d, 2, len(cols)] as gate/up, dW2 rows [len(cols), d]).
+    """
+    X = np.asarray(X, dtype)
+    dO = np.asarray(dO, dtype)
+    n = W2.shape[1]
+    lo, hi = int(R.offsets[e]), int(R.offsets[e + 1])
+    tok = np.asarray(R.row_token[lo:hi], np.int64)
+    s = np.asarray(R.row_w[lo:hi], dtype)[:, None]
+    Xe, dOe = X[tok], dO[tok]
+    W1e, W2e = np.asarray(W1[e], dtype), np.asarray(W2[e], dtype)
+    d = X.shape[1]
+    dW1c = np.zeros((d, 2, len(cols)), dtype)
+    dW2r = np.zeros((len(cols), d), dtype)
+    for i, j in enumerate(cols):
+        H = np.stack([Xe @ W1e[:, j], Xe @ W1e[:, n + j]], axis=1)  # [rows, 2]: n = 1 column pair
+        a = swiglu(H)                                                # [rows, 1]
+        dAp = (dOe @ W2e[j, :])[:, None]
+        dH = dswiglu(s * dAp, H)
+        dW1c[:, 0, i] = Xe.T @ dH[:, 0]
+        dW1c[:, 1, i] = Xe.T @ dH[:, 1]
+        dW2r[i] = ((s * a)[:, 0]) @ dOe
+    return dW1c, dW2r
+
+
 def cached_bytes(T, d, n, P):
     """Activation bytes kept from forward to backward in bf16: X and H,
     2Td + 4Pn (Section 3.2; P = TK under TC)."""
