@@ -33,7 +33,8 @@
 //
 // The MFMA is issued as D = Nfrag x Mfrag, so a lane's accumulator holds one
 // m (lane % 32) and 16 n values in four runs of 4 consecutive columns; row
-// reductions (dS) stay mostly in-lane and stores are 8-byte runs per row.
+// reductions (dS) stay mostly in-lane; epilogues regroup the runs for
+// 16-byte (or, staged through LDS, whole-row) stores.
 #pragma once
 #include "device_common.h"
 

@@ -224,21 +224,109 @@ struct OpUp {
   }
 };
 
+// Row-contiguous stores of a wave's output: the two 32-column accumulator
+// blocks j, j+1 of one 32-row block (64 columns, 128 bytes of a bf16 row) go
+// through the wave's own 2 KB of LDS, 16 rows at a time, and come back so
+// that 8 lanes hold one 128-byte row segment.  Each store instruction then
+// writes 8 whole cache lines instead of 32-byte pieces of 32 rows.  The LDS
+// operations of one wave complete in order, so no barrier is needed; the
+// 16-byte chunk c of staged row r sits at chunk c ^ ((r >> 1) & 7), which
+// keeps both the writes (one chunk of 16 rows) and the reads (two whole
+// rows per 16 lanes) free of bank conflicts.
+constexpr int kStageBytesPerWave = 16 * 128;
+template <class Cfg>
+constexpr bool kStagedStores = Cfg::RN % 2 == 0 && Cfg::LDS_BYTES + Cfg::NW * kStageBytesPerWave + 256 <= 160 * 1024;
+// The lane index from a volatile asm: address arithmetic derived from it
+// stays in the epilogue instead of being hoisted out of the persistent tile
+// loop, where it would hold registers across the k loop.
+__device__ __forceinline__ int epilogue_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
+__device__ __forceinline__ void store_rows64_staged(char* wl, uint16_t* blk, int64_t ld, int rows_valid,
+                                                    const u32x2 (&v0)[4], const u32x2 (&v1)[4]) {
+  const int lane = epilogue_lane();
+  const int r = lane & 31, hi = lane >> 5;
+  u32x4 c[2][2];  // [block][g/2]: 16 bytes, chunk 4*block + g + hi of row r
+#pragma unroll
+  for (int g = 0; g < 4; g += 2) {
+    {
+      const auto a = __builtin_amdgcn_permlane32_swap(v0[g][0], v0[g + 1][0], false, false);
+      const auto b = __builtin_amdgcn_permlane32_swap(v0[g][1], v0[g + 1][1], false, false);
+      c[0][g / 2] = u32x4{a[0], b[0], a[1], b[1]};
+    }
+    {
+      const auto a = __builtin_amdgcn_permlane32_swap(v1[g][0], v1[g + 1][0], false, false);
+      const auto b = __builtin_amdgcn_permlane32_swap(v1[g][1], v1[g + 1][1], false, false);
+      c[1][g / 2] = u32x4{a[0], b[0], a[1], b[1]};
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    if ((r >> 4) == q) {
+      const int rr = r & 15;
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int g = 0; g < 4; g += 2) {
+          const int ch = 4 * b + g + hi;
+          *(u32x4*)(wl + rr * 128 + ((ch ^ ((rr >> 1) & 7)) << 4)) = c[b][g / 2];
+        }
+    }
+    // other lanes' data is read back: keep the compiler from reordering or
+    // forwarding across this point (the hardware keeps one wave's LDS
+    // operations in order)
+    asm volatile("" ::: "memory");
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int R = 8 * t + (lane >> 3), C = lane & 7;
+      const u32x4 x = *(const u32x4*)(wl + R * 128 + ((C ^ ((R >> 1) & 7)) << 4));
+      const int row = 16 * q + R;
+      if (row < rows_valid) *(u32x4*)(blk + (row * (int)ld + 8 * C)) = x;
+    }
+    asm volatile("" ::: "memory");  // reads of this round before the next round's writes
+  }
+}
+
 template <class Cfg>
 __device__ __forceinline__ void store_rows_bf16(uint16_t* out, int64_t ld, int row_base, int mrows, int n0,
-                                                Acc<Cfg>& t) {
+                                                Acc<Cfg>& t, char* epi) {
+  if constexpr (!kStagedStores<Cfg>) {
+#pragma unroll
+    for (int i = 0; i < Cfg::RM; ++i) {
+      const int m = t.m_of(i);
+      if (m >= mrows) continue;
+      uint16_t* y = out + (size_t)(row_base + m) * ld + n0;
+#pragma unroll
+      for (int j = 0; j < Cfg::RN; ++j) {
+        u32x2 v[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          v[g] = pack_bf16x4(t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
+        store_block_bf16(y + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1), v);
+      }
+    }
+    return;
+  }
+  char* wl = epi + (threadIdx.x >> 6) * kStageBytesPerWave;
+  const int wm0 = t.m_of(0) - (threadIdx.x & 31);
 #pragma unroll
   for (int i = 0; i < Cfg::RM; ++i) {
-    const int m = t.m_of(i);
-    if (m >= mrows) continue;
-    uint16_t* y = out + (size_t)(row_base + m) * ld + n0;
+    const int m0 = wm0 + 32 * i;  // first tile row of the block
+    if (m0 >= mrows) continue;
 #pragma unroll
-    for (int j = 0; j < Cfg::RN; ++j) {
-      u32x2 v[4];
+    for (int j = 0; j + 1 < Cfg::RN; j += 2) {
+      u32x2 v0[4], v1[4];
 #pragma unroll
-      for (int g = 0; g < 4; ++g)
-        v[g] = pack_bf16x4(t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
-      store_block_bf16(y + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1), v);
+      for (int g = 0; g < 4; ++g) {
+        v0[g] = pack_bf16x4(t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
+        v1[g] = pack_bf16x4(t.acc[i][j + 1][4 * g], t.acc[i][j + 1][4 * g + 1], t.acc[i][j + 1][4 * g + 2],
+                            t.acc[i][j + 1][4 * g + 3]);
+      }
+      const int col = n0 + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1);
+      store_rows64_staged(wl, out + (size_t)(row_base + m0) * ld + col, ld, mrows - m0, v0, v1);
     }
   }
 }
@@ -249,7 +337,7 @@ struct OpDown {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
   struct Params { DownArgs a; };
-  static constexpr int EPI_LDS = 0;
+  static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
   }
@@ -263,8 +351,8 @@ struct OpDown {
     const uint16_t* w = p.a.W2 + (size_t)ti.e * p.a.n * p.a.d;
     s.init(w, p.a.d, nullptr, 0, p.a.n, p.a.d, ColOffset{ti.n0});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
-    store_rows_bf16<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t);
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
+    store_rows_bf16<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
   }
 };
 
@@ -294,8 +382,12 @@ struct OpDH {
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* smem) {
     constexpr int RM = Cfg::RM, RN = Cfg::RN;
     const int n = p.a.n;
-    const int lane = threadIdx.x & 63;
+    const int lane = epilogue_lane();
     const int wn = t.wave_n();
+    const int wm0 = ((threadIdx.x >> 6) % Cfg::WM) * (Cfg::BM / Cfg::WM);
+    auto m_of = [&](int i) { return wm0 + 32 * i + (lane & 31); };
+    // first column of accumulator block j
+    auto col_of = [&](int j) { return ti.n0 + wn * (Cfg::BN / Cfg::WN) + 32 * j; };
     float* red = (float*)smem;  // [BM][WN], the epilogue's own LDS
     // H values of one accumulator row block (gate and up halves) and the
     // row's routing score, double-buffered: the loads of block i+1 are in
@@ -303,13 +395,13 @@ struct OpDH {
     u32x2 hg[2][RN][4], hu[2][RN][4];
     float sw[2];
     auto load_block = [&](int i, int b) {
-      const int m = t.m_of(i);
+      const int m = m_of(i);
       const size_t row = (size_t)(ti.row_base + (m < ti.mrows ? m : 0));
       const uint16_t* h = p.a.H + row * (2 * n);
       sw[b] = p.a.row_w[row];
 #pragma unroll
       for (int j = 0; j < RN; ++j) {
-        const int col = ti.n0 + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1);  // first column of the block
+        const int col = col_of(j);
         load_block_bf16(h + col, hg[b][j]);
         load_block_bf16(h + n + col, hu[b][j]);
       }
@@ -319,7 +411,7 @@ struct OpDH {
     for (int i = 0; i < RM; ++i) {
       const int b = i & 1;
       if (i + 1 < RM) load_block(i + 1, b ^ 1);
-      const int m = t.m_of(i);
+      const int m = m_of(i);
       const bool valid = m < ti.mrows;
       const size_t row = (size_t)(ti.row_base + (valid ? m : 0));
       const float s = valid ? sw[b] : 0.f;
@@ -329,7 +421,7 @@ struct OpDH {
       if (valid) {
 #pragma unroll
         for (int j = 0; j < RN; ++j) {
-          const int col = ti.n0 + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1);
+          const int col = col_of(j);
           u32x2 vg[4], vu[4], va[4];
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
@@ -384,7 +476,7 @@ struct OpDXt {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DXtArgs a; };
-  static constexpr int EPI_LDS = 0;
+  static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
   }
@@ -398,8 +490,8 @@ struct OpDXt {
     // rows of W1_e [d][2n] are the d columns of dX~, with 2n contiguous
     s.init(p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, nullptr, ti.n0, Cfg::BN);
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
-    store_rows_bf16<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t);
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
+    store_rows_bf16<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
   }
 };
 
@@ -410,7 +502,7 @@ struct OpDW2 {
   using Cfg = Cfg_;
   static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW2Args a; };
-  static constexpr int EPI_LDS = 0;
+  static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
   static __device__ int count(const Params& p, int*) { return p.a.E * (p.a.n / Cfg::BM) * (p.a.d / Cfg::BN); }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
     return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.n, p.a.d, id, ti);
@@ -421,8 +513,8 @@ struct OpDW2 {
   static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dO, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.n0});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
-    store_rows_bf16<Cfg>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti.m0, Cfg::BM, ti.n0, t);
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
+    store_rows_bf16<Cfg>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti.m0, Cfg::BM, ti.n0, t, epi);
   }
 };
 
@@ -432,7 +524,7 @@ struct OpDW1 {
   using Cfg = Cfg_;
   static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW1Args a; };
-  static constexpr int EPI_LDS = 0;
+  static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
   static __device__ int count(const Params& p, int*) { return p.a.E * (p.a.d / Cfg::BM) * (2 * p.a.n / Cfg::BN); }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
     return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.d, 2 * p.a.n, id, ti);
@@ -443,8 +535,8 @@ struct OpDW1 {
   static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dH, 2 * p.a.n, nullptr, ti.k_begin, ti.k_len, 2 * p.a.n, ColOffset{ti.n0});
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
-    store_rows_bf16<Cfg>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, Cfg::BM, ti.n0, t);
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
+    store_rows_bf16<Cfg>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, Cfg::BM, ti.n0, t, epi);
   }
 };
 
