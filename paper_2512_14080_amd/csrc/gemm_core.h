@@ -36,6 +36,8 @@
 // reductions (dS) stay mostly in-lane; epilogues regroup the runs for
 // 16-byte (or, staged through LDS, whole-row) stores.
 #pragma once
+#include <type_traits>
+
 #include "device_common.h"
 
 namespace smoe {
@@ -91,6 +93,11 @@ struct GemmCfg {
   static_assert(RM >= 1 && RN >= 1 && BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "wave tile");
   static_assert(BM % 64 == 0 && BN % 64 == 0, "tile multiple of 64");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  // wave w owns rows wave_m(w) * BM/WM .. and columns wave_n(w) * BN/WN ..;
+  // waves w and w + 4 share a SIMD and sit in different row blocks, so a
+  // tile with only its first rows valid still keeps every SIMD busy
+  static __device__ __forceinline__ int wave_m(int w) { return w / WN; }
+  static __device__ __forceinline__ int wave_n(int w) { return w % WN; }
 };
 
 // ---------------------------------------------------------------- ROWS side
@@ -263,22 +270,29 @@ struct Acc {
   // tile-local coordinates of accumulator element (i, j, 4g..4g+3) of this lane
   __device__ __forceinline__ static int m_of(int i) {
     const int wave = threadIdx.x >> 6;
-    return (wave % Cfg::WM) * (Cfg::BM / Cfg::WM) + i * 32 + (threadIdx.x & 31);
+    return Cfg::wave_m(wave) * (Cfg::BM / Cfg::WM) + i * 32 + (threadIdx.x & 31);
   }
   __device__ __forceinline__ static int n_of(int j, int g) {
     const int wave = threadIdx.x >> 6;
-    return (wave / Cfg::WM) * (Cfg::BN / Cfg::WN) + j * 32 + 8 * g + 4 * ((threadIdx.x >> 5) & 1);
+    return Cfg::wave_n(wave) * (Cfg::BN / Cfg::WN) + j * 32 + 8 * g + 4 * ((threadIdx.x >> 5) & 1);
   }
-  __device__ __forceinline__ static int wave_n() { return (threadIdx.x >> 6) / Cfg::WM; }
+  __device__ __forceinline__ static int wave_n() { return Cfg::wave_n(threadIdx.x >> 6); }
 };
 
-// For varlen-M scheduling: find the expert e and its local m-tile for the
-// global m-tile index mt, where expert e owns ceil(count_e / BM) tiles.
-// Runs on wave 0; result broadcast through sh[0..3] (LDS).  Returns false if
-// mt is past the last tile.  The barrier waits for LDS only, so DMA loads in
-// flight stay in flight.
+// Varlen-M tiles come in two classes: the full m-tiles of every expert
+// (floor(count_e / BM) each, expert-major) and the partial last m-tile of
+// each expert with count_e % BM != 0.  The schedule runs the partial tiles
+// last: with their idle row blocks skipped they are the cheapest tiles, so
+// the final, ragged round of a launch is short.
+constexpr int kPartialTile = 1 << 30;  // flag on a tile id: index among the partial tiles
+
+// Find the expert e and the m-tile for index mt of its class (partial: mt
+// counts the experts that have a partial tile).  Runs on wave 0; result
+// broadcast through sh[0..3] (LDS).  Returns false if mt is past the class.
+// The barrier waits for LDS only, so DMA loads in flight stay in flight.
 template <int BM>
-__device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets, int E, int mt, int* sh, TileInfo& ti) {
+__device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets, int E, int mt, bool partial, int* sh,
+                                            TileInfo& ti) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
     int base = 0;
@@ -290,7 +304,7 @@ __device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets,
         off = offsets[e];
         cnt = offsets[e + 1] - off;
       }
-      const int nt = (cnt + BM - 1) / BM;
+      const int nt = partial ? (cnt % BM != 0) : cnt / BM;
       const int inc = wave_incl_scan(nt);
       const int start = base + inc - nt;
       const bool hit = (e < E) && (mt >= start) && (mt < start + nt);
@@ -298,8 +312,8 @@ __device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets,
       if (b) {
         const int src = __ffsll((unsigned long long)b) - 1;
         found_e = __shfl(e, src, kWave);
-        found_m0 = (mt - __shfl(start, src, kWave)) * BM;
         found_cnt = __shfl(cnt, src, kWave);
+        found_m0 = partial ? (found_cnt / BM) * BM : (mt - __shfl(start, src, kWave)) * BM;
         found_off = __shfl(off, src, kWave);
         break;
       }
@@ -321,43 +335,66 @@ __device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets,
   return true;
 }
 
-// Number of varlen-M m-tiles, sum_e ceil(count_e / BM), from wave 0 through sh[0].
+// Varlen-M m-tile counts from wave 0: sh[0] = all m-tiles, sum_e
+// ceil(count_e / BM), sh[1] = partial ones.  Returns sh[0].
 template <int BM>
 __device__ __forceinline__ int count_m_tiles(const int32_t* __restrict__ offsets, int E, int* sh) {
   if (threadIdx.x < 64) {
-    int total = 0;
-    for (int e = threadIdx.x; e < E; e += 64) total += (offsets[e + 1] - offsets[e] + BM - 1) / BM;
+    int total = 0, part = 0;
+    for (int e = threadIdx.x; e < E; e += 64) {
+      const int cnt = offsets[e + 1] - offsets[e];
+      total += (cnt + BM - 1) / BM;
+      part += cnt % BM != 0;
+    }
     total = wave_sum(total);
-    if (threadIdx.x == 0) sh[0] = total;
+    part = wave_sum(part);
+    if (threadIdx.x == 0) {
+      sh[0] = total;
+      sh[1] = part;
+    }
   }
   barrier_lds();
   return sh[0];
 }
 
 // Persistent schedule.  The grid holds one workgroup per CU, a multiple of 8,
-// and workgroup b runs on XCD b % 8 (round-robin dispatch).  The ntiles
-// logical tiles are cut into 8 contiguous ranges, one per XCD; the G/8
-// workgroups of an XCD take its range round-robin.  Tiles that run at the
-// same time on one XCD are then neighbours in the logical order (same
-// expert, shared operand rows in that XCD's L2), and every XCD gets the same
-// number of real tiles.
+// and workgroup b runs on XCD b % 8 (round-robin dispatch).  Tiles come in a
+// main class [0, nmain) and a tail class [nmain, ntiles) (the partial
+// varlen-M tiles; empty for other GEMMs).  Each class is cut into 8
+// contiguous ranges, one per XCD; XCD x runs its main range, then its tail
+// range, and its G/8 workgroups take that sequence round-robin.  Tiles that
+// run at the same time on one XCD are then neighbours in the logical order
+// (same expert, shared operand rows in that XCD's L2), every XCD gets the
+// same amount of work, and the tail tiles form the last rounds.  id() returns
+// main tiles as their index and tail tiles as kPartialTile | index in class.
 struct Sched {
-  int ntiles, per_xcd, gx, x, slot;
-  __device__ __forceinline__ void init(int n) {
-    ntiles = n;
-    per_xcd = (n + 7) >> 3;
+  int nmain, ntail, cm, ct, fx, hx, gx, x, slot;
+  __device__ __forceinline__ void init(int ntiles, int tail) {
+    ntail = tail;
+    nmain = ntiles - tail;
+    cm = (nmain + 7) >> 3;
+    ct = (ntail + 7) >> 3;
     gx = gridDim.x >> 3;
     x = blockIdx.x & 7;
     slot = blockIdx.x >> 3;
+    fx = max(0, min(cm, nmain - x * cm));
+    hx = max(0, min(ct, ntail - x * ct));
   }
   // logical id of this workgroup's k-th tile, or -1 when it has no more
   __device__ __forceinline__ int id(int k) const {
-    const int local = slot + k * gx;
-    if (local >= per_xcd) return -1;
-    const int l = x * per_xcd + local;
-    return l < ntiles ? l : -1;
+    const int l = slot + k * gx;
+    if (l < fx) return x * cm + l;
+    if (l < fx + hx) return kPartialTile | (x * ct + (l - fx));
+    return -1;
   }
 };
+
+// Ops with a tail class define  int count_tail(const Params&, const int* sh)
+// (called after count() with the same sh).
+template <class Op, class = void>
+struct HasCountTail : std::false_type {};
+template <class Op>
+struct HasCountTail<Op, std::void_t<decltype(&Op::count_tail)>> : std::true_type {};
 
 // The main loop shared by every GEMM.  Op supplies:
 //   using Cfg = GemmCfg<...>;  static constexpr int M_MODE, N_MODE, EPI_LDS;
@@ -379,9 +416,14 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   using NSide = typename SideT<Op::N_MODE, Cfg::BN, Cfg::BK, Cfg::NW>::type;
   constexpr int BM = Cfg::BM, BN = Cfg::BN, S = Cfg::STAGES, BK = Cfg::BK, SUB = Cfg::SUB;
   __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES + (Op::EPI_LDS > 0 ? Op::EPI_LDS : 16)];
-  __shared__ int sh[16];  // [0..3], [4..7]: tile lookups of even / odd k; [8]: tile count
+  __shared__ int sh[16];  // [0..3], [4..7]: tile lookups of even / odd k; [8..9]: tile counts
   Sched sched;
-  sched.init(Op::count(p, sh + 8));
+  {
+    const int ntiles = Op::count(p, sh + 8);
+    int tail = 0;
+    if constexpr (HasCountTail<Op>::value) tail = Op::count_tail(p, sh + 8);
+    sched.init(ntiles, tail);
+  }
   const int id = sched.id(0);
   TileInfo ti;
   // tile() may synchronise the workgroup: ids are workgroup-uniform
@@ -392,9 +434,12 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   Op::init_n(p, ti, ns);
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
   const int wave = threadIdx.x >> 6;
-  const int wm0 = (wave % Cfg::WM) * (BM / Cfg::WM);
-  const int wn0 = (wave / Cfg::WM) * (BN / Cfg::WN);
+  const int wm0 = Cfg::wave_m(wave) * (BM / Cfg::WM);
+  const int wn0 = Cfg::wave_n(wave) * (BN / Cfg::WN);
   constexpr int kPerStage = Cfg::QM + Cfg::QN;  // DMA ops per wave per stage
+  // weight-gradient GEMMs spread each stage's DMA over its sub-steps; the
+  // others issue it at once and let rowless waves skip their MFMAs
+  constexpr bool kSpreadDma = Op::M_MODE == KOUTER && Op::N_MODE == KOUTER;
 
   // stages 0 .. S-2 of a tile, and the row indices of stage S-1 (gathered k)
   auto prologue = [&](const TileInfo& t, MSide& a, NSide& b) {
@@ -430,6 +475,10 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
       Op::init_n(p, tn, ns_next);
     }
     const int nk = (ti.k_len + BK - 1) / BK;
+    // a wave whose rows all lie past the tile's valid rows skips its MFMAs
+    // (it still issues its share of the DMA and joins every barrier); the
+    // weight-gradient GEMMs (k outer on both sides) always have full tiles
+    const bool active = wm0 < ti.mrows;
     // gathered k rows: their index loads are younger than the DMA, so only a
     // full drain covers them
     bool gathered = false;
@@ -457,18 +506,7 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
       const char* ln = cur + Cfg::M_BYTES;
       // fragments of sub-step s+1 are read while the MFMAs of sub-step s issue
       bf16x8 fm[2][Cfg::RM], fn[2][Cfg::RN];
-#pragma unroll
-      for (int i = 0; i < Cfg::RM; ++i) fm[0][i] = MSide::frag(lm, wm0 + 32 * i, 0);
-#pragma unroll
-      for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = NSide::frag(ln, wn0 + 32 * j, 0);
-#pragma unroll
-      for (int s = 0; s < SUB; ++s) {
-        // the next stage's DMA is spread over the sub-steps so the
-        // vector-memory issue does not stall the MFMA stream in one burst
-        if (issue_next) {
-          ms.issue(st_next, knext * BK, s, SUB);
-          ns.issue(st_next + Cfg::M_BYTES, knext * BK, s, SUB);
-        }
+      auto mfma_substep = [&](int s) {
         const int cb = s & 1, nb = cb ^ 1;
         if (s + 1 < SUB) {
 #pragma unroll
@@ -481,6 +519,36 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
 #pragma unroll
           for (int j = 0; j < Cfg::RN; ++j)
             acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[cb][j], fm[cb][i], acc.acc[i][j], 0, 0, 0);
+      };
+      auto first_frags = [&]() {
+#pragma unroll
+        for (int i = 0; i < Cfg::RM; ++i) fm[0][i] = MSide::frag(lm, wm0 + 32 * i, 0);
+#pragma unroll
+        for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = NSide::frag(ln, wn0 + 32 * j, 0);
+      };
+      if constexpr (kSpreadDma) {
+        // the next stage's DMA is spread over the sub-steps so the
+        // vector-memory issue does not stall the MFMA stream in one burst
+        first_frags();
+#pragma unroll
+        for (int s = 0; s < SUB; ++s) {
+          if (issue_next) {
+            ms.issue(st_next, knext * BK, s, SUB);
+            ns.issue(st_next + Cfg::M_BYTES, knext * BK, s, SUB);
+          }
+          mfma_substep(s);
+        }
+      } else {
+        // the whole next stage is requested first: it has the full step to land
+        if (issue_next) {
+          ms.issue(st_next, knext * BK);
+          ns.issue(st_next + Cfg::M_BYTES, knext * BK);
+        }
+        if (active) {
+          first_frags();
+#pragma unroll
+          for (int s = 0; s < SUB; ++s) mfma_substep(s);
+        }
       }
       if (issue_next) {
         if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * BK);

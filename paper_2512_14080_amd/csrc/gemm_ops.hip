@@ -59,14 +59,17 @@ __device__ __forceinline__ u32x2 pack_bf16x4(float a, float b, float c, float d)
 
 
 // ---------------------------------------------------------------- scheduling
-// Logical tile ids are m-tile-major: id = mt * (N / BN) + nt, so neighbouring
-// ids share the rows of one m-tile and the weights of one expert.
+// Logical tile ids are m-tile-major within their class (full m-tiles, then
+// the partial ones): id = mt * (N / BN) + nt, so neighbouring ids share the
+// rows of one m-tile and the weights of one expert.
 template <int BM, int BN>
 __device__ __forceinline__ bool tile_varlen_m(const int32_t* offsets, int E, int N, int K, int id, int* sh,
                                               TileInfo& ti) {
   const int nnt = N / BN;
+  const bool partial = (id & kPartialTile) != 0;
+  id &= kPartialTile - 1;
   const int mt = id / nnt, nt = id % nnt;
-  if (!find_m_tile<BM>(offsets, E, mt, sh, ti)) return false;
+  if (!find_m_tile<BM>(offsets, E, mt, partial, sh, ti)) return false;
   ti.n0 = nt * BN;
   ti.k_begin = 0;
   ti.k_len = K;
@@ -76,6 +79,11 @@ __device__ __forceinline__ bool tile_varlen_m(const int32_t* offsets, int E, int
 template <int BM, int BN>
 __device__ __forceinline__ int count_varlen_m(const int32_t* offsets, int E, int N, int* sh) {
   return count_m_tiles<BM>(offsets, E, sh) * (N / BN);
+}
+// tiles of the tail class (partial m-tiles), after count_varlen_m wrote sh
+template <int BN>
+__device__ __forceinline__ int count_varlen_m_tail(int N, const int* sh) {
+  return sh[1] * (N / BN);
 }
 
 template <int BM, int BN>
@@ -175,6 +183,9 @@ struct OpUp {
   static constexpr int EPI_LDS = 0;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, sh);
+  }
+  static __device__ int count_tail(const Params& p, const int* sh) {
+    return count_varlen_m_tail<Cfg::BN>(2 * p.a.n, sh);
   }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, p.a.d, id, sh, ti);
@@ -341,6 +352,9 @@ struct OpDown {
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
   }
+  static __device__ int count_tail(const Params& p, const int* sh) {
+    return count_varlen_m_tail<Cfg::BN>(p.a.d, sh);
+  }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, p.a.n, id, sh, ti);
   }
@@ -369,6 +383,9 @@ struct OpDH {
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, sh);
   }
+  static __device__ int count_tail(const Params& p, const int* sh) {
+    return count_varlen_m_tail<Cfg::BN>(p.a.n, sh);
+  }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, p.a.d, id, sh, ti);
   }
@@ -384,7 +401,7 @@ struct OpDH {
     const int n = p.a.n;
     const int lane = epilogue_lane();
     const int wn = t.wave_n();
-    const int wm0 = ((threadIdx.x >> 6) % Cfg::WM) * (Cfg::BM / Cfg::WM);
+    const int wm0 = Cfg::wave_m(threadIdx.x >> 6) * (Cfg::BM / Cfg::WM);
     auto m_of = [&](int i) { return wm0 + 32 * i + (lane & 31); };
     // first column of accumulator block j
     auto col_of = [&](int j) { return ti.n0 + wn * (Cfg::BN / Cfg::WN) + 32 * j; };
@@ -479,6 +496,9 @@ struct OpDXt {
   static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
+  }
+  static __device__ int count_tail(const Params& p, const int* sh) {
+    return count_varlen_m_tail<Cfg::BN>(p.a.d, sh);
   }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, 2 * p.a.n, id, sh, ti);
