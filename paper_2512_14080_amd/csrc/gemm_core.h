@@ -283,79 +283,9 @@ struct Acc {
 // (floor(count_e / BM) each, expert-major) and the partial last m-tile of
 // each expert with count_e % BM != 0.  The schedule runs the partial tiles
 // last: with their idle row blocks skipped they are the cheapest tiles, so
-// the final, ragged round of a launch is short.
+// the final, ragged round of a launch is short.  The m-tile list itself is
+// built once per forward / backward call (mtiles_kernel).
 constexpr int kPartialTile = 1 << 30;  // flag on a tile id: index among the partial tiles
-
-// Find the expert e and the m-tile for index mt of its class (partial: mt
-// counts the experts that have a partial tile).  Runs on wave 0; result
-// broadcast through sh[0..3] (LDS).  Returns false if mt is past the class.
-// The barrier waits for LDS only, so DMA loads in flight stay in flight.
-template <int BM>
-__device__ __forceinline__ bool find_m_tile(const int32_t* __restrict__ offsets, int E, int mt, bool partial, int* sh,
-                                            TileInfo& ti) {
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    int base = 0;
-    int found_e = -1, found_m0 = 0, found_cnt = 0, found_off = 0;
-    for (int e0 = 0; e0 < E; e0 += 64) {
-      const int e = e0 + lane;
-      int off = 0, cnt = 0;
-      if (e < E) {
-        off = offsets[e];
-        cnt = offsets[e + 1] - off;
-      }
-      const int nt = partial ? (cnt % BM != 0) : cnt / BM;
-      const int inc = wave_incl_scan(nt);
-      const int start = base + inc - nt;
-      const bool hit = (e < E) && (mt >= start) && (mt < start + nt);
-      const uint64_t b = __ballot(hit);
-      if (b) {
-        const int src = __ffsll((unsigned long long)b) - 1;
-        found_e = __shfl(e, src, kWave);
-        found_cnt = __shfl(cnt, src, kWave);
-        found_m0 = partial ? (found_cnt / BM) * BM : (mt - __shfl(start, src, kWave)) * BM;
-        found_off = __shfl(off, src, kWave);
-        break;
-      }
-      base += __shfl(inc, 63, kWave);
-    }
-    if (lane == 0) {
-      sh[0] = found_e;
-      sh[1] = found_m0;
-      sh[2] = found_cnt;
-      sh[3] = found_off;
-    }
-  }
-  barrier_lds();
-  ti.e = sh[0];
-  if (ti.e < 0) return false;
-  ti.m0 = sh[1];
-  ti.mrows = min(BM, sh[2] - sh[1]);
-  ti.row_base = sh[3] + sh[1];
-  return true;
-}
-
-// Varlen-M m-tile counts from wave 0: sh[0] = all m-tiles, sum_e
-// ceil(count_e / BM), sh[1] = partial ones.  Returns sh[0].
-template <int BM>
-__device__ __forceinline__ int count_m_tiles(const int32_t* __restrict__ offsets, int E, int* sh) {
-  if (threadIdx.x < 64) {
-    int total = 0, part = 0;
-    for (int e = threadIdx.x; e < E; e += 64) {
-      const int cnt = offsets[e + 1] - offsets[e];
-      total += (cnt + BM - 1) / BM;
-      part += cnt % BM != 0;
-    }
-    total = wave_sum(total);
-    part = wave_sum(part);
-    if (threadIdx.x == 0) {
-      sh[0] = total;
-      sh[1] = part;
-    }
-  }
-  barrier_lds();
-  return sh[0];
-}
 
 // Persistent schedule.  The grid holds one workgroup per CU, a multiple of 8,
 // and workgroup b runs on XCD b % 8 (round-robin dispatch).  Tiles come in a

@@ -59,31 +59,110 @@ __device__ __forceinline__ u32x2 pack_bf16x4(float a, float b, float c, float d)
 
 
 // ---------------------------------------------------------------- scheduling
+// ---------------------------------------------------------------- m-tile list
+// The varlen-M m-tiles (BM = kMTile rows) as a list, built on the device from
+// the expert offsets: int32 header {all m-tiles, partial m-tiles, 0, 0}, then
+// one {expert, m0, rows, first global row} entry per m-tile, the full tiles
+// of every expert in expert order first and the partial last tiles after
+// them.  A GEMM workgroup reads its tile's entry with one scalar load.
+constexpr int kMTile = 256;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+#define SMOE_CONST __attribute__((address_space(4)))
+
+size_t mtiles_bytes(int64_t capacity, int E) { return 16 * (size_t)(1 + capacity / kMTile + E); }
+
+constexpr int kMTilesThreads = 1024;
+__global__ __launch_bounds__(kMTilesThreads) void mtiles_kernel(const int32_t* __restrict__ offsets, int E,
+                                                               int32_t* __restrict__ out) {
+  __shared__ int pf[4097], pp[4097];  // per-expert exclusive prefix of full / partial m-tiles
+  __shared__ int scan_lds[kMTilesThreads / 64];
+  const int tid = threadIdx.x;
+  // thread t owns experts 4t .. 4t+3 (E <= 4096)
+  int nf[4], np[4], sf = 0, sp = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    const int cnt = e < E ? offsets[e + 1] - offsets[e] : 0;
+    nf[q] = cnt / kMTile;
+    np[q] = cnt % kMTile != 0;
+    sf += nf[q];
+    sp += np[q];
+  }
+  int F, H;
+  int bf = block_excl_scan<kMTilesThreads>(sf, &F, scan_lds);
+  int bp = block_excl_scan<kMTilesThreads>(sp, &H, scan_lds);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    if (e < E) {
+      pf[e] = bf;
+      pp[e] = bp;
+    }
+    bf += nf[q];
+    bp += np[q];
+  }
+  if (tid == 0) {
+    pf[E] = F;
+    pp[E] = H;
+  }
+  __syncthreads();
+  if (tid == 0) *(i32x4*)out = i32x4{F + H, H, 0, 0};
+  for (int t = tid; t < F + H; t += kMTilesThreads) {
+    const bool part = t >= F;
+    const int key = part ? t - F : t;
+    const int* pre = part ? pp : pf;
+    // the expert e with pre[e] <= key < pre[e + 1]
+    int lo = 0, hi = E;  // pre[lo] <= key < pre[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (pre[mid] <= key) lo = mid; else hi = mid;
+    }
+    const int off = offsets[lo], cnt = offsets[lo + 1] - off;
+    const int m0 = part ? (cnt / kMTile) * kMTile : (key - pre[lo]) * kMTile;
+    *(i32x4*)(out + 4 + 4 * t) = i32x4{lo, m0, min(kMTile, cnt - m0), off + m0};
+  }
+}
+
+hipError_t launch_mtiles(const int32_t* offsets, int E, int32_t* out, hipStream_t s) {
+  if (E > 4096) return hipErrorInvalidValue;
+  mtiles_kernel<<<1, kMTilesThreads, 0, s>>>(offsets, E, out);
+  return hipGetLastError();
+}
+
 // Logical tile ids are m-tile-major within their class (full m-tiles, then
 // the partial ones): id = mt * (N / BN) + nt, so neighbouring ids share the
-// rows of one m-tile and the weights of one expert.
+// rows of one m-tile and the weights of one expert.  The list entry is
+// read with a scalar load (the id is workgroup-uniform).
 template <int BM, int BN>
-__device__ __forceinline__ bool tile_varlen_m(const int32_t* offsets, int E, int N, int K, int id, int* sh,
-                                              TileInfo& ti) {
+__device__ __forceinline__ bool tile_varlen_m(const int32_t* mtiles, int N, int K, int id, TileInfo& ti) {
+  static_assert(BM == kMTile, "varlen-M tiles are the m-tile list's tiles");
   const int nnt = N / BN;
   const bool partial = (id & kPartialTile) != 0;
   id &= kPartialTile - 1;
   const int mt = id / nnt, nt = id % nnt;
-  if (!find_m_tile<BM>(offsets, E, mt, partial, sh, ti)) return false;
+  const SMOE_CONST i32x4* list = (const SMOE_CONST i32x4*)mtiles;
+  const i32x4 h = list[0];
+  const int idx = partial ? h[0] - h[1] + mt : mt;
+  if (idx >= h[0]) return false;
+  const i32x4 t = list[1 + idx];
+  ti.e = t[0];
+  ti.m0 = t[1];
+  ti.mrows = t[2];
+  ti.row_base = t[3];
   ti.n0 = nt * BN;
   ti.k_begin = 0;
   ti.k_len = K;
   return true;
 }
 
-template <int BM, int BN>
-__device__ __forceinline__ int count_varlen_m(const int32_t* offsets, int E, int N, int* sh) {
-  return count_m_tiles<BM>(offsets, E, sh) * (N / BN);
-}
-// tiles of the tail class (partial m-tiles), after count_varlen_m wrote sh
 template <int BN>
-__device__ __forceinline__ int count_varlen_m_tail(int N, const int* sh) {
-  return sh[1] * (N / BN);
+__device__ __forceinline__ int count_varlen_m(const int32_t* mtiles, int N) {
+  return ((const SMOE_CONST i32x4*)mtiles)[0][0] * (N / BN);
+}
+// tiles of the tail class (partial m-tiles)
+template <int BN>
+__device__ __forceinline__ int count_varlen_m_tail(const int32_t* mtiles, int N) {
+  return ((const SMOE_CONST i32x4*)mtiles)[0][1] * (N / BN);
 }
 
 template <int BM, int BN>
@@ -182,13 +261,13 @@ struct OpUp {
   };
   static constexpr int EPI_LDS = 0;
   static __device__ int count(const Params& p, int* sh) {
-    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, sh);
+    return count_varlen_m<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
   }
   static __device__ int count_tail(const Params& p, const int* sh) {
-    return count_varlen_m_tail<Cfg::BN>(2 * p.a.n, sh);
+    return count_varlen_m_tail<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
   }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, 2 * p.a.n, p.a.d, id, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, 2 * p.a.n, p.a.d, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
@@ -350,13 +429,13 @@ struct OpDown {
   struct Params { DownArgs a; };
   static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
   static __device__ int count(const Params& p, int* sh) {
-    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
+    return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.d);
   }
   static __device__ int count_tail(const Params& p, const int* sh) {
-    return count_varlen_m_tail<Cfg::BN>(p.a.d, sh);
+    return count_varlen_m_tail<Cfg::BN>(p.a.mtiles, p.a.d);
   }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, p.a.n, id, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, p.a.d, p.a.n, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.A, p.a.n, nullptr, ti.row_base, ti.mrows);
@@ -381,13 +460,13 @@ struct OpDH {
   struct Params { DHArgs a; };
   static constexpr int EPI_LDS = Cfg::BM * Cfg::WN * 4;  // dS partial sums [BM][WN]
   static __device__ int count(const Params& p, int* sh) {
-    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, sh);
+    return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.n);
   }
   static __device__ int count_tail(const Params& p, const int* sh) {
-    return count_varlen_m_tail<Cfg::BN>(p.a.n, sh);
+    return count_varlen_m_tail<Cfg::BN>(p.a.mtiles, p.a.n);
   }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.n, p.a.d, id, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, p.a.n, p.a.d, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dO, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
@@ -495,13 +574,13 @@ struct OpDXt {
   struct Params { DXtArgs a; };
   static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
   static __device__ int count(const Params& p, int* sh) {
-    return count_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, sh);
+    return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.d);
   }
   static __device__ int count_tail(const Params& p, const int* sh) {
-    return count_varlen_m_tail<Cfg::BN>(p.a.d, sh);
+    return count_varlen_m_tail<Cfg::BN>(p.a.mtiles, p.a.d);
   }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.E, p.a.d, 2 * p.a.n, id, sh, ti);
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, p.a.d, 2 * p.a.n, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.dH, 2 * p.a.n, nullptr, ti.row_base, ti.mrows);

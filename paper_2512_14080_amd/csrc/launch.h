@@ -22,26 +22,34 @@ struct RouterGemmArgs {
 };
 hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s);
 
+// The varlen-M m-tile list (mtiles_kernel): built from the expert offsets
+// once per forward / backward call, read by the up, down, dH and dX~ GEMMs.
+size_t mtiles_bytes(int64_t capacity, int E);
+hipError_t launch_mtiles(const int32_t* offsets, int E, int32_t* out, hipStream_t s);
+
 struct UpArgs {
   const uint16_t* X; const uint16_t* W1; const int32_t* offsets; const int32_t* row_token;
-  uint16_t* H; uint16_t* A; int d, n, E, capacity;
+  uint16_t* H; uint16_t* A; int d, n, E, capacity; const int32_t* mtiles;
 };
 hipError_t launch_up(const UpArgs& a, hipStream_t s);
 
 struct DownArgs {
   const uint16_t* A; const uint16_t* W2; const int32_t* offsets; uint16_t* Y; int d, n, E, capacity;
+  const int32_t* mtiles;
 };
 hipError_t launch_down(const DownArgs& a, hipStream_t s);
 
 struct DHArgs {
   const uint16_t* dO; const uint16_t* W2; const uint16_t* H; const int32_t* offsets; const int32_t* row_token;
   const float* row_w; uint16_t* dH; uint16_t* Ap; float* dS; float* dS_part; int d, n, E, capacity;
+  const int32_t* mtiles;
 };
 int dh_n_tiles(int n);
 hipError_t launch_dh(const DHArgs& a, hipStream_t s);
 
 struct DXtArgs {
   const uint16_t* dH; const uint16_t* W1; const int32_t* offsets; uint16_t* dXt; int d, n, E, capacity;
+  const int32_t* mtiles;
 };
 hipError_t launch_dxt(const DXtArgs& a, hipStream_t s);
 

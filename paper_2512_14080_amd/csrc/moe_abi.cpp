@@ -76,8 +76,10 @@ std::vector<std::pair<hipEvent_t, hipEvent_t>> g_prof_pool;     // free pairs
 struct FwdWs {
   uint16_t* A;
   uint16_t* Y;
+  int32_t* mtiles;
 };
 struct BwdWs {
+  int32_t* mtiles;
   uint16_t* dH;
   uint16_t* Ap;
   uint16_t* dXt;
@@ -98,6 +100,7 @@ size_t fwd_layout(const moe_dims& m, int64_t cap, char* base, FwdWs* w) {
   size_t off = 0;
   off = carve(base, off, (size_t)cap * m.n * 2, w ? (void**)&w->A : nullptr);
   off = carve(base, off, (size_t)cap * m.d * 2, w ? (void**)&w->Y : nullptr);
+  off = carve(base, off, smoe::mtiles_bytes(cap, m.E), w ? (void**)&w->mtiles : nullptr);
   return off;
 }
 
@@ -105,6 +108,7 @@ size_t bwd_layout(const moe_dims& m, int64_t cap, char* base, BwdWs* w) {
   const int nnt = smoe::dh_n_tiles(m.n);
   const int splits = smoe::dwr_splits(m.T, m.d, m.E);
   size_t off = 0;
+  off = carve(base, off, smoe::mtiles_bytes(cap, m.E), w ? (void**)&w->mtiles : nullptr);
   off = carve(base, off, (size_t)cap * 2 * m.n * 2, w ? (void**)&w->dH : nullptr);
   off = carve(base, off, (size_t)cap * m.n * 2, w ? (void**)&w->Ap : nullptr);
   off = carve(base, off, (size_t)cap * m.d * 2, w ? (void**)&w->dXt : nullptr);
@@ -331,9 +335,12 @@ int moe_fwd(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W
   FwdWs w;
   fwd_layout(m, r->capacity, (char*)ws, &w);
   hipStream_t stream = (hipStream_t)stream_;
+  HIP_TRY(smoe::launch_mtiles(r->offsets, m.E, w.mtiles, stream), "m-tile list");
   LAUNCH(MOE_KC_UP,
-         smoe::launch_up({X, W1, r->offsets, r->row_token, H, w.A, m.d, m.n, m.E, r->capacity}, stream), "up-proj");
-  LAUNCH(MOE_KC_DOWN, smoe::launch_down({w.A, W2, r->offsets, w.Y, m.d, m.n, m.E, r->capacity}, stream), "down-proj");
+         smoe::launch_up({X, W1, r->offsets, r->row_token, H, w.A, m.d, m.n, m.E, r->capacity, w.mtiles}, stream),
+         "up-proj");
+  LAUNCH(MOE_KC_DOWN, smoe::launch_down({w.A, W2, r->offsets, w.Y, m.d, m.n, m.E, r->capacity, w.mtiles}, stream),
+         "down-proj");
   LAUNCH(MOE_KC_AGG_O, smoe::launch_agg_o(w.Y, *r, O, m.T, m.d, stream), "aggregation");
   return MOE_OK;
 }
@@ -366,14 +373,16 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   hipStream_t stream = (hipStream_t)stream_;
   float* dS_out = dS ? dS : w.dS;
   const int nnt = smoe::dh_n_tiles(m.n);
+  HIP_TRY(smoe::launch_mtiles(r->offsets, m.E, w.mtiles, stream), "m-tile list");
   LAUNCH(MOE_KC_DH,
          smoe::launch_dh({dO, W2, H, r->offsets, r->row_token, r->row_w, w.dH, w.Ap, dS_out, w.dS_part, m.d, m.n, m.E,
-                          r->capacity},
+                          r->capacity, w.mtiles},
                          stream),
          "dH");
   if (nnt > 1) HIP_TRY(smoe::launch_reduce_rowparts(w.dS_part, dS_out, r->capacity, nnt, stream), "dS reduce");
   LAUNCH(MOE_KC_DW2, smoe::launch_dw2({w.Ap, dO, r->offsets, r->row_token, dW2, m.d, m.n, m.E}, stream), "dW2");
-  LAUNCH(MOE_KC_DXT, smoe::launch_dxt({w.dH, W1, r->offsets, w.dXt, m.d, m.n, m.E, r->capacity}, stream), "dX~");
+  LAUNCH(MOE_KC_DXT, smoe::launch_dxt({w.dH, W1, r->offsets, w.dXt, m.d, m.n, m.E, r->capacity, w.mtiles}, stream),
+         "dX~");
   LAUNCH(MOE_KC_DW1, smoe::launch_dw1({X, w.dH, r->offsets, r->row_token, dW1, m.d, m.n, m.E}, stream), "dW1");
   if (Wr) HIP_TRY(smoe::launch_transpose_wr(Wr, w.WrT, m.d, m.E, stream), "W_r transpose");
   LAUNCH(MOE_KC_AGG_DX,
