@@ -115,17 +115,34 @@ struct RowsSide {
   static constexpr int Q = R * BK / (NW * 512);  // instructions per wave
   static_assert(Q >= 1 && Q * NW * 512 == R * BK, "rows x k of a stage must be whole DMA instructions per wave");
   static __device__ __forceinline__ int swz(int r) { return BK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3); }
-  const char* ptr[Q];               // row start (k = 0) of the row this lane loads, per instruction
+  const char* ptr[Q];  // row start (k = 0) of the row this lane loads, per instruction (after commit)
+  const uint16_t* base_;
+  int64_t ld_;
+  int32_t row_[Q];     // the row this lane loads, per instruction
+  // The rows of a tile: gathered rows are loaded from idx here, but the row
+  // pointers are only formed in commit(), so a next tile's index loads stay
+  // in flight (behind the current tile's stages) instead of being waited for.
   __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, const int32_t* idx, int row_base, int nrows) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    base_ = base;
+    ld_ = ld;
+#pragma unroll
+    for (int j = 0; j < Q; ++j) {
+      const int lrow = RPI * (wave + NW * j) + lane / C;
+      const int r = min(lrow, nrows - 1);
+      row_[j] = idx ? idx[row_base + r] : row_base + r;
+    }
+  }
+  // Called where the index loads are known to be complete (after a full
+  // drain); the empty asm keeps the pointer arithmetic after that point.
+  __device__ __forceinline__ void commit() {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
-      const int q = wave + NW * j;
-      const int lrow = RPI * q + lane / C;
+      asm volatile("" : "+v"(row_[j]));
+      const int lrow = RPI * (wave + NW * j) + lane / C;
       const int logical = (lane % C) ^ swz(lrow);
-      const int r = min(lrow, nrows - 1);
-      const int64_t row = idx ? (int64_t)idx[row_base + r] : (int64_t)(row_base + r);
-      ptr[j] = (const char*)(base + row * ld) + logical * 16;
+      ptr[j] = (const char*)(base_ + (int64_t)row_[j] * ld_) + logical * 16;
     }
   }
   // instructions j with j % parts == part (so a stage can be issued in pieces)
@@ -186,6 +203,7 @@ struct KOuterSide {
       colb[j] = gc < cvalid ? gc * 2 : -1;
     }
   }
+  __device__ __forceinline__ void commit() {}
   // gathered operands: fetch the row indices of the stage at k0 (registers)
   __device__ __forceinline__ void prefetch_idx(int k0) {
     if (!gidx) return;
@@ -362,6 +380,8 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   NSide ns, ns_next;
   Op::init_m(p, ti, ms);
   Op::init_n(p, ti, ns);
+  ms.commit();
+  ns.commit();
   const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
   const int wave = threadIdx.x >> 6;
   const int wm0 = Cfg::wave_m(wave) * (BM / Cfg::WM);
@@ -487,6 +507,9 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
     }
     barrier_lds();  // every wave is done with the stage buffers
     if (idn >= 0) {
+      // the last step's full drain covered the next tile's index loads
+      ms_next.commit();
+      ns_next.commit();
       ms = ms_next;
       ns = ns_next;
       prologue(tn, ms, ns);
