@@ -32,31 +32,44 @@ __device__ __forceinline__ float topk_value(uint32_t k) {
 }
 
 // Workgroup = 64 tokens (one membership word).  `in` and `scores` may alias
-// (logits overwritten in place by the scores).  With STASH, the scores are
-// staged in LDS and written transposed (scores_t[e][t]) in 64-token runs.
+// (logits overwritten in place by the scores).  With STASH every output of the
+// workgroup's 64 tokens is staged in LDS and written at the end: the scores
+// (token-major and transposed, scores_t[e][t] in 64-token runs) and the top-K
+// lists.  With no global store pending while the token loop runs, the wait
+// for the next token's row (requested one token ahead) covers only loads.
+constexpr int kStashPitch = 65;  // floats per expert row of the stash (bank-conflict-free both ways)
 template <int EPL, bool STASH>
 __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float* scores, float* __restrict__ scores_t,
                                                          int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
                                                          uint64_t* __restrict__ mask, int T, int E, int K, int W,
                                                          int do_softmax) {
   extern __shared__ __attribute__((aligned(16))) char dyn[];
-  unsigned long long* mword = (unsigned long long*)dyn;      // [E]
-  float* st = (float*)(dyn + ((E * 8 + 15) & ~15));           // [E][64] when STASH
+  unsigned long long* mword = (unsigned long long*)dyn;                  // [E]
+  float* st = (float*)(dyn + ((E * 8 + 15) & ~15));                       // STASH: [E][kStashPitch]
+  int* sidx = (int*)(st + (STASH ? E * kStashPitch : 0));                 // STASH: [64][K]
+  float* sw = (float*)(sidx + (STASH ? 64 * K : 0));                      // STASH: [64][K]
   const int w = blockIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = lane_id();
   for (int e = threadIdx.x; e < E; e += kTopkWaves * 64) mword[e] = 0ull;
   __syncthreads();
-  for (int i = wave; i < 64; i += kTopkWaves) {
+  auto load_row = [&](int i, float (&v)[EPL]) {
     const int t = w * 64 + i;
-    if (t >= T) break;
-    const float* row = in + (size_t)t * E;
-    float v[EPL];
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
       const int e = lane + 64 * j;
-      v[j] = e < E ? row[e] : -INFINITY;
+      v[j] = (t < T && e < E) ? in[(size_t)t * E + e] : -INFINITY;
     }
+  };
+  float vn[EPL];
+  load_row(wave, vn);
+  for (int i = wave; i < 64; i += kTopkWaves) {
+    const int t = w * 64 + i;
+    if (t >= T) break;
+    float v[EPL];
+#pragma unroll
+    for (int j = 0; j < EPL; ++j) v[j] = vn[j];
+    if (i + kTopkWaves < 64) load_row(i + kTopkWaves, vn);  // the wave's next token, in flight meanwhile
     if (do_softmax) {
       float m = -INFINITY;
 #pragma unroll
@@ -75,23 +88,25 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
         const int e = lane + 64 * j;
         if (e < E) {
           v[j] = v[j] / s;
-          scores[(size_t)t * E + e] = v[j];
+          if (!STASH) scores[(size_t)t * E + e] = v[j];
         }
       }
     }
-    if (scores_t) {
+    if (STASH || scores_t) {
 #pragma unroll
       for (int j = 0; j < EPL; ++j) {
         const int e = lane + 64 * j;
         if (e < E) {
           if (STASH)
-            st[e * 64 + i] = v[j];
+            st[e * kStashPitch + i] = v[j];
           else
             scores_t[(size_t)e * T + t] = v[j];
         }
       }
     }
-    // K rounds of wave arg-max over (value desc, expert asc)
+    // K rounds of wave arg-max over (value desc, expert asc): the wave maximum
+    // of the 32-bit keys (a DPP max), then the lowest expert holding it from
+    // ballots (expert 64j + l is value j of lane l: lowest j, then lowest lane)
     uint32_t taken = 0;
     int sel_e[16];
     float sel_v[16];
@@ -100,24 +115,29 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
       sel_e[k] = 0;
       sel_v[k] = 0.f;
       if (k < K) {
-        // (key, ~expert) packed in 64 bits: its maximum is the first expert by
-        // (score desc, expert asc); 0 marks "no candidate" (a real candidate's
-        // low word ~e is never 0)
-        uint64_t best = 0;
+        uint32_t best = 0;
+        int bj = -1;  // j of this lane's best candidate (the lowest j on equal keys)
 #pragma unroll
         for (int j = 0; j < EPL; ++j) {
           const int e = lane + 64 * j;
           if (e < E && !((taken >> j) & 1u)) {
-            const uint64_t c = ((uint64_t)topk_key(v[j]) << 32) | (uint32_t)~(uint32_t)e;
-            best = c > best ? c : best;
+            const uint32_t c = topk_key(v[j]);
+            if (bj < 0 || c > best) {
+              best = c;
+              bj = j;
+            }
           }
         }
-        best = dpp_reduce(best, [](uint64_t a, uint64_t b) { return a > b ? a : b; });
-        const int be = best ? (int)~(uint32_t)best : 0x7fffffff;
-        const float bv = topk_value((uint32_t)(best >> 32));
-        if ((be & 63) == lane) taken |= 1u << (be >> 6);
+        const uint32_t m = dpp_reduce(bj >= 0 ? best : 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+        int be = 0x7fffffff;
+#pragma unroll
+        for (int j = 0; j < EPL; ++j) {
+          const uint64_t hit = __ballot(bj == j && best == m);
+          if (hit && be == 0x7fffffff) be = __ffsll((unsigned long long)hit) - 1 + 64 * j;
+        }
+        if (be != 0x7fffffff && (be & 63) == lane) taken |= 1u << (be >> 6);
         sel_e[k] = be;
-        sel_v[k] = bv;
+        sel_v[k] = topk_value(m);
       }
     }
     // renormalisation denominator: selected scores summed in ascending expert
@@ -135,18 +155,34 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
       if (k < K && lane == k) {
-        topk_idx[(size_t)t * K + k] = sel_e[k];
-        topk_w[(size_t)t * K + k] = sel_v[k] / denom;
+        if (STASH) {
+          sidx[i * K + k] = sel_e[k];
+          sw[i * K + k] = sel_v[k] / denom;
+        } else {
+          topk_idx[(size_t)t * K + k] = sel_e[k];
+          topk_w[(size_t)t * K + k] = sel_v[k] / denom;
+        }
         atomicOr(&mword[sel_e[k]], 1ull << i);
       }
     }
   }
   __syncthreads();
   for (int e = threadIdx.x; e < E; e += kTopkWaves * 64) mask[(size_t)e * W + w] = mword[e];
-  if (STASH && scores_t) {
-    for (int idx = threadIdx.x; idx < E * 64; idx += kTopkWaves * 64) {
-      const int e = idx >> 6, i = idx & 63;
-      if (w * 64 + i < T) scores_t[(size_t)e * T + w * 64 + i] = st[idx];
+  if (STASH) {
+    const int nt = min(64, T - w * 64);  // tokens of this workgroup
+    if (do_softmax)
+      for (int idx = threadIdx.x; idx < nt * E; idx += kTopkWaves * 64) {
+        const int i = idx / E, e = idx % E;
+        scores[(size_t)(w * 64 + i) * E + e] = st[e * kStashPitch + i];
+      }
+    if (scores_t)
+      for (int idx = threadIdx.x; idx < E * 64; idx += kTopkWaves * 64) {
+        const int e = idx >> 6, i = idx & 63;
+        if (i < nt) scores_t[(size_t)e * T + w * 64 + i] = st[e * kStashPitch + i];
+      }
+    for (int idx = threadIdx.x; idx < nt * K; idx += kTopkWaves * 64) {
+      topk_idx[(size_t)w * 64 * K + idx] = sidx[idx];
+      topk_w[(size_t)w * 64 * K + idx] = sw[idx];
     }
   }
 }
@@ -366,21 +402,23 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
 
 // ---------------------------------------------------------------- launchers
 
-static size_t topk_lds_bytes(int E, bool stash) { return ((E * 8 + 15) & ~15) + (stash ? (size_t)E * 64 * 4 : 0); }
+static size_t topk_lds_bytes(int E, int K, bool stash) {
+  return ((E * 8 + 15) & ~15) + (stash ? (size_t)E * kStashPitch * 4 + 64 * (size_t)K * 8 : 0);
+}
 
 hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
                              uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s) {
   const dim3 grid(W), block(kTopkWaves * 64);
   const int epl = (E + 63) / 64;
-  // the transposed-score stash must fit the default 64 KB of dynamic LDS
-  const bool stash = scores_t && topk_lds_bytes(E, true) <= 65536;
+  // the stash must fit the default 64 KB of dynamic LDS
+  const bool stash = topk_lds_bytes(E, K, true) <= 65536;
 #define SMOE_TOPK(N)                                                                                               \
   if (epl <= N) {                                                                                                  \
     if (stash)                                                                                                     \
-      topk_route_kernel<N, true><<<grid, block, topk_lds_bytes(E, true), s>>>(in, scores, scores_t, topk_idx,      \
+      topk_route_kernel<N, true><<<grid, block, topk_lds_bytes(E, K, true), s>>>(in, scores, scores_t, topk_idx,      \
                                                                                topk_w, mask, T, E, K, W, do_softmax); \
     else                                                                                                           \
-      topk_route_kernel<N, false><<<grid, block, topk_lds_bytes(E, false), s>>>(in, scores, scores_t, topk_idx,    \
+      topk_route_kernel<N, false><<<grid, block, topk_lds_bytes(E, K, false), s>>>(in, scores, scores_t, topk_idx,    \
                                                                                  topk_w, mask, T, E, K, W, do_softmax); \
     return hipGetLastError();                                                                                      \
   }
