@@ -66,6 +66,21 @@ __device__ __forceinline__ uint32_t score_key(float x) {
 
 constexpr int kSelThreads = 1024;
 
+// 32 x 32 bit transpose in registers (recursive block swaps): afterwards
+// A[b] bit i = bit b of the original A[i].
+__device__ __forceinline__ void transpose32(uint32_t (&A)[32]) {
+  uint32_t m = 0x0000FFFFu;
+#pragma unroll
+  for (int j = 16; j != 0; j >>= 1, m ^= m << j) {
+#pragma unroll
+    for (int k = 0; k < 32; k = (k + j + 1) & ~j) {
+      const uint32_t t = ((A[k] >> j) ^ A[k + j]) & m;
+      A[k + j] ^= t;
+      A[k] ^= t << j;
+    }
+  }
+}
+
 // One block per expert.  Copies the TC mask row of expert e into the rounded
 // mask and flips the `need` selected bits:
 //   pad  (dir > 0): the need best non-TC tokens by (score desc, token asc);
@@ -170,11 +185,17 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
   uint32_t prefix = 0;
   int remaining = need;
   int nties;
+  uint32_t gt_mask = 0, tie_mask = 0;  // register form: candidates with key > tau / == tau
   if constexpr (KPT > 0) {
     // Register form: bit i of `alive` marks key i as a candidate that still
-    // matches the prefix.  After the first few bits (sign, exponent) only a
-    // few keys survive, and slots dead in the whole wave are skipped.
+    // matches the prefix.  The keys are first transposed into bit planes
+    // (plane[b] bit i = bit b of key i), so a pass costs a few mask
+    // operations and popcounts per lane instead of a ballot per key.
     uint32_t alive = (uint32_t)cmask;
+    uint32_t plane[32];
+#pragma unroll
+    for (int i = 0; i < 32; ++i) plane[i] = i < KPT ? keys[i] : 0u;
+    transpose32(plane);
     auto block_total = [&](int cnt) {
       if (lane == 0) cnt_lds[parity][wave] = cnt;
       __syncthreads();
@@ -184,37 +205,59 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
       parity ^= 1;
       return total;
     };
-    auto wave_alive = [&]() {
-      uint32_t x = alive;
+    auto wave_sum_u = [&](uint32_t x) { return dpp_reduce(x, [](uint32_t a, uint32_t b) { return a + b; }); };
+    // two bits per pass: block counts of the alive keys whose next digit is
+    // 3, 2 and 1 decide the digit of tau (16 passes, one barrier each)
+    __shared__ int cnt3_lds[2][3][kWaves];
 #pragma unroll
-      for (int o = 32; o > 0; o >>= 1) x |= (uint32_t)__shfl_xor((int)x, o, kWave);
-      return (uint32_t)__builtin_amdgcn_readfirstlane((int)x);
-    };
-    for (int bit = 31; bit >= 0; --bit) {
-      const uint32_t any = wave_alive();
-      int cnt = 0;
-      uint32_t hit = 0;
-#pragma unroll
-      for (int i = 0; i < KPT; ++i) {
-        if ((any >> i) & 1u) {
-          const bool h = ((alive >> i) & 1u) && ((keys[i] >> bit) & 1u);
-          cnt += __popcll(__ballot(h));
-          hit |= (uint32_t)h << i;
-        }
+    for (int sh = 30; sh >= 0; sh -= 2) {
+      const uint32_t hi = plane[sh + 1], lo = plane[sh];
+      const uint32_t a3 = alive & hi & lo, a2 = alive & hi & ~lo, a1 = alive & ~hi & lo;
+      // per-wave counts (each <= 64 * 32): digits 3 and 2 share one word
+      const uint32_t c32 = wave_sum_u((uint32_t)__popc(a3) | ((uint32_t)__popc(a2) << 16));
+      const uint32_t c1 = wave_sum_u((uint32_t)__popc(a1));
+      if (lane == 0) {
+        cnt3_lds[parity][0][wave] = (int)c1;
+        cnt3_lds[parity][1][wave] = (int)(c32 >> 16);
+        cnt3_lds[parity][2][wave] = (int)(c32 & 0xffffu);
       }
-      const int total = block_total(cnt);
-      if (total >= remaining) {
-        prefix |= 1u << bit;
-        alive &= hit;
+      __syncthreads();
+      int t1 = 0, t2 = 0, t3 = 0;
+#pragma unroll
+      for (int q = 0; q < kWaves; ++q) {
+        t1 += cnt3_lds[parity][0][q];
+        t2 += cnt3_lds[parity][1][q];
+        t3 += cnt3_lds[parity][2][q];
+      }
+      parity ^= 1;
+      if (t3 >= remaining) {
+        prefix |= 3u << sh;
+        alive = a3;
+      } else if (t3 + t2 >= remaining) {
+        prefix |= 2u << sh;
+        remaining -= t3;
+        alive = a2;
+      } else if (t3 + t2 + t1 >= remaining) {
+        prefix |= 1u << sh;
+        remaining -= t3 + t2;
+        alive = a1;
       } else {
-        remaining -= total;
-        alive &= ~hit;
+        remaining -= t3 + t2 + t1;
+        alive &= ~(hi | lo);
       }
     }
-    int cnt = 0;
+    // the survivors are exactly the candidate keys equal to tau
+    nties = block_total((int)wave_sum_u((uint32_t)__popc(alive)));
+    tie_mask = alive;
+    // key > tau from the planes (most significant bit first, tau uniform)
+    uint32_t eq = 0xffffffffu;
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) cnt += __popcll(__ballot((alive >> i) & 1u));
-    nties = block_total(cnt);  // the survivors are exactly the keys equal to tau
+    for (int b = 31; b >= 0; --b) {
+      const uint32_t tb = ((prefix >> b) & 1u) ? 0xffffffffu : 0u;
+      gt_mask |= eq & plane[b] & ~tb;
+      eq &= ~(plane[b] ^ tb);
+    }
+    gt_mask &= (uint32_t)cmask;
   } else {
     for (int bit = 31; bit >= 0; --bit) {
       const int total = count_eq((prefix >> bit) | 1u, bit);
@@ -262,8 +305,7 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     __shared__ int tie_base[KPT * kWaves];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
-      const bool tie = ((cmask >> i) & 1ull) && keys[i] == tau;
-      const uint64_t ties = __ballot(tie);
+      const uint64_t ties = __ballot((tie_mask >> i) & 1u);
       if (lane == 0) tie_base[i * kWaves + wave] = __popcll(ties);
     }
     __syncthreads();
@@ -276,9 +318,8 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     for (int i = 0; i < KPT; ++i) {
       if (i >= slots) break;
       const int w = i * kWaves + wave;
-      const bool cand = (cmask >> i) & 1ull;
-      const bool gt = cand && keys[i] > tau;
-      const bool tie = cand && keys[i] == tau;
+      const bool gt = (gt_mask >> i) & 1u;
+      const bool tie = (tie_mask >> i) & 1u;
       const uint64_t ties = __ballot(tie);
       const int rank = tie_base[w] + __popcll(ties & lanemask_lt());
       const bool flip = gt || (tie && rank >= first_tie && rank < last_tie);
