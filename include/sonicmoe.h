@@ -111,7 +111,11 @@ enum {
   MOE_ROUTE_SCORES_IN = 1,     /* skip the router GEMM and softmax; r->scores is
                                   an input holding S_full                      */
   MOE_ROUTE_WRITE_LOGITS = 2,  /* keep the logits in r->logits                 */
-  MOE_ROUTE_WRITE_SCORES_T = 4 /* also write r->scores_t                       */
+  MOE_ROUTE_WRITE_SCORES_T = 4, /* also write r->scores_t                      */
+  MOE_ROUTE_COUNTS_ONLY = 8     /* metadata stops at mask, mask_prefix and
+                                   counts: enough for moe_round_tokens, which
+                                   builds the rounded routing's own metadata;
+                                   offsets and the row lists are not written */
 };
 
 /*

@@ -25,6 +25,7 @@ MOE_ROUTING_SCORES_T = 2
 MOE_ROUTE_SCORES_IN = 1
 MOE_ROUTE_WRITE_LOGITS = 2
 MOE_ROUTE_WRITE_SCORES_T = 4
+MOE_ROUTE_COUNTS_ONLY = 8
 
 ROUND_MODES = {"nearest": 0, "up": 1, "down": 2, "balance": 3, "stochastic": 4}
 

@@ -11,7 +11,7 @@ namespace smoe {
 // routing
 hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
                              uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s);
-hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, hipStream_t s);
+hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, bool counts_only, hipStream_t s);
 hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, hipStream_t s);
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
                         hipStream_t s);

@@ -276,7 +276,7 @@ int moe_route(moe_dims m, const moe_bf16* X, const moe_bf16* Wr, const float* bi
     return fail(MOE_ERR_INVALID_ARG, "MOE_ROUTE_WRITE_LOGITS needs r->logits");
   if ((flags & MOE_ROUTE_WRITE_SCORES_T) && !r->scores_t)
     return fail(MOE_ERR_INVALID_ARG, "MOE_ROUTE_WRITE_SCORES_T needs r->scores_t");
-  if (flags & ~(MOE_ROUTE_SCORES_IN | MOE_ROUTE_WRITE_LOGITS | MOE_ROUTE_WRITE_SCORES_T))
+  if (flags & ~(MOE_ROUTE_SCORES_IN | MOE_ROUTE_WRITE_LOGITS | MOE_ROUTE_WRITE_SCORES_T | MOE_ROUTE_COUNTS_ONLY))
     return fail(MOE_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
   hipStream_t stream = (hipStream_t)stream_;
   float* scores_t = (flags & MOE_ROUTE_WRITE_SCORES_T) ? r->scores_t : nullptr;
@@ -291,7 +291,8 @@ int moe_route(moe_dims m, const moe_bf16* X, const moe_bf16* Wr, const float* bi
          smoe::launch_topk_route(in, r->scores, scores_t, r->topk_idx, r->topk_w, r->mask, m.T, m.E, m.K, r->words,
                                  scores_in ? 0 : 1, stream),
          "softmax/top-K");
-  LAUNCH(MOE_KC_META, smoe::launch_tc_metadata(*r, m.T, m.E, m.K, stream), "routing metadata");
+  LAUNCH(MOE_KC_META, smoe::launch_tc_metadata(*r, m.T, m.E, m.K, (flags & MOE_ROUTE_COUNTS_ONLY) != 0, stream),
+         "routing metadata");
   return MOE_OK;
 }
 

@@ -433,9 +433,10 @@ hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, in
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, hipStream_t s) {
+hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, bool counts_only, hipStream_t s) {
   const int W = r.words;
   expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
+  if (counts_only) return hipGetLastError();
   scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.counts, r.offsets, E);
   tc_place_kernel<<<dim3((T + 255) / 256), dim3(256), 0, s>>>(r.topk_idx, r.topk_w, r.mask, r.mask_prefix, r.offsets,
                                                               r.tok_offsets, r.tok_count, r.tok_rows, r.row_token,

@@ -61,10 +61,13 @@ class DeviceLayer:
         self.tr = None
         if round_mode:
             self.tr = B.Routing(self.D, B.moe_round_capacity(self.D, self.m_tile), 0, device)
-        self.route_flags = B.MOE_ROUTE_WRITE_LOGITS | (B.MOE_ROUTE_WRITE_SCORES_T if round_mode else 0)
+        # token rounding builds its own metadata: the token-choice routing
+        # only needs its mask, counts and transposed scores
+        for_round = (B.MOE_ROUTE_WRITE_SCORES_T | B.MOE_ROUTE_COUNTS_ONLY) if round_mode else 0
+        self.route_flags = B.MOE_ROUTE_WRITE_LOGITS | for_round
         if scores_in is not None:
             self.tc.arrays()["scores"].copy_(torch.from_numpy(np.ascontiguousarray(scores_in, np.float32)))
-            self.route_flags = B.MOE_ROUTE_SCORES_IN | (B.MOE_ROUTE_WRITE_SCORES_T if round_mode else 0)
+            self.route_flags = B.MOE_ROUTE_SCORES_IN | for_round
         self.u = None if u is None else torch.from_numpy(np.asarray(u, np.float32)).to(device)
         cap = self.routing.capacity
         self.H = torch.empty((cap, 2 * n), dtype=torch.bfloat16, device=device)
