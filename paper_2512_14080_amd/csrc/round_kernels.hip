@@ -13,6 +13,26 @@
 
 namespace smoe {
 
+// The per-expert rounding decision of the independent subroutines (all but
+// Balance-f): direction of f^TR_e - f_e and its size.
+__device__ __forceinline__ void tr_decide_one(int f, float u_e, int T, int M, int mode, int* dir, int* need) {
+  const int lo = (f / M) * M;
+  const int hi = lo + ((f % M) ? M : 0);
+  bool pad;
+  if (mode == MOE_ROUND_NEAREST)
+    pad = (hi - f) < (f - lo);
+  else if (mode == MOE_ROUND_UP)
+    pad = hi > f;
+  else if (mode == MOE_ROUND_DOWN)
+    pad = false;
+  else  // stochastic: Bernoulli((f - lo)/M) from the supplied uniform
+    pad = (u_e * (float)M) < (float)(f - lo);
+  pad = pad && (hi <= T);
+  const int ftr = pad ? hi : lo;
+  *dir = ftr > f ? 1 : (ftr < f ? -1 : 0);
+  *need = ftr > f ? ftr - f : f - ftr;
+}
+
 // Decide f^TR_e for every expert; writes round_dir[e] and the number of
 // tokens to change, need[e] = |f^TR_e - f_e|.
 __global__ __launch_bounds__(256) void tr_decide_kernel(const int32_t* __restrict__ counts, const float* __restrict__ u,
@@ -38,22 +58,10 @@ __global__ __launch_bounds__(256) void tr_decide_kernel(const int32_t* __restric
     return;
   }
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
-    const int f = counts[e];
-    const int lo = (f / M) * M;
-    const int hi = lo + ((f % M) ? M : 0);
-    bool pad;
-    if (mode == MOE_ROUND_NEAREST)
-      pad = (hi - f) < (f - lo);
-    else if (mode == MOE_ROUND_UP)
-      pad = hi > f;
-    else if (mode == MOE_ROUND_DOWN)
-      pad = false;
-    else  // stochastic: Bernoulli((f - lo)/M) from the supplied uniform
-      pad = (u[e] * (float)M) < (float)(f - lo);
-    pad = pad && (hi <= T);
-    const int ftr = pad ? hi : lo;
-    round_dir[e] = ftr > f ? 1 : (ftr < f ? -1 : 0);
-    need[e] = ftr > f ? ftr - f : f - ftr;
+    int dir, nd;
+    tr_decide_one(counts[e], mode == MOE_ROUND_STOCHASTIC ? u[e] : 0.f, T, M, mode, &dir, &nd);
+    round_dir[e] = dir;
+    need[e] = nd;
   }
 }
 
@@ -96,16 +104,27 @@ template <int KPT>
 __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* __restrict__ tc_mask,
                                                                 uint64_t* __restrict__ tr_mask,
                                                                 const float* __restrict__ scores_t,
-                                                                const int32_t* __restrict__ round_dir,
-                                                                const int32_t* __restrict__ need_arr, int T, int W) {
+                                                                int32_t* __restrict__ round_dir,
+                                                                const int32_t* __restrict__ need_arr,
+                                                                const int32_t* __restrict__ counts,
+                                                                const float* __restrict__ u, int M, int mode, int T,
+                                                                int W) {
   constexpr int kWaves = kSelThreads / 64;
   __shared__ int lds[kWaves];
   __shared__ int cnt_lds[2][kWaves];  // per-wave counts of a pass, double-buffered by pass parity
   const int e = blockIdx.x;
   const uint64_t* src = tc_mask + (size_t)e * W;
   uint64_t* dst = tr_mask + (size_t)e * W;
-  const int dir = round_dir[e];
-  const int need = need_arr[e];
+  // the decision: taken here unless a Balance-f pass (sequential over
+  // experts) made it already (need_arr non-null)
+  int dir, need;
+  if (need_arr) {
+    dir = round_dir[e];
+    need = need_arr[e];
+  } else {
+    tr_decide_one(counts[e], mode == MOE_ROUND_STOCHASTIC ? u[e] : 0.f, T, M, mode, &dir, &need);
+    if (threadIdx.x == 0) round_dir[e] = dir;
+  }
   if (dir == 0 || need == 0) {
     for (int w = threadIdx.x; w < W; w += kSelThreads) dst[w] = src[w];
     return;
@@ -337,11 +356,17 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
 
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
                         hipStream_t s) {
-  int32_t* need = tr.scratch;
-  tr_decide_kernel<<<dim3(1), dim3(256), 0, s>>>(tc.counts, u, tr.round_dir, need, T, E, M, mode);
+  // Balance-f is sequential over experts: its own pass decides; the other
+  // subroutines are decided inside the selection workgroups
+  int32_t* need = nullptr;
+  if (mode == MOE_ROUND_BALANCE) {
+    need = tr.scratch;
+    tr_decide_kernel<<<dim3(1), dim3(256), 0, s>>>(tc.counts, u, tr.round_dir, need, T, E, M, mode);
+  }
   const int slots = (T + kSelThreads - 1) / kSelThreads;
   auto select = [&](auto kernel) {
-    kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, T, tr.words);
+    kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, tc.counts, u, M,
+                                                 mode, T, tr.words);
   };
   if (slots <= 4)
     select(tr_select_kernel<4>);

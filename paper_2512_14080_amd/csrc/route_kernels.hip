@@ -297,9 +297,22 @@ constexpr int kMetaBatch = 8;
 __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restrict__ mask,
                                                          const float* __restrict__ scores_t, int32_t* __restrict__ cnt,
                                                          float* __restrict__ denom, int32_t* __restrict__ word_sum,
-                                                         int T, int E, int W) {
+                                                         const int32_t* __restrict__ counts,
+                                                         int32_t* __restrict__ offsets, int T, int E, int W) {
   const int w = blockIdx.x;
   const int lane = lane_id();
+  if (w == W) {
+    // the extra workgroup: offsets = exclusive scan of the expert counts
+    int running = 0;
+    for (int e0 = 0; e0 < E; e0 += 64) {
+      const int v = e0 + lane < E ? counts[e0 + lane] : 0;
+      const int inc = wave_incl_scan(v);
+      if (e0 + lane < E) offsets[e0 + lane] = running + inc - v;
+      running += __shfl(inc, 63, kWave);
+    }
+    if (lane == 0) offsets[E] = running;
+    return;
+  }
   const int t = w * 64 + lane;
   const bool live = t < T;
   int c = 0;
@@ -334,10 +347,12 @@ __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restr
 // [q*Ew, (q+1)*Ew); it first counts its experts per token, and the counts of
 // the lower ranges (exchanged through LDS) give each token's first slot.
 constexpr int kPlaceWaves = 4;
+constexpr int kPlaceSumWords = 4096;  // T <= 262144
 
 __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
     const uint64_t* __restrict__ mask, const int32_t* __restrict__ prefix, const int32_t* __restrict__ offsets,
-    const int32_t* __restrict__ tok_count, const int32_t* __restrict__ word_base, int32_t* __restrict__ tok_offsets,
+    const int32_t* __restrict__ tok_count, const int32_t* __restrict__ word_base,
+    const int32_t* __restrict__ word_sum, int32_t* __restrict__ tok_offsets,
     const float* __restrict__ scores_t, const float* __restrict__ denom, int32_t* __restrict__ tok_rows,
     int32_t* __restrict__ row_token, int32_t* __restrict__ row_expert, float* __restrict__ row_w, int T, int E,
     int W) {
@@ -358,14 +373,30 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
     for (int u = 0; u < n; ++u) c += (int)((readlane_u64(words, u) >> lane) & 1ull);
   }
   cnt[q][lane] = c;
+  // the word's base: given (word_base), or summed here from the word sums
+  __shared__ int wsum[kPlaceWaves];
+  int base;
+  if (word_base) {
+    base = word_base[w];
+  } else {
+    int part = 0;
+    for (int i = threadIdx.x; i < w; i += 64 * kPlaceWaves) part += word_sum[i];
+    part = wave_sum(part);
+    if (lane == 0) wsum[q] = part;
+  }
   __syncthreads();
-  // token t's first row: the word's base (scan of the word sums) plus the
-  // rows of the word's earlier tokens; wave 0 also writes tok_offsets
+  if (!word_base) {
+    base = 0;
+#pragma unroll
+    for (int p = 0; p < kPlaceWaves; ++p) base += wsum[p];
+  }
+  // token t's first row: the word's base plus the rows of the word's earlier
+  // tokens; wave 0 also writes tok_offsets
   const int ct = live ? tok_count[t] : 0;
-  const int tok_first = word_base[w] + wave_incl_scan(ct) - ct;
+  const int tok_first = base + wave_incl_scan(ct) - ct;
   if (q == 0) {
     if (live) tok_offsets[t] = tok_first;
-    if (w == W - 1 && lane == 0) tok_offsets[T] = word_base[W];
+    if (w == W - 1 && lane == 63) tok_offsets[T] = tok_first + ct;
   }
   int j = tok_first;
   for (int p = 0; p < q; ++p) j += cnt[p][lane];
@@ -449,10 +480,15 @@ hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, i
   int32_t* word_sum = r.scratch + E + 64;  // [W]
   int32_t* word_base = word_sum + W + 1;   // [W + 1]
   expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
-  scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.counts, r.offsets, E);
-  token_count_kernel<<<dim3(W), dim3(64), 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, word_sum, T, E, W);
-  scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(word_sum, word_base, W);
-  token_place_kernel<<<dim3(W), dim3(64 * kPlaceWaves), 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_count, word_base,
+  // one extra workgroup turns the expert counts into offsets
+  token_count_kernel<<<dim3(W + 1), dim3(64), 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, word_sum, r.counts,
+                                                      r.offsets, T, E, W);
+  // up to kPlaceSumWords words every placement workgroup sums the word sums
+  // before it itself; beyond that a scan kernel provides the bases
+  const bool scan_words = W > kPlaceSumWords;
+  if (scan_words) scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(word_sum, word_base, W);
+  token_place_kernel<<<dim3(W), dim3(64 * kPlaceWaves), 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_count,
+                                                                scan_words ? word_base : nullptr, word_sum,
                                                                 r.tok_offsets, scores_t, r.tok_denom, r.tok_rows,
                                                                 r.row_token, r.row_expert, r.row_w, T, E, W);
   return hipGetLastError();
