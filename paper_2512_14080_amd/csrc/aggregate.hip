@@ -25,7 +25,9 @@ __device__ __forceinline__ float bcast_f(float v, int l) {
 // without branches: lanes 0..7 fetch the batch's row indices and weights
 // (padding slots clamped to the token's last row, weight 0) and broadcast
 // them, then the row loads of every chunk are issued before any is
-// accumulated, so a lane keeps NC * kAggBatch HBM reads in flight.
+// accumulated, so a lane keeps NC * kAggBatch HBM reads in flight.  Every Y
+// row is read exactly once and O is not read again here: both go through the
+// caches as nontemporal accesses.
 template <int NC>
 __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__ Y, const int32_t* __restrict__ tok_offsets,
                                                     const int32_t* __restrict__ tok_rows, const float* __restrict__ row_w,
@@ -56,7 +58,7 @@ __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__
     for (int ci = 0; ci < NC; ++ci) {
       const int c = min(c0 + lane * 8 + 512 * ci, d - 8);  // lanes past the row end re-read its last chunk
 #pragma unroll
-      for (int u = 0; u < kAggBatch; ++u) v[ci][u] = *(const u32x4*)(Y + (size_t)r[u] * d + c);
+      for (int u = 0; u < kAggBatch; ++u) v[ci][u] = __builtin_nontemporal_load((const u32x4*)(Y + (size_t)r[u] * d + c));
     }
 #pragma unroll
     for (int ci = 0; ci < NC; ++ci)
@@ -75,7 +77,7 @@ __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__
       u32x4 o;
 #pragma unroll
       for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[ci][2 * q], acc[ci][2 * q + 1]);
-      *(u32x4*)(O + (size_t)t * d + c) = o;
+      __builtin_nontemporal_store(o, (u32x4*)(O + (size_t)t * d + c));
     }
   }
 }
@@ -117,7 +119,7 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
       for (int u = 0; u < kAggBatch; ++u) r[u] = bcast_i(rl, u);
       u32x4 v[kAggBatch];
 #pragma unroll
-      for (int u = 0; u < kAggBatch; ++u) v[u] = *(const u32x4*)(dXt + (size_t)r[u] * d + c);
+      for (int u = 0; u < kAggBatch; ++u) v[u] = __builtin_nontemporal_load((const u32x4*)(dXt + (size_t)r[u] * d + c));
       float keep[kAggBatch];
 #pragma unroll
       for (int u = 0; u < kAggBatch; ++u) keep[u] = jb + u < j1 ? 1.f : 0.f;  // padding slots re-read the last row
@@ -146,7 +148,7 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
     u32x4 o;
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[2 * q], acc[2 * q + 1]);
-    *(u32x4*)(dX + (size_t)t * d + c) = o;
+    __builtin_nontemporal_store(o, (u32x4*)(dX + (size_t)t * d + c));
   }
   if (dL) {
     for (int e = lane; e < E; e += 64) {

@@ -322,7 +322,10 @@ struct OpUp {
 // operations of one wave complete in order, so no barrier is needed; the
 // 16-byte chunk c of staged row r sits at chunk c ^ ((r >> 1) & 7), which
 // keeps both the writes (one chunk of 16 rows) and the reads (two whole
-// rows per 16 lanes) free of bank conflicts.
+// rows per 16 lanes) free of bank conflicts.  The stores are nontemporal:
+// these outputs (Y, dX~, the weight gradients) are consumed by a later
+// kernel that streams them once, and left in the cache as dirty lines they
+// only add write-back traffic at the end of the producing kernel.
 constexpr int kStageBytesPerWave = 16 * 128;
 template <class Cfg>
 constexpr bool kStagedStores = Cfg::RN % 2 == 0 && Cfg::LDS_BYTES + Cfg::NW * kStageBytesPerWave + 256 <= 160 * 1024;
@@ -374,7 +377,7 @@ __device__ __forceinline__ void store_rows64_staged(char* wl, uint16_t* blk, int
       const int R = 8 * t + (lane >> 3), C = lane & 7;
       const u32x4 x = *(const u32x4*)(wl + R * 128 + ((C ^ ((R >> 1) & 7)) << 4));
       const int row = 16 * q + R;
-      if (row < rows_valid) *(u32x4*)(blk + (row * (int)ld + 8 * C)) = x;
+      if (row < rows_valid) __builtin_nontemporal_store(x, (u32x4*)(blk + (row * (int)ld + 8 * C)));
     }
     asm volatile("" ::: "memory");  // reads of this round before the next round's writes
   }
