@@ -13,6 +13,7 @@ namespace smoe {
 
 constexpr int kAggBatch = 8;  // rows whose loads are in flight together
 constexpr int kColRows = 128;  // tokens per chunk of the dbias column sum
+constexpr int kDLPerLane = 4;  // router-gradient row entries per lane collected in registers (E <= 256)
 static_assert(kAggBatch == 8, "lane & 7 picks a batch slot");
 
 __device__ __forceinline__ int bcast_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
@@ -84,53 +85,75 @@ __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__
 
 // dX_t = sum over the token's rows of dX~ + sum_j dl_j W_r[:, e_j], with the
 // router gradient on the token's selected set dl_j = s_j (dS_j - sum_k s_k dS_k).
-// Also writes the dense router-logit gradient row dL[t, :] (bf16) for dW_r.
+// Also writes the dense router-logit gradient row dL[t, :] (bf16) for dW_r
+// (when dL is given; the launch for column slice 0 does it).
 // W_r^T [E][d] is a bf16 copy (exact: W_r is bf16), so each row term is one
-// 16-byte load per lane; a batch's dX~ rows and W_r^T rows are all requested
-// before any is accumulated.
+// 16-byte load per lane.  As in the forward kernel, a batch's dX~ rows are
+// requested for every column chunk before any is accumulated; the W_r^T rows
+// (a few hundred KB, cache resident) follow chunk by chunk.
+template <int NC>
 __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict__ dXt, const float* __restrict__ dS,
                                                      const uint16_t* __restrict__ WrT,
                                                      const int32_t* __restrict__ tok_offsets,
                                                      const int32_t* __restrict__ tok_rows,
                                                      const int32_t* __restrict__ row_expert,
                                                      const float* __restrict__ row_w, uint16_t* __restrict__ dX,
-                                                     uint16_t* __restrict__ dL, int T, int d, int E) {
+                                                     uint16_t* __restrict__ dL, int T, int d, int E, int c0) {
   // wave-uniform token: row indices and weights become scalar loads
   const int t = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (t >= T) return;
   const int lane = lane_id();
   const int j0 = tok_offsets[t], j1 = tok_offsets[t + 1];
+  // g = sum_k s_k dS_k in row order; lanes 0..7 fetch a batch's terms
   float g = 0.f;
   if (WrT)
-    for (int j = j0; j < j1; ++j) {
-      const int r = tok_rows[j];
-      g += row_w[r] * dS[r];
-    }
-  for (int c = lane * 8; c < d; c += 512) {
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int jb = j0; jb < j1; jb += kAggBatch) {
-      // slot lane&7 of the batch: one vector load per level, then broadcast
       const int slot = jb + (lane & 7);
       const int rl = tok_rows[min(slot, j1 - 1)];
-      const int el = WrT ? row_expert[rl] : 0;
-      const float dll = (WrT && slot < j1) ? row_w[rl] * (dS[rl] - g) : 0.f;
-      int r[kAggBatch];
+      const float pl = slot < j1 ? row_w[rl] * dS[rl] : 0.f;
 #pragma unroll
-      for (int u = 0; u < kAggBatch; ++u) r[u] = bcast_i(rl, u);
-      u32x4 v[kAggBatch];
+      for (int u = 0; u < kAggBatch; ++u) g += bcast_f(pl, u);
+    }
+  // dL[t, e] for e = lane + 64 q (q < kDLPerLane), collected from the batches
+  const bool dl_fast = dL != nullptr && E <= 64 * kDLPerLane;
+  float dlv[kDLPerLane] = {0.f, 0.f, 0.f, 0.f};
+  float acc[NC][8];
 #pragma unroll
-      for (int u = 0; u < kAggBatch; ++u) v[u] = __builtin_nontemporal_load((const u32x4*)(dXt + (size_t)r[u] * d + c));
-      float keep[kAggBatch];
+  for (int ci = 0; ci < NC; ++ci)
 #pragma unroll
-      for (int u = 0; u < kAggBatch; ++u) keep[u] = jb + u < j1 ? 1.f : 0.f;  // padding slots re-read the last row
+    for (int q = 0; q < 8; ++q) acc[ci][q] = 0.f;
+  for (int jb = j0; jb < j1; jb += kAggBatch) {
+    // slot lane&7 of the batch: one vector load per level, then broadcast
+    const int slot = jb + (lane & 7);
+    const int rl = tok_rows[min(slot, j1 - 1)];
+    const int el = WrT ? row_expert[rl] : 0;
+    const float dll = (WrT && slot < j1) ? row_w[rl] * (dS[rl] - g) : 0.f;
+    int r[kAggBatch];
+#pragma unroll
+    for (int u = 0; u < kAggBatch; ++u) r[u] = bcast_i(rl, u);
+    u32x4 v[NC][kAggBatch];
+#pragma unroll
+    for (int ci = 0; ci < NC; ++ci) {
+      const int c = min(c0 + lane * 8 + 512 * ci, d - 8);  // lanes past the row end re-read its last chunk
+#pragma unroll
+      for (int u = 0; u < kAggBatch; ++u) v[ci][u] = __builtin_nontemporal_load((const u32x4*)(dXt + (size_t)r[u] * d + c));
+    }
+    float keep[kAggBatch];
+#pragma unroll
+    for (int u = 0; u < kAggBatch; ++u) keep[u] = jb + u < j1 ? 1.f : 0.f;  // padding slots re-read the last row
+#pragma unroll
+    for (int ci = 0; ci < NC; ++ci)
 #pragma unroll
       for (int u = 0; u < kAggBatch; ++u)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          acc[2 * q] += keep[u] * bf_lo(v[u][q]);
-          acc[2 * q + 1] += keep[u] * bf_hi(v[u][q]);
+          acc[ci][2 * q] += keep[u] * bf_lo(v[ci][u][q]);
+          acc[ci][2 * q + 1] += keep[u] * bf_hi(v[ci][u][q]);
         }
-      if (WrT) {
+    if (WrT) {
+#pragma unroll
+      for (int ci = 0; ci < NC; ++ci) {
+        const int c = min(c0 + lane * 8 + 512 * ci, d - 8);
         u32x4 wv[kAggBatch];
 #pragma unroll
         for (int u = 0; u < kAggBatch; ++u) wv[u] = *(const u32x4*)(WrT + (size_t)bcast_i(el, u) * d + c);
@@ -139,18 +162,37 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
           const float dl = bcast_f(dll, u);  // 0 for padding slots
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            acc[2 * q] += dl * bf_lo(wv[u][q]);
-            acc[2 * q + 1] += dl * bf_hi(wv[u][q]);
+            acc[ci][2 * q] += dl * bf_lo(wv[u][q]);
+            acc[ci][2 * q + 1] += dl * bf_hi(wv[u][q]);
           }
         }
       }
-    }
-    u32x4 o;
+      if (dl_fast)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[2 * q], acc[2 * q + 1]);
-    __builtin_nontemporal_store(o, (u32x4*)(dX + (size_t)t * d + c));
+        for (int u = 0; u < kAggBatch; ++u) {
+          const int e = bcast_i(el, u);
+          const float dl = bcast_f(dll, u);
+#pragma unroll
+          for (int q = 0; q < kDLPerLane; ++q)
+            if (jb + u < j1 && e == lane + 64 * q) dlv[q] = dl;
+        }
+    }
   }
-  if (dL) {
+#pragma unroll
+  for (int ci = 0; ci < NC; ++ci) {
+    const int c = c0 + lane * 8 + 512 * ci;
+    if (c < d) {
+      u32x4 o;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = pack_bf2(acc[ci][2 * q], acc[ci][2 * q + 1]);
+      __builtin_nontemporal_store(o, (u32x4*)(dX + (size_t)t * d + c));
+    }
+  }
+  if (dl_fast) {
+#pragma unroll
+    for (int q = 0; q < kDLPerLane; ++q)
+      if (lane + 64 * q < E) dL[(size_t)t * E + lane + 64 * q] = f2bf(dlv[q]);
+  } else if (dL) {
     for (int e = lane; e < E; e += 64) {
       float v = 0.f;
       for (int j = j0; j < j1; ++j) {
@@ -231,8 +273,21 @@ hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, in
 
 hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const uint16_t* WrT, const moe_routing& r, uint16_t* dX,
                          uint16_t* dL, int T, int d, int E, hipStream_t s) {
-  agg_dx_kernel<<<dim3((T + 3) / 4), dim3(256), 0, s>>>(dXt, dS, WrT, r.tok_offsets, r.tok_rows, r.row_expert, r.row_w,
-                                                        dX, dL, T, d, E);
+  const dim3 grid((T + 3) / 4), block(256);
+  const int nc = (d + 511) / 512;
+  if (nc <= 1)
+    agg_dx_kernel<1><<<grid, block, 0, s>>>(dXt, dS, WrT, r.tok_offsets, r.tok_rows, r.row_expert, r.row_w, dX, dL, T,
+                                            d, E, 0);
+  else if (nc == 2)
+    agg_dx_kernel<2><<<grid, block, 0, s>>>(dXt, dS, WrT, r.tok_offsets, r.tok_rows, r.row_expert, r.row_w, dX, dL, T,
+                                            d, E, 0);
+  else if (nc == 3)
+    agg_dx_kernel<3><<<grid, block, 0, s>>>(dXt, dS, WrT, r.tok_offsets, r.tok_rows, r.row_expert, r.row_w, dX, dL, T,
+                                            d, E, 0);
+  else  // rows wider than 1536: 2048-column slices, one launch each; the first writes dL
+    for (int c0 = 0; c0 < d; c0 += 2048)
+      agg_dx_kernel<4><<<grid, block, 0, s>>>(dXt, dS, WrT, r.tok_offsets, r.tok_rows, r.row_expert, r.row_w, dX,
+                                              c0 == 0 ? dL : nullptr, T, d, E, c0);
   return hipGetLastError();
 }
 

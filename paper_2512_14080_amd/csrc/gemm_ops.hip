@@ -793,7 +793,7 @@ hipError_t launch_dw1(const DW1Args& a, hipStream_t s) {
 
 int dwr_splits(int T, int d, int E) {
   const int tiles = (d / 128) * ((E + 127) / 128);
-  int s = (256 + tiles - 1) / tiles;  // aim for one tile per CU
+  int s = 256 / tiles;  // at most one tile per CU: a second round would double the time
   const int max_s = (T + 255) / 256;  // at least 256 tokens per split
   if (s > max_s) s = max_s;
   return s < 1 ? 1 : s;
