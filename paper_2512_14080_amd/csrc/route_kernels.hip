@@ -187,6 +187,202 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
   }
 }
 
+// Lane-per-token selection (K <= KM <= 8; E a multiple of 4 * NW, E <= 256).
+// A workgroup owns the 64 tokens of one membership word, lane l token 64w + l,
+// and its NW waves split the experts into NW contiguous slices, so the
+// per-token work is ordinary per-lane arithmetic instead of wave-wide
+// reductions.  Each wave keeps its slice of the token's row in LDS as
+// [slice/4][64] float4 (lane l's column: conflict-free in every pass):
+//   1. row max (the row loads are issued 16 float4 at a time), combined
+//      across the slices;
+//   2. exp(x - max) and the slice sums, combined in slice order;
+//   3. scores = exp / sum (written token-major and, coalesced across lanes,
+//      transposed), and a KM-slot insertion network over the (key, expert)
+//      pairs of the slice: an element moves down past every slot whose pair
+//      it exceeds; the network runs only when some lane's element beats its
+//      last slot.  The slices' lists are then merged (top-KM of two sorted
+//      lists: pairwise maxima of one list against the other reversed, then a
+//      bitonic clean-up), every wave doing the same merge;
+//   4. membership: expert e is selected iff its pair ranks at or above the
+//      K-th slot; a ballot per expert is the membership word.  The selected
+//      scores are summed in ascending expert order for the renormalisation
+//      denominator (each slice lists its selected scores in order in LDS,
+//      the first wave adds the lists slice by slice).
+// The (score, index) pairs are compared exactly, as in the wave-per-token
+// kernel above: equal keys order by the lower expert.
+template <int KM>
+__device__ __forceinline__ void topk_cex(uint64_t& a, uint64_t& b) {  // a >= b afterwards
+  const bool sw = b > a;
+  const uint64_t hi = sw ? b : a;
+  b = sw ? a : b;
+  a = hi;
+}
+template <int KM>
+__device__ __forceinline__ void topk_merge(uint64_t (&a)[KM], const uint64_t (&b)[KM]) {
+#pragma unroll
+  for (int i = 0; i < KM; ++i) a[i] = a[i] > b[KM - 1 - i] ? a[i] : b[KM - 1 - i];
+#pragma unroll
+  for (int h = KM / 2; h >= 1; h >>= 1)
+#pragma unroll
+    for (int i = 0; i < KM; ++i)
+      if ((i & h) == 0) topk_cex<KM>(a[i], a[i + h]);
+}
+
+template <int KM, int NW>
+__global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, float* scores, float* __restrict__ scores_t,
+                                                            int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
+                                                            uint64_t* __restrict__ mask, int T, int E, int K, int W,
+                                                            int do_softmax) {
+  extern __shared__ __attribute__((aligned(16))) char dyn[];
+  const int w = blockIdx.x;
+  const int q = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = lane_id();
+  const int t = w * 64 + lane;
+  const bool live = t < T;
+  const int Eq = E / NW, Gq = Eq >> 2, e0 = q * Eq;
+  f32x4* cols = (f32x4*)dyn + (size_t)q * Gq * 64;      // [Gq][64]
+  float* xmax = (float*)(dyn + (size_t)E * 256);           // [NW][64]
+  float* xsum = xmax + NW * 64;                            // [NW][64]
+  uint64_t* lists = (uint64_t*)(xsum + NW * 64);           // [NW][KM][64]
+  float* sv = (float*)(lists + NW * KM * 64);              // [NW][KM][64] selected scores, expert order
+  int* nsel = (int*)(sv + NW * KM * 64);                   // [NW][64]
+  // a lane past T reads token 0's row and discards it
+  const f32x4* row = (const f32x4*)(in + (size_t)(live ? t : 0) * E + e0);
+  const f32x4 ninf = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  float m = -INFINITY;
+#pragma unroll 16
+  for (int g = 0; g < Gq; ++g) {
+    const f32x4 x0 = row[g];
+    const f32x4 x = live ? x0 : ninf;
+    cols[g * 64 + lane] = x;
+    m = fmaxf(m, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+  }
+  float s = 1.f;
+  if (do_softmax) {
+    if constexpr (NW > 1) {
+      xmax[q * 64 + lane] = m;
+      __syncthreads();
+#pragma unroll
+      for (int p = 0; p < NW; ++p) m = fmaxf(m, xmax[p * 64 + lane]);
+    }
+    s = 0.f;
+#pragma unroll 4
+    for (int g = 0; g < Gq; ++g) {
+      f32x4 x = cols[g * 64 + lane];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        x[c] = expf(x[c] - m);
+        s += x[c];
+      }
+      cols[g * 64 + lane] = x;
+    }
+    if constexpr (NW > 1) {
+      xsum[q * 64 + lane] = s;
+      __syncthreads();
+      s = xsum[lane];
+#pragma unroll
+      for (int p = 1; p < NW; ++p) s += xsum[p * 64 + lane];
+    }
+  }
+  uint64_t top[KM];
+#pragma unroll
+  for (int k = 0; k < KM; ++k) top[k] = 0;  // below every (key, ~expert) pair
+  for (int g = 0; g < Gq; ++g) {
+    f32x4 p = cols[g * 64 + lane];
+    const int eg = e0 + 4 * g;
+    if (do_softmax) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) p[c] = p[c] / s;
+      cols[g * 64 + lane] = p;
+      if (live) *(f32x4*)(scores + (size_t)t * E + eg) = p;
+    }
+    if (scores_t && live) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) scores_t[(size_t)(eg + c) * T + t] = p[c];
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint64_t x0 = ((uint64_t)topk_key(p[c]) << 32) | (uint32_t)~(uint32_t)(eg + c);
+      if (__ballot(live && x0 > top[KM - 1])) {
+        uint64_t x = x0;
+#pragma unroll
+        for (int k = 0; k < KM; ++k) topk_cex<KM>(top[k], x);
+      }
+    }
+  }
+  if constexpr (NW > 1) {
+#pragma unroll
+    for (int k = 0; k < KM; ++k) lists[(q * KM + k) * 64 + lane] = top[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < KM; ++k) top[k] = lists[k * 64 + lane];
+#pragma unroll
+    for (int p = 1; p < NW; ++p) {
+      uint64_t b[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) b[k] = lists[(p * KM + k) * 64 + lane];
+      topk_merge<KM>(top, b);
+    }
+  }
+  uint64_t thr = top[0];
+#pragma unroll
+  for (int k = 1; k < KM; ++k)
+    if (k == K - 1) thr = top[k];
+  // membership words of this wave's experts (expert e0 + 64 r + lane in mw[r])
+  constexpr int kWords = NW > 1 ? 1 : 4;
+  float den = 0.f;
+  int ns = 0;
+  uint64_t mw[kWords];
+#pragma unroll
+  for (int r = 0; r < kWords; ++r) mw[r] = 0ull;
+#pragma unroll
+  for (int r = 0; r < kWords; ++r) {
+    const int g1 = min(Gq, 16 * r + 16);
+    for (int g = 16 * r; g < g1; ++g) {
+      const f32x4 p = cols[g * 64 + lane];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int el = 4 * g + c;  // expert e0 + el
+        const uint64_t x = ((uint64_t)topk_key(p[c]) << 32) | (uint32_t)~(uint32_t)(e0 + el);
+        const bool sel = live && x >= thr;
+        const uint64_t word = __ballot(sel);
+        if (lane == (el & 63)) mw[r] = word;
+        if constexpr (NW > 1) {
+          if (sel) sv[(q * KM + ns) * 64 + lane] = p[c];
+          ns += sel;
+        } else {
+          den += sel ? p[c] : 0.f;  // +0 for the others leaves the sum unchanged
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kWords; ++r)
+    if (64 * r + lane < Eq) mask[(size_t)(e0 + 64 * r + lane) * W + w] = mw[r];
+  if constexpr (NW > 1) {
+    nsel[q * 64 + lane] = ns;
+    __syncthreads();
+    if (q != 0) return;
+    // selected scores in ascending expert order: slice by slice
+    for (int p = 0; p < NW; ++p) {
+      const int np = nsel[p * 64 + lane];
+      for (int j = 0; j < np; ++j) den += sv[(p * KM + j) * 64 + lane];
+    }
+  }
+  if (live) {
+#pragma unroll
+    for (int k = 0; k < KM; ++k)
+      if (k < K) {
+        topk_idx[(size_t)t * K + k] = (int32_t)~(uint32_t)top[k];
+        topk_w[(size_t)t * K + k] = topk_value((uint32_t)(top[k] >> 32)) / den;
+      }
+  }
+}
+
+static size_t topk_lane_lds(int E, int KM, int NW) {
+  return (size_t)E * 256 + (NW > 1 ? (size_t)NW * 64 * (4 + 4 + 8 * KM + 4 * KM + 4) : 0);
+}
+
 // Per expert: popcount prefix over its mask words and its count f_e.
 __global__ __launch_bounds__(256) void expert_scan_kernel(const uint64_t* __restrict__ mask,
                                                           int32_t* __restrict__ prefix, int32_t* __restrict__ counts,
@@ -290,9 +486,9 @@ __global__ __launch_bounds__(256) void tc_place_kernel(const int32_t* __restrict
 // denominator (selected scores summed in ascending expert order, fp32).
 // The wave first loads the mask words of 64 experts at once (lane i holds
 // expert c + i), then walks the experts in ascending order, taking each word
-// from its lane with a readlane; the score loads of 8 experts are issued
-// before any is summed.
-constexpr int kMetaBatch = 8;
+// from its lane with a readlane; the score loads of kMetaBatch experts are
+// issued before any is summed (the passes are load-latency bound).
+constexpr int kMetaBatch = 32;
 
 __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restrict__ mask,
                                                          const float* __restrict__ scores_t, int32_t* __restrict__ cnt,
@@ -365,6 +561,9 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
   const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
   const int ew = (E + kPlaceWaves - 1) / kPlaceWaves;
   const int e_lo = min(E, q * ew), e_hi = min(E, e_lo + ew);
+  // independent loads first: they overlap the count pass and the barrier
+  const int ct = live ? tok_count[t] : 0;
+  const float dn = live ? denom[t] : 1.f;
   int c = 0;
   for (int c0 = e_lo; c0 < e_hi; c0 += 64) {
     const int el = c0 + lane;
@@ -392,7 +591,6 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
   }
   // token t's first row: the word's base plus the rows of the word's earlier
   // tokens; wave 0 also writes tok_offsets
-  const int ct = live ? tok_count[t] : 0;
   const int tok_first = base + wave_incl_scan(ct) - ct;
   if (q == 0) {
     if (live) tok_offsets[t] = tok_first;
@@ -400,7 +598,6 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
   }
   int j = tok_first;
   for (int p = 0; p < q; ++p) j += cnt[p][lane];
-  const float dn = live ? denom[t] : 1.f;
   for (int c0 = e_lo; c0 < e_hi; c0 += 64) {
     const int el = c0 + lane;
     const uint64_t words = el < e_hi ? mask[(size_t)el * W + w] : 0ull;
@@ -439,6 +636,23 @@ static size_t topk_lds_bytes(int E, int K, bool stash) {
 
 hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
                              uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s) {
+  if (E % 4 == 0 && E <= 256 && K <= 8 && K <= E) {
+#define SMOE_TOPK_LANE(KM, NW)                                                                                    \
+  topk_lane_kernel<KM, NW><<<dim3(W), dim3(64 * NW), topk_lane_lds(E, KM, NW), s>>>(                              \
+      in, scores, scores_t, topk_idx, topk_w, mask, T, E, K, W, do_softmax)
+    // four waves per word when the experts split into four slices of whole
+    // float4s and the workgroup's LDS stays within the default 64 KB
+    const bool four = E % 16 == 0 && topk_lane_lds(E, 8, 4) <= 65536;
+    if (K <= 2) {
+      if (four) SMOE_TOPK_LANE(2, 4); else SMOE_TOPK_LANE(2, 1);
+    } else if (K <= 4) {
+      if (four) SMOE_TOPK_LANE(4, 4); else SMOE_TOPK_LANE(4, 1);
+    } else {
+      if (four) SMOE_TOPK_LANE(8, 4); else SMOE_TOPK_LANE(8, 1);
+    }
+#undef SMOE_TOPK_LANE
+    return hipGetLastError();
+  }
   const dim3 grid(W), block(kTopkWaves * 64);
   const int epl = (E + 63) / 64;
   // the stash must fit the default 64 KB of dynamic LDS
