@@ -141,6 +141,13 @@ def test_k_equals_e_and_k_one():
     check_layer(W.MoEConfig("k1", T=300, d=128, n=64, E=8, K=1, m_tile=16), seed=4)
 
 
+def test_wave_per_token_topk_shapes():
+    """Shapes outside the lane-per-token top-K (E > 256, K > 8) take the
+    wave-per-token kernel; the routing and the layer still match."""
+    check_layer(W.MoEConfig("e264", T=300, d=128, n=64, E=264, K=3, m_tile=16), seed=13)
+    check_layer(W.MoEConfig("k10", T=300, d=128, n=64, E=16, K=10, m_tile=16), seed=14, round_mode="nearest")
+
+
 def test_single_token_and_one_hot_expert():
     check_layer(TINY, seed=5, T=1)
     check_layer(TINY, seed=6, T=65, round_mode="nearest")
