@@ -481,14 +481,43 @@ __global__ __launch_bounds__(256) void tc_place_kernel(const int32_t* __restrict
   if (t == T - 1) tok_offsets[T] = T * K;
 }
 
+// 64-bit value of lane (lane ^ s), and of lane src (any per-lane index).
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int s) {
+  const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, s, kWave);
+  const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), s, kWave);
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  const uint32_t lo = (uint32_t)__shfl((int)(uint32_t)v, src, kWave);
+  const uint32_t hi = (uint32_t)__shfl((int)(uint32_t)(v >> 32), src, kWave);
+  return ((uint64_t)hi << 32) | lo;
+}
+// 64 x 64 bit transpose across a wave: lane i holds row i on entry; on exit
+// lane j holds column j (bit i of lane j's result = bit j of lane i's input).
+// Six butterfly stages, each exchanging the off-diagonal s x s blocks of
+// every 2s x 2s block between lanes i and i ^ s.
+__device__ __forceinline__ uint64_t wave_transpose64(uint64_t x, int lane) {
+  constexpr uint64_t kLow[6] = {0x00000000FFFFFFFFull, 0x0000FFFF0000FFFFull, 0x00FF00FF00FF00FFull,
+                                0x0F0F0F0F0F0F0F0Full, 0x3333333333333333ull, 0x5555555555555555ull};
+#pragma unroll
+  for (int k = 0; k < 6; ++k) {
+    const int s = 32 >> k;
+    const uint64_t m = kLow[k];  // bit positions j with (j & s) == 0
+    const uint64_t y = shfl_xor_u64(x, s);
+    x = (lane & s) ? (((y >> s) & m) | (x & ~m)) : ((x & m) | ((y & m) << s));
+  }
+  return x;
+}
+
 // General placement (any membership, e.g. after token rounding), one wave per
 // 64-token word.  Pass 1: per-token expert count and renormalisation
 // denominator (selected scores summed in ascending expert order, fp32).
-// The wave first loads the mask words of 64 experts at once (lane i holds
-// expert c + i), then walks the experts in ascending order, taking each word
-// from its lane with a readlane; the score loads of kMetaBatch experts are
-// issued before any is summed (the passes are load-latency bound).
-constexpr int kMetaBatch = 32;
+// The wave loads the mask words of 64 experts (lane i: expert c0 + i) and
+// transposes them, so that lane l holds token l's membership bits of those
+// experts; it then walks its own set bits, lowest expert first, issuing the
+// score loads of kMetaBatch experts before summing them.
+constexpr int kMetaBatch = 8;
+constexpr int kMetaChunks = 4;  // 64-expert chunks whose mask words are loaded together
 
 __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restrict__ mask,
                                                          const float* __restrict__ scores_t, int32_t* __restrict__ cnt,
@@ -513,21 +542,33 @@ __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restr
   const bool live = t < T;
   int c = 0;
   float s = 0.f;
-  for (int c0 = 0; c0 < E; c0 += 64) {
-    const uint64_t words = c0 + lane < E ? mask[(size_t)(c0 + lane) * W + w] : 0ull;
-    const int n = min(64, E - c0);
-    for (int j0 = 0; j0 < n; j0 += kMetaBatch) {
-      float v[kMetaBatch];
+  for (int cb = 0; cb < E; cb += 64 * kMetaChunks) {
+    uint64_t words[kMetaChunks];
 #pragma unroll
-      for (int u = 0; u < kMetaBatch; ++u) {
-        const uint64_t word = readlane_u64(words, j0 + u);  // 0 past n
-        const bool hit = live && ((word >> lane) & 1ull);
-        v[u] = hit ? scores_t[(size_t)(c0 + j0 + u) * T + t] : 0.f;
-        c += hit;
+    for (int h = 0; h < kMetaChunks; ++h) {
+      const int e = cb + 64 * h + lane;
+      words[h] = e < E ? mask[(size_t)e * W + w] : 0ull;
+    }
+#pragma unroll
+    for (int h = 0; h < kMetaChunks; ++h) {
+      const int c0 = cb + 64 * h;
+      if (c0 >= E) break;
+      uint64_t bits = wave_transpose64(words[h], lane);
+      if (!live) bits = 0;
+      c += __popcll(bits);
+      while (__ballot(bits != 0)) {
+        float v[kMetaBatch];
+#pragma unroll
+        for (int u = 0; u < kMetaBatch; ++u) {
+          const bool has = bits != 0;
+          const int i = has ? __ffsll((unsigned long long)bits) - 1 : 0;
+          v[u] = has ? scores_t[(size_t)(c0 + i) * T + t] : 0.f;
+          bits &= bits - 1;
+        }
+        // adding +0 for a miss leaves the sum unchanged (it is never -0)
+#pragma unroll
+        for (int u = 0; u < kMetaBatch; ++u) s += v[u];
       }
-      // adding +0 for a miss leaves the sum unchanged (it is never -0)
-#pragma unroll
-      for (int u = 0; u < kMetaBatch; ++u) s += v[u];
     }
   }
   if (live) {
@@ -541,7 +582,10 @@ __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restr
 // Pass 2: rows of every token (expert ascending), renormalised weights.  The
 // kPlaceWaves waves of a workgroup share one word: wave q places experts
 // [q*Ew, (q+1)*Ew); it first counts its experts per token, and the counts of
-// the lower ranges (exchanged through LDS) give each token's first slot.
+// the lower ranges (exchanged through LDS) give each token's first slot.  As
+// in pass 1, each lane walks its own token's set bits (from the transposed
+// mask words); the expert's mask word and row base come from the lane that
+// loaded them.
 constexpr int kPlaceWaves = 4;
 constexpr int kPlaceSumWords = 4096;  // T <= 262144
 
@@ -564,12 +608,18 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
   // independent loads first: they overlap the count pass and the barrier
   const int ct = live ? tok_count[t] : 0;
   const float dn = live ? denom[t] : 1.f;
-  int c = 0;
-  for (int c0 = e_lo; c0 < e_hi; c0 += 64) {
+  // the first chunk's words and row bases stay in registers for pass 2
+  const int el0 = e_lo + lane;
+  const uint64_t words0 = el0 < e_hi ? mask[(size_t)el0 * W + w] : 0ull;
+  const int bases0 = el0 < e_hi ? offsets[el0] + prefix[(size_t)el0 * W + w] : 0;
+  uint64_t bits0 = wave_transpose64(words0, lane);
+  if (!live) bits0 = 0;
+  int c = __popcll(bits0);
+  for (int c0 = e_lo + 64; c0 < e_hi; c0 += 64) {
     const int el = c0 + lane;
     const uint64_t words = el < e_hi ? mask[(size_t)el * W + w] : 0ull;
-    const int n = min(64, e_hi - c0);
-    for (int u = 0; u < n; ++u) c += (int)((readlane_u64(words, u) >> lane) & 1ull);
+    const uint64_t bits = wave_transpose64(words, lane);
+    c += live ? __popcll(bits) : 0;
   }
   cnt[q][lane] = c;
   // the word's base: given (word_base), or summed here from the word sums
@@ -599,29 +649,36 @@ __global__ __launch_bounds__(64 * kPlaceWaves) void token_place_kernel(
   int j = tok_first;
   for (int p = 0; p < q; ++p) j += cnt[p][lane];
   for (int c0 = e_lo; c0 < e_hi; c0 += 64) {
-    const int el = c0 + lane;
-    const uint64_t words = el < e_hi ? mask[(size_t)el * W + w] : 0ull;
-    const int bases = el < e_hi ? offsets[el] + prefix[(size_t)el * W + w] : 0;
-    const int n = min(64, e_hi - c0);
-    for (int j0 = 0; j0 < n; j0 += kMetaBatch) {
+    uint64_t words = words0, bits = bits0;
+    int bases = bases0;
+    if (c0 != e_lo) {
+      const int el = c0 + lane;
+      words = el < e_hi ? mask[(size_t)el * W + w] : 0ull;
+      bases = el < e_hi ? offsets[el] + prefix[(size_t)el * W + w] : 0;
+      bits = wave_transpose64(words, lane);
+      if (!live) bits = 0;
+    }
+    while (__ballot(bits != 0)) {
       float v[kMetaBatch];
+      int r[kMetaBatch], ex[kMetaBatch];
       bool hit[kMetaBatch];
 #pragma unroll
       for (int u = 0; u < kMetaBatch; ++u) {
-        const uint64_t word = readlane_u64(words, j0 + u);
-        hit[u] = live && ((word >> lane) & 1ull);
-        v[u] = hit[u] ? scores_t[(size_t)(c0 + j0 + u) * T + t] : 0.f;
+        hit[u] = bits != 0;
+        const int i = hit[u] ? __ffsll((unsigned long long)bits) - 1 : 0;
+        bits &= bits - 1;
+        const uint64_t word = shfl_u64(words, i);  // expert c0 + i's mask word
+        r[u] = __shfl(bases, i, kWave) + __popcll(word & below);
+        ex[u] = c0 + i;
+        v[u] = hit[u] ? scores_t[(size_t)(c0 + i) * T + t] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < kMetaBatch; ++u) {
         if (hit[u]) {
-          const int e = c0 + j0 + u;
-          const uint64_t word = readlane_u64(words, j0 + u);
-          const int r = __builtin_amdgcn_readlane(bases, j0 + u) + __popcll(word & below);
-          tok_rows[j++] = r;
-          row_token[r] = t;
-          row_expert[r] = e;
-          row_w[r] = v[u] / dn;
+          tok_rows[j++] = r[u];
+          row_token[r[u]] = t;
+          row_expert[r[u]] = ex[u];
+          row_w[r[u]] = v[u] / dn;
         }
       }
     }
