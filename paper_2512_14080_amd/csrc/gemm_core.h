@@ -66,6 +66,18 @@ struct TileInfo {
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds_byte) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_byte), "v"(g) : "memory", "m0");
 }
+// The lane index from a volatile asm: per-lane address arithmetic derived
+// from it is recomputed where it is used instead of being hoisted out of the
+// persistent tile loop, where it would hold registers across the k loop.
+__device__ __forceinline__ int volatile_lane() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+// One 4-byte-per-lane LDS DMA (lane l's dword lands at lds_byte + 4 l).
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds_byte) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds_byte), "v"(g) : "memory", "m0");
+}
 // Wait until at most N of this wave's vector-memory ops are outstanding, then
 // workgroup barrier.  LDS reads of the previous step are complete as well.
 template <int N>
@@ -108,7 +120,7 @@ struct GemmCfg {
 // different 16-byte bank groups.
 // DMA instruction q covers rows (64/C)q .. (64/C)q + 64/C - 1; lane l -> row
 // (64/C)q + l/C, physical chunk l%C, logical chunk (l%C) ^ swz(row).
-template <int R, int BK, int NW>
+template <int R, int BK, int NW, bool AI = false>
 struct RowsSide {
   static constexpr int C = BK / 8;              // chunks per row
   static constexpr int RPI = 64 / C;            // rows per DMA instruction
@@ -119,26 +131,41 @@ struct RowsSide {
   const uint16_t* base_;
   int64_t ld_;
   int32_t row_[Q];     // the row this lane loads, per instruction
-  // The rows of a tile: gathered rows are loaded from idx here, but the row
-  // pointers are only formed in commit(), so a next tile's index loads stay
-  // in flight (behind the current tile's stages) instead of being waited for.
+  // AI (always-gathered sides): LDS bytes (NW * Q * 256) that receive the
+  // tile's row indices by DMA
+  uint32_t idx_lds = 0;
+  // The rows of a tile: gathered rows are looked up in idx here, but the row
+  // pointers are only formed in commit().  With AI the index loads are LDS
+  // DMA issued in program order with the stage DMA (inline asm the compiler
+  // cannot move), so a next tile's lookups are in flight behind the current
+  // tile's stages and land before its last full drain; loaded into registers,
+  // the compiler is free to sink them to their use after the k loop, where
+  // they would be waited for on the critical path.  With AI, idx must not be
+  // null.
   __device__ __forceinline__ void init(const uint16_t* base, int64_t ld, const int32_t* idx, int row_base, int nrows) {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6, lane = AI ? volatile_lane() : threadIdx.x & 63;
     base_ = base;
     ld_ = ld;
+    const uint32_t w = __builtin_amdgcn_readfirstlane(wave);
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
       const int lrow = RPI * (wave + NW * j) + lane / C;
       const int r = min(lrow, nrows - 1);
-      row_[j] = idx ? idx[row_base + r] : row_base + r;
+      if constexpr (AI) {
+        dma4(idx + row_base + r, idx_lds + (w * Q + j) * 256);
+        row_[j] = 0;  // read from LDS in commit()
+      } else {
+        row_[j] = idx ? idx[row_base + r] : row_base + r;
+      }
     }
   }
   // Called where the index loads are known to be complete (after a full
   // drain); the empty asm keeps the pointer arithmetic after that point.
   __device__ __forceinline__ void commit() {
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6, lane = AI ? volatile_lane() : threadIdx.x & 63;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
+      if constexpr (AI) row_[j] = *(const SMOE_LDS int32_t*)(uintptr_t)(idx_lds + (wave * Q + j) * 256 + lane * 4);
       asm volatile("" : "+v"(row_[j]));
       const int lrow = RPI * (wave + NW * j) + lane / C;
       const int logical = (lane % C) ^ swz(lrow);
@@ -262,14 +289,14 @@ struct KOuterSide {
   }
 };
 
-template <int MODE, int R, int BK, int NW>
+template <int MODE, int R, int BK, int NW, bool AI = false>
 struct SideT;
-template <int R, int BK, int NW>
-struct SideT<ROWS, R, BK, NW> {
-  using type = RowsSide<R, BK, NW>;
+template <int R, int BK, int NW, bool AI>
+struct SideT<ROWS, R, BK, NW, AI> {
+  using type = RowsSide<R, BK, NW, AI>;
 };
-template <int R, int BK, int NW>
-struct SideT<KOUTER, R, BK, NW> {
+template <int R, int BK, int NW, bool AI>
+struct SideT<KOUTER, R, BK, NW, AI> {
   using type = KOuterSide<R, BK, NW>;
 };
 
@@ -339,6 +366,13 @@ struct Sched {
 
 // Ops with a tail class define  int count_tail(const Params&, const int* sh)
 // (called after count() with the same sh).
+// Ops whose M side gathers rows define  static constexpr int IDX_LDS  (bytes
+// for the next tile's row indices, loaded by DMA).
+template <class Op, class = void>
+struct IdxLds : std::integral_constant<int, 0> {};
+template <class Op>
+struct IdxLds<Op, std::void_t<decltype(Op::IDX_LDS)>> : std::integral_constant<int, Op::IDX_LDS> {};
+
 template <class Op, class = void>
 struct HasCountTail : std::false_type {};
 template <class Op>
@@ -360,10 +394,14 @@ struct HasCountTail<Op, std::void_t<decltype(&Op::count_tail)>> : std::true_type
 template <class Op>
 __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_kernel(const typename Op::Params p) {
   using Cfg = typename Op::Cfg;
-  using MSide = typename SideT<Op::M_MODE, Cfg::BM, Cfg::BK, Cfg::NW>::type;
+  // an M side with IDX_LDS always gathers its rows: indices by LDS DMA
+  using MSide = typename SideT<Op::M_MODE, Cfg::BM, Cfg::BK, Cfg::NW, (IdxLds<Op>::value > 0)>::type;
   using NSide = typename SideT<Op::N_MODE, Cfg::BN, Cfg::BK, Cfg::NW>::type;
   constexpr int BM = Cfg::BM, BN = Cfg::BN, S = Cfg::STAGES, BK = Cfg::BK, SUB = Cfg::SUB;
-  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES + (Op::EPI_LDS > 0 ? Op::EPI_LDS : 16)];
+  constexpr int kEpiBytes = (Op::EPI_LDS > 0 ? (Op::EPI_LDS + 255) / 256 * 256 : 256);
+  constexpr int kIdxLds = IdxLds<Op>::value;
+  static_assert(Cfg::LDS_BYTES + kEpiBytes + kIdxLds <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES + kEpiBytes + kIdxLds];
   __shared__ int sh[16];  // [0..3], [4..7]: tile lookups of even / odd k; [8..9]: tile counts
   Sched sched;
   {
@@ -376,13 +414,15 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   TileInfo ti;
   // tile() may synchronise the workgroup: ids are workgroup-uniform
   if (id < 0 || !Op::tile(p, id, ti, sh)) return;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
   MSide ms, ms_next;
   NSide ns, ns_next;
+  if constexpr (kIdxLds > 0) ms.idx_lds = ms_next.idx_lds = lds0 + Cfg::LDS_BYTES + kEpiBytes;
   Op::init_m(p, ti, ms);
   Op::init_n(p, ti, ns);
+  if constexpr (kIdxLds > 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the first tile's index DMA
   ms.commit();
   ns.commit();
-  const uint32_t lds0 = (uint32_t)(uintptr_t)smem;
   const int wave = threadIdx.x >> 6;
   const int wm0 = Cfg::wave_m(wave) * (BM / Cfg::WM);
   const int wn0 = Cfg::wave_n(wave) * (BN / Cfg::WN);

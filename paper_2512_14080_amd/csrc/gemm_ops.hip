@@ -260,6 +260,7 @@ struct OpUp {
     }
   };
   static constexpr int EPI_LDS = 0;
+  static constexpr int IDX_LDS = Cfg::NW * Cfg::QM * 256;  // gathered X rows of the next tile
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
   }
@@ -269,7 +270,7 @@ struct OpUp {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, 2 * p.a.n, p.a.d, id, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW, true>& s) {
     s.init(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
   }
   static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
@@ -329,14 +330,9 @@ struct OpUp {
 constexpr int kStageBytesPerWave = 16 * 128;
 template <class Cfg>
 constexpr bool kStagedStores = Cfg::RN % 2 == 0 && Cfg::LDS_BYTES + Cfg::NW * kStageBytesPerWave + 256 <= 160 * 1024;
-// The lane index from a volatile asm: address arithmetic derived from it
-// stays in the epilogue instead of being hoisted out of the persistent tile
-// loop, where it would hold registers across the k loop.
-__device__ __forceinline__ int epilogue_lane() {
-  int l;
-  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
-  return l;
-}
+// Epilogue address arithmetic uses the lane index from a volatile asm, so
+// it stays in the epilogue instead of being hoisted out of the tile loop.
+__device__ __forceinline__ int epilogue_lane() { return volatile_lane(); }
 
 __device__ __forceinline__ void store_rows64_staged(char* wl, uint16_t* blk, int64_t ld, int rows_valid,
                                                     const u32x2 (&v0)[4], const u32x2 (&v1)[4]) {
@@ -462,6 +458,7 @@ struct OpDH {
   static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DHArgs a; };
   static constexpr int EPI_LDS = Cfg::BM * Cfg::WN * 4;  // dS partial sums [BM][WN]
+  static constexpr int IDX_LDS = Cfg::NW * Cfg::QM * 256;  // gathered dO rows of the next tile
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.n);
   }
@@ -471,7 +468,7 @@ struct OpDH {
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
     return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, p.a.n, p.a.d, id, ti);
   }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW, true>& s) {
     s.init(p.a.dO, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
   }
   static __device__ void init_n(const Params& p, const TileInfo& ti, RowsSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
@@ -488,70 +485,70 @@ struct OpDH {
     // first column of accumulator block j
     auto col_of = [&](int j) { return ti.n0 + wn * (Cfg::BN / Cfg::WN) + 32 * j; };
     float* red = (float*)smem;  // [BM][WN], the epilogue's own LDS
-    // H values of one accumulator row block (gate and up halves) and the
-    // row's routing score, double-buffered: the loads of block i+1 are in
-    // flight while block i is computed and stored.
-    u32x2 hg[2][RN][4], hu[2][RN][4];
-    float sw[2];
-    auto load_block = [&](int i, int b) {
+    // H values (gate and up halves) of one 32 x 32 accumulator block,
+    // double-buffered over the blocks in (i, j) order: the loads of the next
+    // block are in flight while this one is computed and stored.
+    float swr[RM];
+#pragma unroll
+    for (int i = 0; i < RM; ++i) {
+      const int m = m_of(i);
+      swr[i] = m < ti.mrows ? p.a.row_w[(size_t)(ti.row_base + m)] : 0.f;
+    }
+    u32x2 hg[2][4], hu[2][4];
+    auto load_block = [&](int blk, int b) {
+      const int i = blk / RN, j = blk % RN;
       const int m = m_of(i);
       const size_t row = (size_t)(ti.row_base + (m < ti.mrows ? m : 0));
       const uint16_t* h = p.a.H + row * (2 * n);
-      sw[b] = p.a.row_w[row];
-#pragma unroll
-      for (int j = 0; j < RN; ++j) {
-        const int col = col_of(j);
-        load_block_bf16(h + col, hg[b][j]);
-        load_block_bf16(h + n + col, hu[b][j]);
-      }
+      const int col = col_of(j);
+      load_block_bf16(h + col, hg[b]);
+      load_block_bf16(h + n + col, hu[b]);
     };
     load_block(0, 0);
+    float part = 0.f;
 #pragma unroll
-    for (int i = 0; i < RM; ++i) {
-      const int b = i & 1;
-      if (i + 1 < RM) load_block(i + 1, b ^ 1);
+    for (int blk = 0; blk < RM * RN; ++blk) {
+      const int i = blk / RN, j = blk % RN, b = blk & 1;
+      if (blk + 1 < RM * RN) load_block(blk + 1, b ^ 1);
       const int m = m_of(i);
       const bool valid = m < ti.mrows;
       const size_t row = (size_t)(ti.row_base + (valid ? m : 0));
-      const float s = valid ? sw[b] : 0.f;
-      uint16_t* dh = p.a.dH + row * (2 * n);
-      uint16_t* ap = p.a.Ap + row * n;
-      float part = 0.f;
+      const float s = swr[i];
+      if (j == 0) part = 0.f;
       if (valid) {
+        uint16_t* dh = p.a.dH + row * (2 * n);
+        uint16_t* ap = p.a.Ap + row * n;
+        const int col = col_of(j);
+        u32x2 vg[4], vu[4], va[4];
 #pragma unroll
-        for (int j = 0; j < RN; ++j) {
-          const int col = col_of(j);
-          u32x2 vg[4], vu[4], va[4];
+        for (int g = 0; g < 4; ++g) {
+          const float gv[4] = {bf_lo(hg[b][g][0]), bf_hi(hg[b][g][0]), bf_lo(hg[b][g][1]), bf_hi(hg[b][g][1])};
+          const float uv[4] = {bf_lo(hu[b][g][0]), bf_hi(hu[b][g][0]), bf_lo(hu[b][g][1]), bf_hi(hu[b][g][1])};
+          float dg[4], du[4], apv[4];
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const float gv[4] = {bf_lo(hg[b][j][g][0]), bf_hi(hg[b][j][g][0]), bf_lo(hg[b][j][g][1]),
-                                 bf_hi(hg[b][j][g][1])};
-            const float uv[4] = {bf_lo(hu[b][j][g][0]), bf_hi(hu[b][j][g][0]), bf_lo(hu[b][j][g][1]),
-                                 bf_hi(hu[b][j][g][1])};
-            float dg[4], du[4], apv[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const float dap = t.acc[i][j][4 * g + r];
-              float sg;
-              const float sl = silu_sig(gv[r], &sg);
-              const float av = sl * uv[r];
-              part += dap * av;
-              const float da = s * dap;
-              dg[r] = da * uv[r] * sg * (1.f + gv[r] * (1.f - sg));
-              du[r] = da * sl;
-              apv[r] = s * av;
-            }
-            vg[g] = pack_bf16x4(dg[0], dg[1], dg[2], dg[3]);
-            vu[g] = pack_bf16x4(du[0], du[1], du[2], du[3]);
-            va[g] = pack_bf16x4(apv[0], apv[1], apv[2], apv[3]);
+          for (int r = 0; r < 4; ++r) {
+            const float dap = t.acc[i][j][4 * g + r];
+            float sg;
+            const float sl = silu_sig(gv[r], &sg);
+            const float av = sl * uv[r];
+            part += dap * av;
+            const float da = s * dap;
+            dg[r] = da * uv[r] * sg * (1.f + gv[r] * (1.f - sg));
+            du[r] = da * sl;
+            apv[r] = s * av;
           }
-          store_block_bf16(dh + col, vg);
-          store_block_bf16(dh + n + col, vu);
-          store_block_bf16(ap + col, va);
+          vg[g] = pack_bf16x4(dg[0], dg[1], dg[2], dg[3]);
+          vu[g] = pack_bf16x4(du[0], du[1], du[2], du[3]);
+          va[g] = pack_bf16x4(apv[0], apv[1], apv[2], apv[3]);
         }
+        store_block_bf16(dh + col, vg);
+        store_block_bf16(dh + n + col, vu);
+        store_block_bf16(ap + col, va);
       }
-      part += __shfl_xor(part, 32, kWave);
-      if (lane < 32) red[m * Cfg::WN + wn] = part;
+      if (j == RN - 1) {
+        float q = part + __shfl_xor(part, 32, kWave);
+        if (lane < 32) red[m * Cfg::WN + wn] = q;
+      }
     }
     barrier_lds();
     const int nnt = n / Cfg::BN;
