@@ -373,6 +373,17 @@ struct IdxLds : std::integral_constant<int, 0> {};
 template <class Op>
 struct IdxLds<Op, std::void_t<decltype(Op::IDX_LDS)>> : std::integral_constant<int, Op::IDX_LDS> {};
 
+// Ops define  static constexpr int EPI_STORES : a lower bound on the vector
+// memory instructions each wave issues in the epilogue of a full tile (all
+// BM rows valid).  A wave's vector memory operations retire in issue order,
+// loads and stores alike, so a wait for stage 0 of a tile only has to leave
+// outstanding the operations issued after it: the other prologue stages and
+// the previous tile's epilogue stores.
+template <class Op, class = void>
+struct EpiStores : std::integral_constant<int, 0> {};
+template <class Op>
+struct EpiStores<Op, std::void_t<decltype(Op::EPI_STORES)>> : std::integral_constant<int, Op::EPI_STORES> {};
+
 template <class Op, class = void>
 struct HasCountTail : std::false_type {};
 template <class Op>
@@ -440,7 +451,11 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
         if constexpr (Op::M_MODE == KOUTER) a.prefetch_idx(st * BK);
         if constexpr (Op::N_MODE == KOUTER) b.prefetch_idx(st * BK);
         if constexpr (Op::M_MODE == KOUTER || Op::N_MODE == KOUTER) {
-          asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+          // gathered k rows: this stage's row indices must have arrived
+          bool g = false;
+          if constexpr (Op::M_MODE == KOUTER) g = g || a.gidx != nullptr;
+          if constexpr (Op::N_MODE == KOUTER) g = g || b.gidx != nullptr;
+          if (g) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
           if constexpr (Op::M_MODE == KOUTER) a.idx_commit();
           if constexpr (Op::N_MODE == KOUTER) b.idx_commit();
         }
@@ -455,6 +470,7 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   Acc<Cfg> acc;
   acc.zero();
   prologue(ti, ms, ns);
+  bool prev_full = false;  // the epilogue just issued was a full tile's
   for (int k = 0;; ++k) {
     // next tile: lookup and side setup overlap this tile's first DMA
     int idn = sched.id(k + 1);
@@ -479,7 +495,15 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
       // ops remain.  At kt = 0 the previous epilogue's stores are younger than
       // stage 0, and gathered index loads are younger than the DMA: full drain.
       const int ahead = (kt == 0 || gathered) ? 0 : min(S - 2, nk - 1 - kt);
-      if (ahead >= 2)
+      // stage 0: the younger prologue stages and epilogue stores may stay outstanding
+      constexpr int kYoung = (S - 2) * kPerStage;
+      constexpr int kYoungEpi = kYoung + EpiStores<Op>::value < 63 ? kYoung + EpiStores<Op>::value : 63;
+      if (kt == 0 && !gathered && nk >= S - 1 && (kYoung > 0 || prev_full)) {
+        if (prev_full)
+          wait_vm_barrier<kYoungEpi>();
+        else
+          wait_vm_barrier<kYoung>();
+      } else if (ahead >= 2)
         wait_vm_barrier<(S >= 4 ? 2 : 0) * kPerStage>();
       else if (ahead == 1)
         wait_vm_barrier<(S >= 3 ? 1 : 0) * kPerStage>();
@@ -555,6 +579,7 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
       prologue(tn, ms, ns);
     }
     Op::epilogue(p, ti, acc, smem + Cfg::LDS_BYTES);
+    prev_full = ti.mrows == BM;
     if (idn < 0) break;
     ti = tn;
     acc.zero();

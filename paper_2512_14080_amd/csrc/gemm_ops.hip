@@ -261,6 +261,8 @@ struct OpUp {
   };
   static constexpr int EPI_LDS = 0;
   static constexpr int IDX_LDS = Cfg::NW * Cfg::QM * 256;  // gathered X rows of the next tile
+  // full tile: per row block, H gate, H up and A, two stores each
+  static constexpr int EPI_STORES = Cfg::RM * (Cfg::RN / 2) * 6;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
   }
@@ -330,6 +332,10 @@ struct OpUp {
 constexpr int kStageBytesPerWave = 16 * 128;
 template <class Cfg>
 constexpr bool kStagedStores = Cfg::RN % 2 == 0 && Cfg::LDS_BYTES + Cfg::NW * kStageBytesPerWave + 256 <= 160 * 1024;
+// store instructions per wave of store_rows_bf16 on a full tile: staged, four
+// per 64-column row block (two rounds of two); direct, two per 32 columns
+template <class Cfg>
+constexpr int kStoresPerFullTile = kStagedStores<Cfg> ? Cfg::RM * (Cfg::RN / 2) * 4 : Cfg::RM * Cfg::RN * 2;
 // Epilogue address arithmetic uses the lane index from a volatile asm, so
 // it stays in the epilogue instead of being hoisted out of the tile loop.
 __device__ __forceinline__ int epilogue_lane() { return volatile_lane(); }
@@ -427,6 +433,7 @@ struct OpDown {
   static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
   struct Params { DownArgs a; };
   static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
+  static constexpr int EPI_STORES = kStoresPerFullTile<Cfg>;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.d);
   }
@@ -459,6 +466,8 @@ struct OpDH {
   struct Params { DHArgs a; };
   static constexpr int EPI_LDS = Cfg::BM * Cfg::WN * 4;  // dS partial sums [BM][WN]
   static constexpr int IDX_LDS = Cfg::NW * Cfg::QM * 256;  // gathered dO rows of the next tile
+  // full tile: per 32 x 32 block, dH gate, dH up and A', two stores each
+  static constexpr int EPI_STORES = Cfg::RM * Cfg::RN * 6;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.n);
   }
@@ -573,6 +582,7 @@ struct OpDXt {
   static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DXtArgs a; };
   static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
+  static constexpr int EPI_STORES = kStoresPerFullTile<Cfg>;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.d);
   }
