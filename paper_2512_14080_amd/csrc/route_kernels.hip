@@ -694,12 +694,20 @@ static size_t topk_lds_bytes(int E, int K, bool stash) {
 hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
                              uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s) {
   if (E % 4 == 0 && E <= 256 && K <= 8 && K <= E) {
+    // LDS beyond the default 64 KB of dynamic LDS is granted per kernel
 #define SMOE_TOPK_LANE(KM, NW)                                                                                    \
-  topk_lane_kernel<KM, NW><<<dim3(W), dim3(64 * NW), topk_lane_lds(E, KM, NW), s>>>(                              \
-      in, scores, scores_t, topk_idx, topk_w, mask, T, E, K, W, do_softmax)
-    // four waves per word when the experts split into four slices of whole
-    // float4s and the workgroup's LDS stays within the default 64 KB
-    const bool four = E % 16 == 0 && topk_lane_lds(E, 8, 4) <= 65536;
+  do {                                                                                                            \
+    const size_t lds = topk_lane_lds(E, KM, NW);                                                                  \
+    if (lds > 65536) {                                                                                            \
+      const hipError_t e = hipFuncSetAttribute((const void*)topk_lane_kernel<KM, NW>,                             \
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);            \
+      if (e != hipSuccess) return e;                                                                              \
+    }                                                                                                             \
+    topk_lane_kernel<KM, NW><<<dim3(W), dim3(64 * NW), lds, s>>>(in, scores, scores_t, topk_idx, topk_w, mask, T, \
+                                                                 E, K, W, do_softmax);                            \
+  } while (0)
+    // four waves per word when the experts split into four slices of whole float4s
+    const bool four = E % 16 == 0;
     if (K <= 2) {
       if (four) SMOE_TOPK_LANE(2, 4); else SMOE_TOPK_LANE(2, 1);
     } else if (K <= 4) {
