@@ -343,7 +343,7 @@ constexpr int kPartialTile = 1 << 30;  // flag on a tile id: index among the par
 // same amount of work, and the tail tiles form the last rounds.  id() returns
 // main tiles as their index and tail tiles as kPartialTile | index in class.
 struct Sched {
-  int nmain, ntail, cm, ct, fx, hx, gx, x, slot;
+  int nmain, ntail, cm, ct, fx, hx, gx, x, slot, base;
   __device__ __forceinline__ void init(int ntiles, int tail) {
     ntail = tail;
     nmain = ntiles - tail;
@@ -354,15 +354,32 @@ struct Sched {
     slot = blockIdx.x >> 3;
     fx = max(0, min(cm, nmain - x * cm));
     hx = max(0, min(ct, ntail - x * ct));
+    base = x * cm;
+  }
+  // the op gives each XCD its own range [begin, begin + count) (no tail class)
+  __device__ __forceinline__ void init_range(int begin, int count) {
+    ntail = ct = hx = 0;
+    gx = gridDim.x >> 3;
+    x = blockIdx.x & 7;
+    slot = blockIdx.x >> 3;
+    nmain = fx = cm = count;
+    base = begin;
   }
   // logical id of this workgroup's k-th tile, or -1 when it has no more
   __device__ __forceinline__ int id(int k) const {
     const int l = slot + k * gx;
-    if (l < fx) return x * cm + l;
+    if (l < fx) return base + l;
     if (l < fx + hx) return kPartialTile | (x * ct + (l - fx));
     return -1;
   }
 };
+
+// Ops that place their tiles on the XCDs themselves define
+//   void xcd_range(const Params&, int xcd, int* begin, int* count)
+template <class Op, class = void>
+struct HasXcdRange : std::false_type {};
+template <class Op>
+struct HasXcdRange<Op, std::void_t<decltype(&Op::xcd_range)>> : std::true_type {};
 
 // Ops with a tail class define  int count_tail(const Params&, const int* sh)
 // (called after count() with the same sh).
@@ -415,7 +432,11 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES + kEpiBytes + kIdxLds];
   __shared__ int sh[16];  // [0..3], [4..7]: tile lookups of even / odd k; [8..9]: tile counts
   Sched sched;
-  {
+  if constexpr (HasXcdRange<Op>::value) {
+    int b, c;
+    Op::xcd_range(p, blockIdx.x & 7, &b, &c);
+    sched.init_range(b, c);
+  } else {
     const int ntiles = Op::count(p, sh + 8);
     int tail = 0;
     if constexpr (HasCountTail<Op>::value) tail = Op::count_tail(p, sh + 8);

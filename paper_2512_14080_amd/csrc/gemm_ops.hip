@@ -72,10 +72,9 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 size_t mtiles_bytes(int64_t capacity, int E) { return 16 * (size_t)(1 + capacity / kMTile + E); }
 
 constexpr int kMTilesThreads = 1024;
-__global__ __launch_bounds__(kMTilesThreads) void mtiles_kernel(const int32_t* __restrict__ offsets, int E,
-                                                               int32_t* __restrict__ out) {
-  __shared__ int pf[4097], pp[4097];  // per-expert exclusive prefix of full / partial m-tiles
-  __shared__ int scan_lds[kMTilesThreads / 64];
+// pf, pp: LDS [4097] each (per-expert exclusive prefix of full / partial m-tiles)
+__device__ __forceinline__ void mtiles_body(const int32_t* __restrict__ offsets, int E, int32_t* __restrict__ out,
+                                            int* pf, int* pp, int* scan_lds) {
   const int tid = threadIdx.x;
   // thread t owns experts 4t .. 4t+3 (E <= 4096)
   int nf[4], np[4], sf = 0, sp = 0;
@@ -123,10 +122,226 @@ __global__ __launch_bounds__(kMTilesThreads) void mtiles_kernel(const int32_t* _
   }
 }
 
+__global__ __launch_bounds__(kMTilesThreads) void mtiles_kernel(const int32_t* __restrict__ offsets, int E,
+                                                               int32_t* __restrict__ out) {
+  __shared__ int pf[4097], pp[4097];
+  __shared__ int scan_lds[kMTilesThreads / 64];
+  mtiles_body(offsets, E, out, pf, pp, scan_lds);
+}
+
 hipError_t launch_mtiles(const int32_t* offsets, int E, int32_t* out, hipStream_t s) {
   if (E > 4096) return hipErrorInvalidValue;
   mtiles_kernel<<<1, kMTilesThreads, 0, s>>>(offsets, E, out);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------ k-chunk list
+// The weight gradients reduce over an expert's rows (varlen K).  With skewed
+// routing a few experts own most rows, and their tiles would run for the
+// whole kernel on a handful of CUs.  The k-chunk list cuts every expert with
+// more than Kc rows into Kc-row chunks (Kc = max(kKcMin, 2P / slabs), so the
+// chunks need at most `slabs` fp32 partial slabs); a split expert's chunks
+// write fp32 partials that dw_reduce_kernel sums in chunk order, the others
+// store bf16 directly.  Entries: split chunks first (the long ones), then
+// the unsplit experts in expert order.  The tiles (entry-major) are cut into
+// 8 contiguous ranges, one per XCD: of equal work when some expert is split
+// (work of a tile: its k steps plus a fixed cost for the prologue and
+// epilogue), else of equal count, as for the other GEMMs.
+// Layout (int32): header[16] = {entries, split experts, Kc, tiles,
+// xcd_start[0..8]}; entries at 16 (int4 {e, k_begin, k_len, slot or -1});
+// split experts at 16 + 4 * (E + kDwSlabs) (int4 {e, first slot, chunks, 0}).
+constexpr int kKcMin = 2048;
+constexpr int kTileFixedSteps = 4;  // prologue + epilogue, in k steps of 64
+constexpr int kKChunksThreads = 1024;
+
+size_t kchunks_bytes(int E) { return 4 * (16 + 4 * (size_t)(E + kDwSlabs) + 4 * (kDwSlabs / 2 + 1)); }
+
+// wpre: LDS [4096 + kDwSlabs + 1] (work prefix over entries)
+__device__ __forceinline__ void kchunks_body(const int32_t* __restrict__ offsets, int E, int tpe, int slabs,
+                                             int32_t* __restrict__ out, int* wpre, int* scan_lds, int* sh_kc) {
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    const int P = offsets[E];
+    int kc = 0x7fffffff;  // no slabs: nothing is split
+    if (slabs > 0) {
+      const int64_t q = (2 * (int64_t)P + slabs - 1) / slabs;
+      kc = (int)max((int64_t)kKcMin, (q + 63) / 64 * 64);
+    }
+    *sh_kc = kc;
+  }
+  __syncthreads();
+  const int Kc = *sh_kc;
+  // thread t owns experts 4t .. 4t+3 (E <= 4096)
+  int f[4], nc[4], sc = 0, su = 0, sx = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    f[q] = e < E ? offsets[e + 1] - offsets[e] : 0;
+    nc[q] = (e < E && f[q] > Kc) ? (f[q] + Kc - 1) / Kc : 0;  // chunks of a split expert
+    sc += nc[q];
+    su += (e < E && nc[q] == 0);
+    sx += nc[q] > 0;
+  }
+  int S, U, X;
+  int bc = block_excl_scan<kKChunksThreads>(sc, &S, scan_lds);
+  int bu = block_excl_scan<kKChunksThreads>(su, &U, scan_lds);
+  int bx = block_excl_scan<kKChunksThreads>(sx, &X, scan_lds);
+  i32x4* ent = (i32x4*)(out + 16);
+  i32x4* spl = (i32x4*)(out + 16 + 4 * (E + kDwSlabs));
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = 4 * tid + q;
+    if (e >= E) continue;
+    const int k0 = offsets[e];
+    if (nc[q] > 0) {
+      for (int c = 0; c < nc[q]; ++c) {
+        const int kb = c * Kc;
+        ent[bc + c] = i32x4{e, k0 + kb, min(Kc, f[q] - kb), bc + c};  // slot = chunk position
+      }
+      spl[bx] = i32x4{e, bc, nc[q], 0};
+      bc += nc[q];
+      ++bx;
+    } else {
+      ent[S + bu] = i32x4{e, k0, f[q], -1};
+      ++bu;
+    }
+  }
+  const int N = S + U;
+  __syncthreads();  // entries written (read back below by other threads)
+  // work prefix over entries: up to 5 entries per thread (E + slabs <= 4160)
+  int w[5], sw = 0;
+#pragma unroll
+  for (int q = 0; q < 5; ++q) {
+    const int i = 5 * tid + q;
+    w[q] = i < N ? tpe * ((ent[i][2] + 63) / 64 + kTileFixedSteps) : 0;
+    sw += w[q];
+  }
+  int Wt;
+  int bw = block_excl_scan<kKChunksThreads>(sw, &Wt, scan_lds);
+#pragma unroll
+  for (int q = 0; q < 5; ++q) {
+    const int i = 5 * tid + q;
+    if (i < N) wpre[i] = bw;
+    bw += w[q];
+  }
+  if (tid == 0) wpre[N] = Wt;
+  __syncthreads();
+  if (tid == 0) {
+    out[0] = N;
+    out[1] = X;
+    out[2] = Kc;
+    out[3] = N * tpe;
+    out[4] = 0;
+    out[12] = N * tpe;
+  }
+  if (tid >= 1 && tid < 8 && X == 0) {
+    // nothing split: equal tile counts (tiles of like length, so no XCD and no
+    // workgroup gets an extra round)
+    out[4 + tid] = min(N * tpe, tid * ((N * tpe + 7) / 8));
+  } else if (tid >= 1 && tid < 8) {
+    // first tile whose work starts at or after tid / 8 of the total
+    const int target = (int)((int64_t)Wt * tid / 8);
+    int lo = 0, hi = N;  // wpre[lo] <= target < wpre[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (wpre[mid] <= target) lo = mid; else hi = mid;
+    }
+    int start = N * tpe;
+    if (N > 0) {
+      const int wt = (wpre[lo + 1] - wpre[lo]) / tpe;  // work of one tile of entry lo
+      const int j = wt > 0 ? min(tpe, (target - wpre[lo] + wt - 1) / wt) : 0;
+      start = lo * tpe + j;
+    }
+    out[4 + tid] = start;
+  }
+}
+
+// The backward's tile lists in one launch: workgroup 0 the m-tile list,
+// 1 and 2 the k-chunk lists of dW2 and dW1.
+static_assert(kMTilesThreads == kKChunksThreads, "one workgroup size");
+__global__ __launch_bounds__(kMTilesThreads) void bwd_lists_kernel(const int32_t* __restrict__ offsets, int E,
+                                                                  int32_t* __restrict__ mtiles, int tpe2, int slabs2,
+                                                                  int32_t* __restrict__ klist2, int tpe1, int slabs1,
+                                                                  int32_t* __restrict__ klist1) {
+  __shared__ int lds[2 * 4097];
+  __shared__ int scan_lds[kMTilesThreads / 64];
+  __shared__ int sh_kc;
+  if (blockIdx.x == 0)
+    mtiles_body(offsets, E, mtiles, lds, lds + 4097, scan_lds);
+  else if (blockIdx.x == 1)
+    kchunks_body(offsets, E, tpe2, slabs2, klist2, lds, scan_lds, &sh_kc);
+  else
+    kchunks_body(offsets, E, tpe1, slabs1, klist1, lds, scan_lds, &sh_kc);
+}
+
+// partials of split experts -> bf16 dW: chunk slabs summed in chunk order
+__global__ __launch_bounds__(256) void dw_reduce_kernel(const int32_t* __restrict__ klist, const float* __restrict__ part,
+                                                        uint16_t* __restrict__ dW, int E, int64_t MN) {
+  const SMOE_CONST int32_t* h = (const SMOE_CONST int32_t*)klist;
+  const int si = blockIdx.y;
+  if (si >= h[1]) return;
+  const SMOE_CONST i32x4* spl = (const SMOE_CONST i32x4*)(klist + 16 + 4 * (E + kDwSlabs));
+  const i32x4 sp = spl[si];
+  const int e = sp[0], first = sp[1], nc = sp[2];
+  for (int64_t i = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x); i < MN; i += 4 * (int64_t)gridDim.x * 256) {
+    f32x4 a = *(const f32x4*)(part + (size_t)first * MN + i);
+    for (int c = 1; c < nc; ++c) {
+      const f32x4 b = *(const f32x4*)(part + (size_t)(first + c) * MN + i);
+      a[0] += b[0];
+      a[1] += b[1];
+      a[2] += b[2];
+      a[3] += b[3];
+    }
+    *(u32x2*)(dW + (size_t)e * MN + i) = u32x2{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3])};
+  }
+}
+
+hipError_t launch_dw_reduce(const int32_t* klist, const float* part, uint16_t* dW, int E, int64_t MN, int slabs,
+                            hipStream_t s) {
+  if (slabs <= 0) return hipSuccess;
+  const int gx = (int)std::min<int64_t>((MN / 4 + 255) / 256, 64);
+  dw_reduce_kernel<<<dim3(gx, slabs / 2), dim3(256), 0, s>>>(klist, part, dW, E, MN);
+  return hipGetLastError();
+}
+
+// A varlen-K tile from the k-chunk list: entry = id / (tiles per entry).
+template <int BM, int BN>
+__device__ __forceinline__ bool tile_kchunk(const int32_t* klist, int E, int M, int N, int id, TileInfo& ti) {
+  const int mtn = M / BM, ntn = N / BN;
+  const SMOE_CONST i32x4* ent = (const SMOE_CONST i32x4*)(klist + 16);
+  const i32x4 t = ent[id / (mtn * ntn)];
+  const int rem = id % (mtn * ntn);
+  ti.e = t[0];
+  ti.m0 = (rem / ntn) * BM;
+  ti.n0 = (rem % ntn) * BN;
+  ti.mrows = BM;
+  ti.row_base = t[3];  // partial slab, or -1
+  ti.k_begin = t[1];
+  ti.k_len = t[2];
+  return true;
+}
+__device__ __forceinline__ void kchunk_xcd_range(const int32_t* klist, int x, int* begin, int* count) {
+  const SMOE_CONST int32_t* h = (const SMOE_CONST int32_t*)klist;
+  *begin = h[4 + x];
+  *count = h[5 + x] - h[4 + x];
+}
+
+// fp32 tile of a partial slab [M][ld]
+template <class Cfg>
+__device__ __forceinline__ void store_part_f32(float* out, int64_t ld, int m0, int n0, Acc<Cfg>& t) {
+#pragma unroll
+  for (int i = 0; i < Cfg::RM; ++i) {
+    float* o = out + (size_t)(m0 + t.m_of(i)) * ld + n0;
+#pragma unroll
+    for (int j = 0; j < Cfg::RN; ++j)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 v;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[q] = t.acc[i][j][4 * g + q];
+        *(f32x4*)(o + t.n_of(j, g)) = v;
+      }
+  }
 }
 
 // Logical tile ids are m-tile-major within their class (full m-tiles, then
@@ -177,21 +392,6 @@ __device__ __forceinline__ bool tile_plain_m(int M, int N, int K, int id, TileIn
   ti.n0 = nt * BN;
   ti.k_begin = 0;
   ti.k_len = K;
-  return true;
-}
-
-// varlen-K: one tile per (expert, m-tile, n-tile); k = the expert's rows
-template <int BM, int BN>
-__device__ __forceinline__ bool tile_varlen_k(const int32_t* offsets, int M, int N, int id, TileInfo& ti) {
-  const int mtn = M / BM, ntn = N / BN;
-  ti.e = id / (mtn * ntn);
-  const int rem = id % (mtn * ntn);
-  ti.m0 = (rem / ntn) * BM;
-  ti.n0 = (rem % ntn) * BN;
-  ti.mrows = BM;
-  ti.row_base = 0;
-  ti.k_begin = offsets[ti.e];
-  ti.k_len = offsets[ti.e + 1] - ti.k_begin;
   return true;
 }
 
@@ -612,9 +812,12 @@ struct OpDW2 {
   static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW2Args a; };
   static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
-  static __device__ int count(const Params& p, int*) { return p.a.E * (p.a.n / Cfg::BM) * (p.a.d / Cfg::BN); }
+  static __device__ int count(const Params& p, int*) { return ((const SMOE_CONST int32_t*)p.a.klist)[3]; }
+  static __device__ void xcd_range(const Params& p, int x, int* begin, int* cnt) {
+    kchunk_xcd_range(p.a.klist, x, begin, cnt);
+  }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
-    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.n, p.a.d, id, ti);
+    return tile_kchunk<Cfg::BM, Cfg::BN>(p.a.klist, p.a.E, p.a.n, p.a.d, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.Ap, p.a.n, nullptr, ti.k_begin, ti.k_len, p.a.n, ColOffset{ti.m0});
@@ -623,7 +826,10 @@ struct OpDW2 {
     s.init(p.a.dO, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
-    store_rows_bf16<Cfg>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti.m0, Cfg::BM, ti.n0, t, epi);
+    if (ti.row_base >= 0)
+      store_part_f32<Cfg>(p.a.part + (size_t)ti.row_base * p.a.n * p.a.d, p.a.d, ti.m0, ti.n0, t);
+    else
+      store_rows_bf16<Cfg>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti.m0, Cfg::BM, ti.n0, t, epi);
   }
 };
 
@@ -634,9 +840,12 @@ struct OpDW1 {
   static constexpr int M_MODE = KOUTER, N_MODE = KOUTER;
   struct Params { DW1Args a; };
   static constexpr int EPI_LDS = kStagedStores<Cfg> ? Cfg::NW * kStageBytesPerWave : 0;
-  static __device__ int count(const Params& p, int*) { return p.a.E * (p.a.d / Cfg::BM) * (2 * p.a.n / Cfg::BN); }
+  static __device__ int count(const Params& p, int*) { return ((const SMOE_CONST int32_t*)p.a.klist)[3]; }
+  static __device__ void xcd_range(const Params& p, int x, int* begin, int* cnt) {
+    kchunk_xcd_range(p.a.klist, x, begin, cnt);
+  }
   static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
-    return tile_varlen_k<Cfg::BM, Cfg::BN>(p.a.offsets, p.a.d, 2 * p.a.n, id, ti);
+    return tile_kchunk<Cfg::BM, Cfg::BN>(p.a.klist, p.a.E, p.a.d, 2 * p.a.n, id, ti);
   }
   static __device__ void init_m(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BM, Cfg::BK, Cfg::NW>& s) {
     s.init(p.a.X, p.a.d, p.a.row_token, ti.k_begin, ti.k_len, p.a.d, ColOffset{ti.m0});
@@ -645,7 +854,10 @@ struct OpDW1 {
     s.init(p.a.dH, 2 * p.a.n, nullptr, ti.k_begin, ti.k_len, 2 * p.a.n, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
-    store_rows_bf16<Cfg>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, Cfg::BM, ti.n0, t, epi);
+    if (ti.row_base >= 0)
+      store_part_f32<Cfg>(p.a.part + (size_t)ti.row_base * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, ti.n0, t);
+    else
+      store_rows_bf16<Cfg>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, Cfg::BM, ti.n0, t, epi);
   }
 };
 
@@ -780,22 +992,66 @@ using W64x256 = GemmCfg<64, 256, 2, 4, 2>;
 using W128x128 = GemmCfg<128, 128, 4, 2, 2>;
 using W64x128 = GemmCfg<64, 128, 2, 4, 2>;
 
+// slabs of one weight-gradient GEMM: at most kDwSlabs, within kDwSlabBytes
+int dw_slabs(int64_t mn) {
+  const int64_t b = kDwSlabBytes / (mn * 4);
+  return (int)std::min<int64_t>(kDwSlabs, b) & ~1;
+}
+size_t dw_part_bytes(int d, int n) {
+  const int64_t mn = (int64_t)d * n;
+  return (size_t)std::max<int64_t>(dw_slabs(2 * mn) * 2 * mn, dw_slabs(mn) * mn) * 4;
+}
+
+// tile shapes of the weight-gradient GEMMs (their k-chunk lists are built
+// for these shapes); dW2: M = n, N = d; dW1: M = d, N = 2n
+static void dw2_tile(int d, int n, int* bm, int* bn) {
+  *bn = d % 256 == 0 ? 256 : 128;
+  *bm = (*bn == 256 && n % 256 == 0) ? 256 : (n % 128 == 0 ? 128 : 64);
+}
+static void dw1_tile(int d, int n, int* bm, int* bn) {
+  *bm = *bn = (d % 256 == 0 && (2 * n) % 256 == 0) ? 256 : 128;
+}
+
+hipError_t launch_bwd_lists(const int32_t* offsets, int E, int d, int n, int32_t* mtiles, int32_t* klist2,
+                            int32_t* klist1, hipStream_t s) {
+  if (E > 4096) return hipErrorInvalidValue;
+  int bm2, bn2, bm1, bn1;
+  dw2_tile(d, n, &bm2, &bn2);
+  dw1_tile(d, n, &bm1, &bn1);
+  const int tpe2 = (n / bm2) * (d / bn2), tpe1 = (d / bm1) * (2 * n / bn1);
+  bwd_lists_kernel<<<3, kMTilesThreads, 0, s>>>(offsets, E, mtiles, tpe2, dw_slabs((int64_t)n * d), klist2, tpe1,
+                                                dw_slabs((int64_t)d * 2 * n), klist1);
+  return hipGetLastError();
+}
+
+// the GEMM over the k-chunk list, then the partials of split experts
+template <class Op, class Args>
+static hipError_t run_dw(const Args& a, int M, int N, uint16_t* dW, hipStream_t s) {
+  using Cfg = typename Op::Cfg;
+  const int tpe = (M / Cfg::BM) * (N / Cfg::BN);
+  const int slabs = dw_slabs((int64_t)M * N);
+  hipError_t err = run<Op>({a}, pad8((a.E + slabs) * tpe), s);
+  if (err != hipSuccess) return err;
+  return launch_dw_reduce(a.klist, a.part, dW, a.E, (int64_t)M * N, slabs, s);
+}
+
 hipError_t launch_dw2(const DW2Args& a, hipStream_t s) {
-  // M = n, N = d
-  if (a.d % 256 == 0) {
-    if (a.n % 256 == 0) return run<OpDW2<W256x256>>({a}, pad8(a.E * (a.n / 256) * (a.d / 256)), s);
-    if (a.n % 128 == 0) return run<OpDW2<W128x256>>({a}, pad8(a.E * (a.n / 128) * (a.d / 256)), s);
-    return run<OpDW2<W64x256>>({a}, pad8(a.E * (a.n / 64) * (a.d / 256)), s);
+  int bm, bn;
+  dw2_tile(a.d, a.n, &bm, &bn);
+  if (bn == 256) {
+    if (bm == 256) return run_dw<OpDW2<W256x256>>(a, a.n, a.d, a.dW2, s);
+    if (bm == 128) return run_dw<OpDW2<W128x256>>(a, a.n, a.d, a.dW2, s);
+    return run_dw<OpDW2<W64x256>>(a, a.n, a.d, a.dW2, s);
   }
-  if (a.n % 128 == 0) return run<OpDW2<W128x128>>({a}, pad8(a.E * (a.n / 128) * (a.d / 128)), s);
-  return run<OpDW2<W64x128>>({a}, pad8(a.E * (a.n / 64) * (a.d / 128)), s);
+  if (bm == 128) return run_dw<OpDW2<W128x128>>(a, a.n, a.d, a.dW2, s);
+  return run_dw<OpDW2<W64x128>>(a, a.n, a.d, a.dW2, s);
 }
 
 hipError_t launch_dw1(const DW1Args& a, hipStream_t s) {
-  // M = d, N = 2n
-  if (a.d % 256 == 0 && (2 * a.n) % 256 == 0)
-    return run<OpDW1<W256x256>>({a}, pad8(a.E * (a.d / 256) * (2 * a.n / 256)), s);
-  return run<OpDW1<W128x128>>({a}, pad8(a.E * (a.d / 128) * (2 * a.n / 128)), s);
+  int bm, bn;
+  dw1_tile(a.d, a.n, &bm, &bn);
+  if (bm == 256) return run_dw<OpDW1<W256x256>>(a, a.d, 2 * a.n, a.dW1, s);
+  return run_dw<OpDW1<W128x128>>(a, a.d, 2 * a.n, a.dW1, s);
 }
 
 int dwr_splits(int T, int d, int E) {

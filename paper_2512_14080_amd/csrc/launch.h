@@ -53,15 +53,31 @@ struct DXtArgs {
 };
 hipError_t launch_dxt(const DXtArgs& a, hipStream_t s);
 
+// Weight gradients (varlen K over each expert's rows).  klist: the GEMM's
+// k-chunk list (kchunks_bytes(E) bytes, written by launch_bwd_lists); part:
+// dw_part_bytes(d, n) bytes of fp32 partials for experts split into row
+// chunks.
+constexpr int kDwSlabs = 64;                                 // partial slabs per GEMM at most
+constexpr int64_t kDwSlabBytes = (int64_t)256 << 20;         // and at most this many bytes
+size_t kchunks_bytes(int E);
+size_t dw_part_bytes(int d, int n);
+int dw_slabs(int64_t mn);
+// the backward's m-tile list (as launch_mtiles) and the k-chunk lists of dW2
+// and dW1, in one launch
+hipError_t launch_bwd_lists(const int32_t* offsets, int E, int d, int n, int32_t* mtiles, int32_t* klist2,
+                            int32_t* klist1, hipStream_t s);
+
 struct DW2Args {
   const uint16_t* Ap; const uint16_t* dO; const int32_t* offsets; const int32_t* row_token; uint16_t* dW2;
   int d, n, E;
+  int32_t* klist; float* part;
 };
 hipError_t launch_dw2(const DW2Args& a, hipStream_t s);
 
 struct DW1Args {
   const uint16_t* X; const uint16_t* dH; const int32_t* offsets; const int32_t* row_token; uint16_t* dW1;
   int d, n, E;
+  int32_t* klist; float* part;
 };
 hipError_t launch_dw1(const DW1Args& a, hipStream_t s);
 

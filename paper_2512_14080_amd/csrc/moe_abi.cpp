@@ -89,6 +89,9 @@ struct BwdWs {
   uint16_t* WrT;
   float* dWr_part;
   float* dbias_part;
+  int32_t* klist2;  // k-chunk lists of the weight gradients
+  int32_t* klist1;
+  float* dw_part;   // fp32 partials of row-chunked experts
 };
 
 size_t carve(char* base, size_t off, size_t bytes, void** out) {
@@ -118,6 +121,9 @@ size_t bwd_layout(const moe_dims& m, int64_t cap, char* base, BwdWs* w) {
   off = carve(base, off, (size_t)m.E * m.d * 2, w ? (void**)&w->WrT : nullptr);
   off = carve(base, off, (size_t)splits * m.d * m.E * 4, w ? (void**)&w->dWr_part : nullptr);
   off = carve(base, off, (size_t)smoe::colsum_chunks(m.T) * m.E * 4, w ? (void**)&w->dbias_part : nullptr);
+  off = carve(base, off, smoe::kchunks_bytes(m.E), w ? (void**)&w->klist2 : nullptr);
+  off = carve(base, off, smoe::kchunks_bytes(m.E), w ? (void**)&w->klist1 : nullptr);
+  off = carve(base, off, smoe::dw_part_bytes(m.d, m.n), w ? (void**)&w->dw_part : nullptr);
   return off;
 }
 
@@ -374,17 +380,17 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   hipStream_t stream = (hipStream_t)stream_;
   float* dS_out = dS ? dS : w.dS;
   const int nnt = smoe::dh_n_tiles(m.n);
-  HIP_TRY(smoe::launch_mtiles(r->offsets, m.E, w.mtiles, stream), "m-tile list");
+  HIP_TRY(smoe::launch_bwd_lists(r->offsets, m.E, m.d, m.n, w.mtiles, w.klist2, w.klist1, stream), "tile lists");
   LAUNCH(MOE_KC_DH,
          smoe::launch_dh({dO, W2, H, r->offsets, r->row_token, r->row_w, w.dH, w.Ap, dS_out, w.dS_part, m.d, m.n, m.E,
                           r->capacity, w.mtiles},
                          stream),
          "dH");
   if (nnt > 1) HIP_TRY(smoe::launch_reduce_rowparts(w.dS_part, dS_out, r->capacity, nnt, stream), "dS reduce");
-  LAUNCH(MOE_KC_DW2, smoe::launch_dw2({w.Ap, dO, r->offsets, r->row_token, dW2, m.d, m.n, m.E}, stream), "dW2");
+  LAUNCH(MOE_KC_DW2, smoe::launch_dw2({w.Ap, dO, r->offsets, r->row_token, dW2, m.d, m.n, m.E, w.klist2, w.dw_part}, stream), "dW2");
   LAUNCH(MOE_KC_DXT, smoe::launch_dxt({w.dH, W1, r->offsets, w.dXt, m.d, m.n, m.E, r->capacity, w.mtiles}, stream),
          "dX~");
-  LAUNCH(MOE_KC_DW1, smoe::launch_dw1({X, w.dH, r->offsets, r->row_token, dW1, m.d, m.n, m.E}, stream), "dW1");
+  LAUNCH(MOE_KC_DW1, smoe::launch_dw1({X, w.dH, r->offsets, r->row_token, dW1, m.d, m.n, m.E, w.klist1, w.dw_part}, stream), "dW1");
   if (Wr) HIP_TRY(smoe::launch_transpose_wr(Wr, w.WrT, m.d, m.E, stream), "W_r transpose");
   LAUNCH(MOE_KC_AGG_DX,
          smoe::launch_agg_dx(w.dXt, dS_out, Wr ? w.WrT : nullptr, *r, dX, Wr ? w.dL : nullptr, m.T, m.d, m.E, stream),

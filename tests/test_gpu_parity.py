@@ -148,6 +148,18 @@ def test_wave_per_token_topk_shapes():
     check_layer(W.MoEConfig("k10", T=300, d=128, n=64, E=16, K=10, m_tile=16), seed=14, round_mode="nearest")
 
 
+def test_weight_gradients_over_row_chunks():
+    """An expert that holds far more rows than the rest (every token picks it)
+    has its weight-gradient reductions cut into row chunks whose fp32 partials
+    are summed in chunk order; dW1 and dW2 still match the oracle."""
+    cfg = W.MoEConfig("hot", T=12000, d=256, n=128, E=16, K=2, m_tile=128)
+    bias = np.zeros(cfg.E, np.float32)
+    bias[3] = 60.0
+    layer, R = check_layer(cfg, seed=15, round_mode="nearest", bias=bias)
+    # the chunk length is at least 2048 rows: the hot expert is split
+    assert R.counts[3] > 2 * 2048
+
+
 def test_single_token_and_one_hot_expert():
     check_layer(TINY, seed=5, T=1)
     check_layer(TINY, seed=6, T=65, round_mode="nearest")
