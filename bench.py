@@ -143,23 +143,63 @@ def measured_traffic(kernel_class):
 
 
 def kernel_work(cls, cfg, P, T):
-    """Algorithmic work of one launch of a kernel class: (amount, unit, bound)."""
-    d, n, E = cfg.d, cfg.n, cfg.E
-    gemm = {
-        "up_proj": 2.0 * P * d * 2 * n, "down_proj": 2.0 * P * n * d, "dH": 2.0 * P * d * n,
-        "dW2": 2.0 * P * n * d, "dXtilde": 2.0 * P * 2 * n * d, "dW1": 2.0 * P * d * 2 * n,
-        "router_gemm": 2.0 * T * d * E, "dWr": 2.0 * T * d * E,
+    """Algorithmic work of one launch of a kernel class: (amount, unit, bound).
+
+    GEMMs count their FLOPs and their unique operand and result bytes (each tensor once; gathered rows counted
+    as the tensor they are gathered from) and are bound by whichever takes longer at peak: MFMA or HBM."""
+    d, n, E, K = cfg.d, cfg.n, cfg.E, cfg.K
+    gemm = {  # FLOPs, bytes
+        "up_proj": (2.0 * P * d * 2 * n, 2.0 * T * d + 2.0 * E * d * 2 * n + 2.0 * P * 2 * n + 2.0 * P * n),
+        "down_proj": (2.0 * P * n * d, 2.0 * P * n + 2.0 * E * n * d + 2.0 * P * d),
+        "dH": (2.0 * P * d * n, 2.0 * T * d + 2.0 * E * n * d + 2 * 2.0 * P * 2 * n + 2.0 * P * n + 4.0 * P),
+        "dW2": (2.0 * P * n * d, 2.0 * P * n + 2.0 * T * d + 2.0 * E * n * d),
+        "dXtilde": (2.0 * P * 2 * n * d, 2.0 * P * 2 * n + 2.0 * E * d * 2 * n + 2.0 * P * d),
+        "dW1": (2.0 * P * d * 2 * n, 2.0 * T * d + 2.0 * P * 2 * n + 2.0 * E * d * 2 * n),
+        "router_gemm": (2.0 * T * d * E, 2.0 * T * d + 2.0 * d * E + 4.0 * T * E),
+        "dWr": (2.0 * T * d * E, 2.0 * T * d + 2.0 * T * E + 4.0 * d * E),
     }
     if cls in gemm:
-        return gemm[cls], "TFLOP/s", "mfma"
+        f, b = gemm[cls]
+        if b / (PEAK_HBM_GBS * 1e9) > f / (PEAK_BF16_TFLOPS * 1e12):
+            return b, "GB/s", "hbm"
+        return f, "TFLOP/s", "mfma"
     hbm = {
         # read the P rows of Y (bf16) + weights/indices, write O
         "aggregate_O": 2.0 * P * d + 8.0 * P + 2.0 * T * d,
         "aggregate_dX": 2.0 * P * d + 12.0 * P + 2.0 * T * d + 2.0 * T * E,
+        # read the logits, write the scores (token-major and transposed), the
+        # top-K lists and the membership bitmap
+        "topk": 12.0 * T * E + 8.0 * T * K + T * E / 8.0,
     }
     if cls in hbm:
         return hbm[cls], "GB/s", "hbm"
     return None, None, None
+
+
+# the expert computation without router or routing (steps up-proj .. dX aggregation)
+MOE_ONLY_CLASSES = ("up_proj", "down_proj", "aggregate_O", "dH", "dW2", "dXtilde", "dW1", "aggregate_dX")
+
+
+def kernel_table(per, cfg, P):
+    """Achieved rate of every kernel class with an algorithmic work model, against its own peak."""
+    out = {}
+    for c, t in per.items():
+        work, unit, bound = kernel_work(c, cfg, P, cfg.T)
+        if work is None or t <= 0:
+            continue
+        if unit == "TFLOP/s":
+            a, peak = work / (t * 1e-3) / 1e12, PEAK_BF16_TFLOPS
+        else:
+            a, peak = work / (t * 1e-3) / 1e9, PEAK_HBM_GBS
+        out[c] = {"ms": round(t, 5), "bound": bound, "achieved": round(a, 1), "unit": unit,
+                  "frac": round(a / peak, 4)}
+    return out
+
+
+def padding_rows(layer):
+    """Rows that 128-row MFMA blocks compute beyond the routed ones: sum_e (ceil(f_e / 128) * 128 - f_e)."""
+    counts = layer.routing.arrays()["counts"].cpu().numpy().astype("int64")
+    return int(((counts + 127) // 128 * 128 - counts).sum())
 
 
 def cpu_baseline(cfg, round_mode, inp, budget_s=15.0):
@@ -310,6 +350,9 @@ def main():
                      "unit": unit, "frac": round(achieved / peak, 4), "traffic": measured_traffic(dominant),
                      "launch_ms": round(dom_avg, 5), "launches": dom_n},
         "kernel_ms": {c: round(t, 5) for c, t in per.items()},
+        "kernels": kernel_table(per, cfg, P),
+        "moe_only_ms": round(sum(per.get(c, 0.0) for c in MOE_ONLY_CLASSES), 4),
+        "padding_rows": padding_rows(layer),
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on a sample ...")
