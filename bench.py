@@ -241,47 +241,14 @@ def cpu_baseline(cfg, round_mode, inp, budget_s=15.0):
                       f"{T / dt:.1f} tokens/s"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default="7b")
-    ap.add_argument("--round", default="nearest", help="rounding mode, or 'none' for token-choice routing")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--breakdown", action="store_true", help="also time every kernel class")
-    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
-                    help="only run one plain device copy of BYTES (HBM counter calibration) and exit")
-    ap.add_argument("--traffic-report", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
-                                                          "COPY_WRITE_DIR", "COPY_BYTES"),
-                    help="print the HBM-traffic markdown summary from rocprofv3 counter runs and exit")
-    args = ap.parse_args()
-    if args.traffic_report:
-        fd, wd, cfd, cwd, nb = args.traffic_report
-        print(traffic_report(fd, wd, cfd, cwd, int(nb)))
-        return
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the layer is built and measured on a "
-              f"single MI355X; multi-GPU sharding is a design note, not part of this build.", file=sys.stderr)
-        sys.exit(2)
-
+def measure(args, cfg, cpu):
+    """One layer configuration: warm-up, per-kernel-class times, the timed steps; the JSON record."""
     import torch
-
-    if args.copy_calibration:
-        a = torch.ones(args.copy_calibration, dtype=torch.uint8, device="cuda")
-        b = torch.empty_like(a)
-        torch.cuda.synchronize()
-        b.copy_(a)
-        torch.cuda.synchronize()
-        log(f"[bench] copied {args.copy_calibration} bytes once")
-        return
 
     from paper_2512_14080_amd import binding as B
     from paper_2512_14080_amd import workloads as W
     from paper_2512_14080_amd.layer import DeviceLayer
 
-    B.lib()  # fail loudly if the library is missing
-    cfg = W.CONFIGS[args.config]
     round_mode = None if args.round == "none" else args.round
     log(f"[bench] config {cfg}, rounding {round_mode}")
     inp = W.make_inputs(cfg, 0)
@@ -354,9 +321,62 @@ def main():
         "moe_only_ms": round(sum(per.get(c, 0.0) for c in MOE_ONLY_CLASSES), 4),
         "padding_rows": padding_rows(layer),
     }
-    if not args.no_cpu_baseline:
+    if cpu:
         log("[bench] timing the CPU oracle on a sample ...")
         out["cpu_baseline"] = cpu_baseline(cfg, round_mode, inp)
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="7b")
+    ap.add_argument("--round", default="nearest", help="rounding mode, or 'none' for token-choice routing")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown", action="store_true", help="also time every kernel class")
+    ap.add_argument("--sweep", default=None,
+                    help="measure every layer of a named sweep (e.g. 'paper': the paper's benchmark shapes), "
+                         "one JSON line each, no CPU baseline")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run one plain device copy of BYTES (HBM counter calibration) and exit")
+    ap.add_argument("--traffic-report", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
+                                                          "COPY_WRITE_DIR", "COPY_BYTES"),
+                    help="print the HBM-traffic markdown summary from rocprofv3 counter runs and exit")
+    args = ap.parse_args()
+    if args.traffic_report:
+        fd, wd, cfd, cwd, nb = args.traffic_report
+        print(traffic_report(fd, wd, cfd, cwd, int(nb)))
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the layer is built and measured on a "
+              f"single MI355X; multi-GPU sharding is a design note, not part of this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_calibration:
+        a = torch.ones(args.copy_calibration, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"[bench] copied {args.copy_calibration} bytes once")
+        return
+
+    from paper_2512_14080_amd import binding as B
+    from paper_2512_14080_amd import workloads as W
+
+    B.lib()  # fail loudly if the library is missing
+    if args.sweep:
+        for name in W.SWEEPS[args.sweep]:
+            out = measure(args, W.CONFIGS[name], cpu=False)
+            print(json.dumps(out), flush=True)
+            log(f"[sweep] {name}: {out['ms_per_step']:.3f} ms/step, {out['value']:.1f} TFLOPS "
+                f"({out['pct_bf16_peak']:.1f}% of peak), MoE only {out['moe_only_ms']:.3f} ms")
+        return
+    out = measure(args, W.CONFIGS[args.config], cpu=not args.no_cpu_baseline)
     print(json.dumps(out), flush=True)
 
 

@@ -58,6 +58,20 @@ CONFIGS = {
     "coarse": MoEConfig("coarse", T=16384, d=4096, n=14336, E=8, K=2, m_tile=128),
 }
 
+# The paper's benchmark layers (Appendix G, the H100 table): four model sizes,
+# each at three granularities with equal FLOPs (n * K fixed).
+PAPER_SHAPES = [
+    ("1.4b", 40960, 768, [(256, 128, 8), (512, 64, 4), (1024, 32, 2)]),
+    ("7b", 24576, 1536, [(256, 128, 8), (512, 64, 4), (1024, 32, 2)]),
+    ("30b", 32768, 4096, [(256, 256, 16), (512, 128, 8), (1024, 64, 4)]),
+    ("120b", 32768, 4096, [(512, 256, 16), (1024, 128, 8), (2048, 64, 4)]),
+]
+for _size, _T, _d, _rows in PAPER_SHAPES:
+    for _n, _E, _K in _rows:
+        _name = f"paper-{_size}-e{_E}k{_K}"
+        CONFIGS[_name] = MoEConfig(_name, T=_T, d=_d, n=_n, E=_E, K=_K, m_tile=128)
+SWEEPS = {"paper": [k for k in CONFIGS if k.startswith("paper-")]}
+
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
     """Round finite fp32 values to bf16 (round-to-nearest-even) and return raw
