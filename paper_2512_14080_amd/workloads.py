@@ -70,7 +70,20 @@ for _size, _T, _d, _rows in PAPER_SHAPES:
     for _n, _E, _K in _rows:
         _name = f"paper-{_size}-e{_E}k{_K}"
         CONFIGS[_name] = MoEConfig(_name, T=_T, d=_d, n=_n, E=_E, K=_K, m_tile=128)
-SWEEPS = {"paper": [k for k in CONFIGS if k.startswith("paper-")]}
+# The paper's token-rounding speed sweeps (Appendix G): four (T, d, n, K)
+# families, each over a range of E, with M_tile = 128.
+TR_SWEEPS = [
+    (16384, 1536, 256, 8, [64, 128, 256, 512]),
+    (16384, 1536, 1024, 2, [16, 32, 64, 128]),
+    (16384, 4096, 512, 8, [64, 128, 256, 512]),
+    (16384, 4096, 1024, 4, [32, 64, 128, 256]),
+]
+for _T, _d, _n, _K, _Es in TR_SWEEPS:
+    for _E in _Es:
+        _name = f"tr-d{_d}n{_n}k{_K}-e{_E}"
+        CONFIGS[_name] = MoEConfig(_name, T=_T, d=_d, n=_n, E=_E, K=_K, m_tile=128)
+SWEEPS = {"paper": [k for k in CONFIGS if k.startswith("paper-")],
+          "tr": [k for k in CONFIGS if k.startswith("tr-")]}
 
 
 def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
