@@ -142,23 +142,26 @@ hipError_t launch_mtiles(const int32_t* offsets, int E, int32_t* out, hipStream_
 // more than Kc rows into Kc-row chunks (Kc = max(kKcMin, 2P / slabs), so the
 // chunks need at most `slabs` fp32 partial slabs); a split expert's chunks
 // write fp32 partials that dw_reduce_kernel sums in chunk order, the others
-// store bf16 directly.  Entries: split chunks first (the long ones), then
-// the unsplit experts in expert order.  The tiles (entry-major) are cut into
-// 8 contiguous ranges, one per XCD: of equal work when some expert is split
-// (work of a tile: its k steps plus a fixed cost for the prologue and
-// epilogue), else of equal count, as for the other GEMMs.
+// store bf16 directly.  The entries (chunks and unsplit experts) are sorted
+// by length, longest first (a counting sort on k steps), and dealt round-robin
+// to the 8 XCDs; each XCD's entries are contiguous in the list, so its 32
+// workgroups take its tiles (entry-major, longest first) round-robin.  Which
+// CU computes a tile does not change any value.
 // Layout (int32): header[16] = {entries, split experts, Kc, tiles,
-// xcd_start[0..8]}; entries at 16 (int4 {e, k_begin, k_len, slot or -1});
-// split experts at 16 + 4 * (E + kDwSlabs) (int4 {e, first slot, chunks, 0}).
+// xcd_start[0..8] (tiles)}; entries at 16 (int4 {e, k_begin, k_len, slot or
+// -1}); unsorted entries at 16 + 4 (E + kDwSlabs); split experts at
+// 16 + 8 (E + kDwSlabs) (int4 {e, first slot, chunks, 0}).
 constexpr int kKcMin = 2048;
-constexpr int kTileFixedSteps = 4;  // prologue + epilogue, in k steps of 64
 constexpr int kKChunksThreads = 1024;
+constexpr int kLenBins = 1024;  // counting-sort bins: k steps of 64 rows, the last bin open-ended
 
-size_t kchunks_bytes(int E) { return 4 * (16 + 4 * (size_t)(E + kDwSlabs) + 4 * (kDwSlabs / 2 + 1)); }
+size_t kchunks_bytes(int E) { return 4 * (16 + 8 * (size_t)(E + kDwSlabs) + 4 * (kDwSlabs / 2 + 1)); }
+__host__ __device__ inline int kchunks_split_off(int E) { return 16 + 8 * (E + kDwSlabs); }
 
-// wpre: LDS [4096 + kDwSlabs + 1] (work prefix over entries)
+// bins: LDS [kLenBins]
 __device__ __forceinline__ void kchunks_body(const int32_t* __restrict__ offsets, int E, int tpe, int slabs,
-                                             int32_t* __restrict__ out, int* wpre, int* scan_lds, int* sh_kc) {
+                                             int32_t* __restrict__ out, int* bins, int* scan_lds, int* sh_kc) {
+  static_assert(kLenBins == kKChunksThreads, "one bin per thread");
   const int tid = threadIdx.x;
   if (tid == 0) {
     const int P = offsets[E];
@@ -169,6 +172,7 @@ __device__ __forceinline__ void kchunks_body(const int32_t* __restrict__ offsets
     }
     *sh_kc = kc;
   }
+  bins[tid] = 0;
   __syncthreads();
   const int Kc = *sh_kc;
   // thread t owns experts 4t .. 4t+3 (E <= 4096)
@@ -187,7 +191,9 @@ __device__ __forceinline__ void kchunks_body(const int32_t* __restrict__ offsets
   int bu = block_excl_scan<kKChunksThreads>(su, &U, scan_lds);
   int bx = block_excl_scan<kKChunksThreads>(sx, &X, scan_lds);
   i32x4* ent = (i32x4*)(out + 16);
-  i32x4* spl = (i32x4*)(out + 16 + 4 * (E + kDwSlabs));
+  i32x4* raw = (i32x4*)(out + 16 + 4 * (E + kDwSlabs));
+  i32x4* spl = (i32x4*)(out + kchunks_split_off(E));
+  auto bin_of = [](int k_len) { return min(kLenBins - 1, (k_len + 63) / 64); };
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int e = 4 * tid + q;
@@ -195,65 +201,45 @@ __device__ __forceinline__ void kchunks_body(const int32_t* __restrict__ offsets
     const int k0 = offsets[e];
     if (nc[q] > 0) {
       for (int c = 0; c < nc[q]; ++c) {
-        const int kb = c * Kc;
-        ent[bc + c] = i32x4{e, k0 + kb, min(Kc, f[q] - kb), bc + c};  // slot = chunk position
+        const int kb = c * Kc, kl = min(Kc, f[q] - kb);
+        raw[bc + c] = i32x4{e, k0 + kb, kl, bc + c};  // slot = chunk position
+        atomicAdd(&bins[bin_of(kl)], 1);
       }
       spl[bx] = i32x4{e, bc, nc[q], 0};
       bc += nc[q];
       ++bx;
     } else {
-      ent[S + bu] = i32x4{e, k0, f[q], -1};
+      raw[S + bu] = i32x4{e, k0, f[q], -1};
+      atomicAdd(&bins[bin_of(f[q])], 1);
       ++bu;
     }
   }
   const int N = S + U;
-  __syncthreads();  // entries written (read back below by other threads)
-  // work prefix over entries: up to 5 entries per thread (E + slabs <= 4160)
-  int w[5], sw = 0;
-#pragma unroll
-  for (int q = 0; q < 5; ++q) {
-    const int i = 5 * tid + q;
-    w[q] = i < N ? tpe * ((ent[i][2] + 63) / 64 + kTileFixedSteps) : 0;
-    sw += w[q];
-  }
-  int Wt;
-  int bw = block_excl_scan<kKChunksThreads>(sw, &Wt, scan_lds);
-#pragma unroll
-  for (int q = 0; q < 5; ++q) {
-    const int i = 5 * tid + q;
-    if (i < N) wpre[i] = bw;
-    bw += w[q];
-  }
-  if (tid == 0) wpre[N] = Wt;
+  __syncthreads();  // raw entries and bin counts complete
+  // first sorted position of each bin, longest bins first (thread t: bin kLenBins-1-t)
+  const int b = kLenBins - 1 - tid;
+  int total;
+  const int first = block_excl_scan<kKChunksThreads>(bins[b], &total, scan_lds);
+  bins[b] = first;  // from here on: the bin's next free position
   __syncthreads();
+  // sorted position s -> XCD s % 8, place s / 8 within that XCD's contiguous range
+  auto xcd_base = [N](int x) {  // entries of the XCDs before x
+    int base = 0;
+    for (int y = 0; y < x; ++y) base += (N + 7 - y) / 8;
+    return base;
+  };
+  for (int i = tid; i < N; i += kKChunksThreads) {
+    const i32x4 r = raw[i];
+    const int s2 = atomicAdd(&bins[bin_of(r[2])], 1);
+    ent[xcd_base(s2 % 8) + s2 / 8] = r;
+  }
   if (tid == 0) {
     out[0] = N;
     out[1] = X;
     out[2] = Kc;
     out[3] = N * tpe;
-    out[4] = 0;
-    out[12] = N * tpe;
   }
-  if (tid >= 1 && tid < 8 && X == 0) {
-    // nothing split: equal tile counts (tiles of like length, so no XCD and no
-    // workgroup gets an extra round)
-    out[4 + tid] = min(N * tpe, tid * ((N * tpe + 7) / 8));
-  } else if (tid >= 1 && tid < 8) {
-    // first tile whose work starts at or after tid / 8 of the total
-    const int target = (int)((int64_t)Wt * tid / 8);
-    int lo = 0, hi = N;  // wpre[lo] <= target < wpre[hi]
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (wpre[mid] <= target) lo = mid; else hi = mid;
-    }
-    int start = N * tpe;
-    if (N > 0) {
-      const int wt = (wpre[lo + 1] - wpre[lo]) / tpe;  // work of one tile of entry lo
-      const int j = wt > 0 ? min(tpe, (target - wpre[lo] + wt - 1) / wt) : 0;
-      start = lo * tpe + j;
-    }
-    out[4 + tid] = start;
-  }
+  if (tid <= 8) out[4 + tid] = xcd_base(tid) * tpe;
 }
 
 // The backward's tile lists in one launch: workgroup 0 the m-tile list,
@@ -280,7 +266,7 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const int32_t* __restric
   const SMOE_CONST int32_t* h = (const SMOE_CONST int32_t*)klist;
   const int si = blockIdx.y;
   if (si >= h[1]) return;
-  const SMOE_CONST i32x4* spl = (const SMOE_CONST i32x4*)(klist + 16 + 4 * (E + kDwSlabs));
+  const SMOE_CONST i32x4* spl = (const SMOE_CONST i32x4*)(klist + kchunks_split_off(E));
   const i32x4 sp = spl[si];
   const int e = sp[0], first = sp[1], nc = sp[2];
   for (int64_t i = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x); i < MN; i += 4 * (int64_t)gridDim.x * 256) {

@@ -57,7 +57,7 @@ hipError_t launch_dxt(const DXtArgs& a, hipStream_t s);
 // k-chunk list (kchunks_bytes(E) bytes, written by launch_bwd_lists); part:
 // dw_part_bytes(d, n) bytes of fp32 partials for experts split into row
 // chunks.
-constexpr int kDwSlabs = 64;                                 // partial slabs per GEMM at most
+constexpr int kDwSlabs = 128;                                // partial slabs per GEMM at most
 constexpr int64_t kDwSlabBytes = (int64_t)256 << 20;         // and at most this many bytes
 size_t kchunks_bytes(int E);
 size_t dw_part_bytes(int d, int n);
