@@ -98,16 +98,15 @@ def traffic_report(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_by
         "Commands (repository root, one MI355X; each counter in a run of its own):",
         "",
         "```",
-        "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- "
+        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- "
         "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
-        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- "
+        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- "
         "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
-        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/copy_fetch -o run -- "
+        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {copy_fetch_dir} -o run -- "
         f"python3 bench.py --copy-calibration {copy_bytes}",
-        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/copy_write -o run -- "
+        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {copy_write_dir} -o run -- "
         f"python3 bench.py --copy-calibration {copy_bytes}",
-        "python3 bench.py --traffic-report gpurun_out/pmc_fetch gpurun_out/pmc_write gpurun_out/copy_fetch "
-        f"gpurun_out/copy_write {copy_bytes}",
+        f"python3 bench.py --traffic-report {fetch_dir} {write_dir} {copy_fetch_dir} {copy_write_dir} {copy_bytes}",
         "```",
         "",
         f"Calibration: a device copy of {copy_bytes} bytes reads FETCH_SIZE = {cf[ck[0]]:.1f} KiB and "

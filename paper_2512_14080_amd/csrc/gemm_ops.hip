@@ -571,6 +571,64 @@ __device__ __forceinline__ void store_rows64_staged(char* wl, uint16_t* blk, int
   }
 }
 
+// Two-step form of the staging above for 32 rows at once, used where an
+// output's two 32-column blocks are produced one after the other: each block
+// is written into a wave-private 4 KB area as soon as it is computed (chunk
+// 4 * jj + g + hi of row r, same swizzle), and the 32 rows are then stored as
+// whole lines.  The area must not be touched by other waves in between.
+__device__ __forceinline__ void stage_block32(char* wl, int jj, const u32x2 (&v)[4]) {
+  const int lane = epilogue_lane();
+  const int r = lane & 31, hi = lane >> 5;
+#pragma unroll
+  for (int g = 0; g < 4; g += 2) {
+    const auto a = __builtin_amdgcn_permlane32_swap(v[g][0], v[g + 1][0], false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(v[g][1], v[g + 1][1], false, false);
+    const int ch = 4 * jj + g + hi;
+    *(u32x4*)(wl + r * 128 + ((ch ^ ((r >> 1) & 7)) << 4)) = u32x4{a[0], b[0], a[1], b[1]};
+  }
+}
+
+__device__ __forceinline__ void store_staged32(const char* wl, uint16_t* blk, int64_t ld, int rows_valid) {
+  asm volatile("" ::: "memory");  // the staged writes of every lane precede these reads
+  const int lane = epilogue_lane();
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int R = 8 * t + (lane >> 3), C = lane & 7;
+    const u32x4 x = *(const u32x4*)(wl + R * 128 + ((C ^ ((R >> 1) & 7)) << 4));
+    if (R < rows_valid) __builtin_nontemporal_store(x, (u32x4*)(blk + (R * (int)ld + 8 * C)));
+  }
+  asm volatile("" ::: "memory");  // and precede the next writes to the area
+}
+
+// The same for an output whose first block is held in a 2 KB half-row area
+// (32 rows x 64 bytes, chunk c of row r at r * 64 + ((c ^ ((r >> 1) & 3)) <<
+// 4)) and whose second block is in chunks 4..7 of a 4 KB area as above.
+__device__ __forceinline__ void stage_half32(char* wh, const u32x2 (&v)[4]) {
+  const int lane = epilogue_lane();
+  const int r = lane & 31, hi = lane >> 5;
+#pragma unroll
+  for (int g = 0; g < 4; g += 2) {
+    const auto a = __builtin_amdgcn_permlane32_swap(v[g][0], v[g + 1][0], false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(v[g][1], v[g + 1][1], false, false);
+    const int ch = g + hi;
+    *(u32x4*)(wh + r * 64 + ((ch ^ ((r >> 1) & 3)) << 4)) = u32x4{a[0], b[0], a[1], b[1]};
+  }
+}
+
+__device__ __forceinline__ void store_staged32_split(const char* wh, const char* wl, uint16_t* blk, int64_t ld,
+                                                     int rows_valid) {
+  asm volatile("" ::: "memory");
+  const int lane = epilogue_lane();
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int R = 8 * t + (lane >> 3), C = lane & 7;
+    const char* src = C < 4 ? wh + R * 64 + ((C ^ ((R >> 1) & 3)) << 4) : wl + R * 128 + ((C ^ ((R >> 1) & 7)) << 4);
+    const u32x4 x = *(const u32x4*)src;
+    if (R < rows_valid) __builtin_nontemporal_store(x, (u32x4*)(blk + (R * (int)ld + 8 * C)));
+  }
+  asm volatile("" ::: "memory");
+}
+
 template <class Cfg>
 __device__ __forceinline__ void store_rows_bf16(uint16_t* out, int64_t ld, int row_base, int mrows, int n0,
                                                 Acc<Cfg>& t, char* epi) {
@@ -650,10 +708,16 @@ struct OpDH {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = ROWS;
   struct Params { DHArgs a; };
-  static constexpr int EPI_LDS = Cfg::BM * Cfg::WN * 4;  // dS partial sums [BM][WN]
+  static constexpr int RED_LDS = Cfg::BM * Cfg::WN * 4;  // dS partial sums [BM][WN]
   static constexpr int IDX_LDS = Cfg::NW * Cfg::QM * 256;  // gathered dO rows of the next tile
-  // full tile: per 32 x 32 block, dH gate, dH up and A', two stores each
-  static constexpr int EPI_STORES = Cfg::RM * Cfg::RN * 6;
+  // dH gate, dH up and A' leave as whole 128-byte lines through
+  // wave-private LDS staging where the LDS allows it
+  static constexpr bool STAGED = Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 8192 &&
+                                 Cfg::LDS_BYTES + RED_LDS + Cfg::NW * kStageBytesPerWave + IDX_LDS <= 160 * 1024;
+  static constexpr int EPI_LDS = RED_LDS + (STAGED ? Cfg::NW * kStageBytesPerWave : 0);
+  // full tile: staged, four stores per output and 64-column row block;
+  // direct, two per output and 32 x 32 block
+  static constexpr int EPI_STORES = STAGED ? Cfg::RM * (Cfg::RN / 2) * 12 : Cfg::RM * Cfg::RN * 6;
   static __device__ int count(const Params& p, int* sh) {
     return count_varlen_m<Cfg::BN>(p.a.mtiles, p.a.n);
   }
@@ -710,7 +774,52 @@ struct OpDH {
       const size_t row = (size_t)(ti.row_base + (valid ? m : 0));
       const float s = swr[i];
       if (j == 0) part = 0.f;
-      if (valid) {
+      if constexpr (STAGED) {
+        // dH gate and up of block j go to the wave's 8 KB of the last stage
+        // buffer at once (no DMA writes it before the next tile's first
+        // barrier); A' of the even block waits in the wave's 2 KB of the
+        // epilogue area, the odd one in the gate area once that is stored.
+        const int m0 = wm0 + 32 * i;
+        if (m0 < ti.mrows) {
+          u32x2 vg[4], vu[4], va[4];
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const float gv[4] = {bf_lo(hg[b][g][0]), bf_hi(hg[b][g][0]), bf_lo(hg[b][g][1]), bf_hi(hg[b][g][1])};
+            const float uv[4] = {bf_lo(hu[b][g][0]), bf_hi(hu[b][g][0]), bf_lo(hu[b][g][1]), bf_hi(hu[b][g][1])};
+            float dg[4], du[4], apv[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float dap = t.acc[i][j][4 * g + r];
+              float sg;
+              const float sl = silu_sig(gv[r], &sg);
+              const float av = sl * uv[r];
+              part += dap * av;
+              const float da = s * dap;
+              dg[r] = da * uv[r] * sg * (1.f + gv[r] * (1.f - sg));
+              du[r] = da * sl;
+              apv[r] = s * av;
+            }
+            vg[g] = pack_bf16x4(dg[0], dg[1], dg[2], dg[3]);
+            vu[g] = pack_bf16x4(du[0], du[1], du[2], du[3]);
+            va[g] = pack_bf16x4(apv[0], apv[1], apv[2], apv[3]);
+          }
+          char* st = smem - Cfg::STAGE_BYTES + (threadIdx.x >> 6) * 8192;
+          char* wh = smem + RED_LDS + (threadIdx.x >> 6) * kStageBytesPerWave;
+          stage_block32(st, j % 2, vg);
+          stage_block32(st + 4096, j % 2, vu);
+          if (j % 2 == 0) {
+            stage_half32(wh, va);
+          } else {
+            const size_t r0 = (size_t)(ti.row_base + m0);
+            const int col = col_of(j - 1), rv = ti.mrows - m0;
+            store_staged32(st, p.a.dH + r0 * (2 * n) + col, 2 * n, rv);
+            store_staged32(st + 4096, p.a.dH + r0 * (2 * n) + n + col, 2 * n, rv);
+            // the gate area is free again: A' of this block joins the even one
+            stage_block32(st, 1, va);
+            store_staged32_split(wh, st, p.a.Ap + r0 * n + col, n, rv);
+          }
+        }
+      } else if (valid) {
         uint16_t* dh = p.a.dH + row * (2 * n);
         uint16_t* ap = p.a.Ap + row * n;
         const int col = col_of(j);
