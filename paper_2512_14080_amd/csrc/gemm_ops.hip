@@ -426,83 +426,6 @@ struct OpRouter {
   }
 };
 
-// ================================================================== up-proj
-// N tile: BN/2 gate columns starting at j0 = nt * BN/2 and the matching up
-// columns.  Wave column group wn owns Wn = BN/WN tile columns: its first
-// Wn/2 are gate columns j0 + wn*Wn/2 + [0, Wn/2) (accumulator blocks
-// j < RN/2) and its last Wn/2 the matching up columns (blocks j >= RN/2).
-template <class Cfg_>
-struct OpUp {
-  using Cfg = Cfg_;
-  static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
-  static constexpr int Wn = Cfg::BN / Cfg::WN;
-  static_assert(Cfg::RN % 2 == 0, "gate and up blocks in one wave");
-  struct Params { UpArgs a; };
-  struct ColMap {
-    int j0, n;
-    __device__ __forceinline__ int operator()(int c) const {
-      const int wn = c / Wn, q = c % Wn;
-      return q < Wn / 2 ? j0 + wn * (Wn / 2) + q : n + j0 + wn * (Wn / 2) + (q - Wn / 2);
-    }
-  };
-  static constexpr int EPI_LDS = 0;
-  static constexpr int IDX_LDS = Cfg::NW * Cfg::QM * 256;  // gathered X rows of the next tile
-  // full tile: per row block, H gate, H up and A, two stores each
-  static constexpr int EPI_STORES = Cfg::RM * (Cfg::RN / 2) * 6;
-  static __device__ int count(const Params& p, int* sh) {
-    return count_varlen_m<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
-  }
-  static __device__ int count_tail(const Params& p, const int* sh) {
-    return count_varlen_m_tail<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
-  }
-  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
-    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, 2 * p.a.n, p.a.d, id, ti);
-  }
-  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW, true>& s) {
-    s.init(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
-  }
-  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
-    const uint16_t* w = p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n);
-    s.init(w, 2 * p.a.n, nullptr, 0, p.a.d, 2 * p.a.n, ColMap{(ti.n0 / Cfg::BN) * (Cfg::BN / 2), p.a.n});
-  }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char*) {
-    constexpr int RN = Cfg::RN;
-    const int n = p.a.n;
-    const int j0 = (ti.n0 / Cfg::BN) * (Cfg::BN / 2);
-    const int wn = t.wave_n();
-#pragma unroll
-    for (int i = 0; i < Cfg::RM; ++i) {
-      const int m = t.m_of(i);
-      if (m >= ti.mrows) continue;
-      const size_t row = (size_t)(ti.row_base + m);
-      uint16_t* h = p.a.H + row * (2 * n);
-      uint16_t* a = p.a.A + row * n;
-#pragma unroll
-      for (int j = 0; j < RN / 2; ++j) {
-        const int col = j0 + wn * (Wn / 2) + 32 * j;  // first column of the 32-column block
-        u32x2 hg[4], hu[4], ha[4];
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          float gv[4], uv[4], av[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            gv[r] = t.acc[i][j][4 * g + r];
-            uv[r] = t.acc[i][j + RN / 2][4 * g + r];
-            float sg;
-            av[r] = silu_sig(gv[r], &sg) * uv[r];
-          }
-          hg[g] = pack_bf16x4(gv[0], gv[1], gv[2], gv[3]);
-          hu[g] = pack_bf16x4(uv[0], uv[1], uv[2], uv[3]);
-          ha[g] = pack_bf16x4(av[0], av[1], av[2], av[3]);
-        }
-        store_block_bf16(h + col, hg);
-        store_block_bf16(h + n + col, hu);
-        store_block_bf16(a + col, ha);
-      }
-    }
-  }
-};
-
 // Row-contiguous stores of a wave's output: the two 32-column accumulator
 // blocks j, j+1 of one 32-row block (64 columns, 128 bytes of a bf16 row) go
 // through the wave's own 2 KB of LDS, 16 rows at a time, and come back so
@@ -669,6 +592,125 @@ __device__ __forceinline__ void store_rows_bf16(uint16_t* out, int64_t ld, int r
     }
   }
 }
+
+// ================================================================== up-proj
+// N tile: BN/2 gate columns starting at j0 = nt * BN/2 and the matching up
+// columns.  Wave column group wn owns Wn = BN/WN tile columns: its first
+// Wn/2 are gate columns j0 + wn*Wn/2 + [0, Wn/2) (accumulator blocks
+// j < RN/2) and its last Wn/2 the matching up columns (blocks j >= RN/2).
+
+template <class Cfg_>
+struct OpUp {
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
+  static constexpr int Wn = Cfg::BN / Cfg::WN;
+  static_assert(Cfg::RN % 2 == 0, "gate and up blocks in one wave");
+  struct Params { UpArgs a; };
+  struct ColMap {
+    int j0, n;
+    __device__ __forceinline__ int operator()(int c) const {
+      const int wn = c / Wn, q = c % Wn;
+      return q < Wn / 2 ? j0 + wn * (Wn / 2) + q : n + j0 + wn * (Wn / 2) + (q - Wn / 2);
+    }
+  };
+  static constexpr int IDX_LDS = Cfg::NW * Cfg::QM * 256;  // gathered X rows of the next tile
+  // with 64 gate and 64 up columns per wave, H and A leave as whole 128-byte
+  // lines through store_rows64_staged
+  static constexpr bool STAGED =
+      Cfg::RN % 4 == 0 && Cfg::LDS_BYTES + Cfg::NW * kStageBytesPerWave + IDX_LDS <= 160 * 1024;
+  static constexpr int EPI_LDS = STAGED ? Cfg::NW * kStageBytesPerWave : 0;
+  // full tile: staged, per row block and 64-column pair, H gate, H up and A,
+  // four stores each; direct, per 32-column block, two stores each
+  static constexpr int EPI_STORES = STAGED ? Cfg::RM * (Cfg::RN / 4) * 12 : Cfg::RM * (Cfg::RN / 2) * 6;
+  static __device__ int count(const Params& p, int* sh) {
+    return count_varlen_m<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
+  }
+  static __device__ int count_tail(const Params& p, const int* sh) {
+    return count_varlen_m_tail<Cfg::BN>(p.a.mtiles, 2 * p.a.n);
+  }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int* sh) {
+    return tile_varlen_m<Cfg::BM, Cfg::BN>(p.a.mtiles, 2 * p.a.n, p.a.d, id, ti);
+  }
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<Cfg::BM, Cfg::BK, Cfg::NW, true>& s) {
+    s.init(p.a.X, p.a.d, p.a.row_token, ti.row_base, ti.mrows);
+  }
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<Cfg::BN, Cfg::BK, Cfg::NW>& s) {
+    const uint16_t* w = p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n);
+    s.init(w, 2 * p.a.n, nullptr, 0, p.a.d, 2 * p.a.n, ColMap{(ti.n0 / Cfg::BN) * (Cfg::BN / 2), p.a.n});
+  }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
+    constexpr int RN = Cfg::RN;
+    const int n = p.a.n;
+    const int j0 = (ti.n0 / Cfg::BN) * (Cfg::BN / 2);
+    const int wn = t.wave_n();
+    if constexpr (STAGED) {
+      char* wl = epi + (threadIdx.x >> 6) * kStageBytesPerWave;
+      const int wm0 = t.m_of(0) - (threadIdx.x & 31);
+#pragma unroll
+      for (int i = 0; i < Cfg::RM; ++i) {
+        const int m0 = wm0 + 32 * i;
+        if (m0 >= ti.mrows) continue;
+        const size_t r0 = (size_t)(ti.row_base + m0);
+#pragma unroll
+        for (int j = 0; j < RN / 2; j += 2) {
+          const int col = j0 + wn * (Wn / 2) + 32 * j;  // first column of the 64-column pair
+          u32x2 hg[2][4], hu[2][4], ha[2][4];
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+              float gv[4], uv[4], av[4];
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                gv[r] = t.acc[i][j + q][4 * g + r];
+                uv[r] = t.acc[i][j + q + RN / 2][4 * g + r];
+                float sg;
+                av[r] = silu_sig(gv[r], &sg) * uv[r];
+              }
+              hg[q][g] = pack_bf16x4(gv[0], gv[1], gv[2], gv[3]);
+              hu[q][g] = pack_bf16x4(uv[0], uv[1], uv[2], uv[3]);
+              ha[q][g] = pack_bf16x4(av[0], av[1], av[2], av[3]);
+            }
+          const int rv = ti.mrows - m0;
+          store_rows64_staged(wl, p.a.H + r0 * (2 * n) + col, 2 * n, rv, hg[0], hg[1]);
+          store_rows64_staged(wl, p.a.H + r0 * (2 * n) + n + col, 2 * n, rv, hu[0], hu[1]);
+          store_rows64_staged(wl, p.a.A + r0 * n + col, n, rv, ha[0], ha[1]);
+        }
+      }
+      return;
+    }
+#pragma unroll
+    for (int i = 0; i < Cfg::RM; ++i) {
+      const int m = t.m_of(i);
+      if (m >= ti.mrows) continue;
+      const size_t row = (size_t)(ti.row_base + m);
+      uint16_t* h = p.a.H + row * (2 * n);
+      uint16_t* a = p.a.A + row * n;
+#pragma unroll
+      for (int j = 0; j < RN / 2; ++j) {
+        const int col = j0 + wn * (Wn / 2) + 32 * j;  // first column of the 32-column block
+        u32x2 hg[4], hu[4], ha[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float gv[4], uv[4], av[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            gv[r] = t.acc[i][j][4 * g + r];
+            uv[r] = t.acc[i][j + RN / 2][4 * g + r];
+            float sg;
+            av[r] = silu_sig(gv[r], &sg) * uv[r];
+          }
+          hg[g] = pack_bf16x4(gv[0], gv[1], gv[2], gv[3]);
+          hu[g] = pack_bf16x4(uv[0], uv[1], uv[2], uv[3]);
+          ha[g] = pack_bf16x4(av[0], av[1], av[2], av[3]);
+        }
+        store_block_bf16(h + col, hg);
+        store_block_bf16(h + n + col, hu);
+        store_block_bf16(a + col, ha);
+      }
+    }
+  }
+};
 
 // ================================================================== down-proj
 template <class Cfg_>
@@ -1036,6 +1078,7 @@ static int mtiles_bound(int capacity, int E, int BM) { return capacity / BM + E;
 
 // tile configurations <BM, BN, WM, WN, STAGES>; varlen-M GEMMs use BM = 256
 using C256x256 = GemmCfg<256, 256, 2, 4, 2>;
+using C256x256w = GemmCfg<256, 256, 4, 2, 2>;  // 64 x 128 per wave
 using C256x128 = GemmCfg<256, 128, 4, 2, 3>;
 using C256x64 = GemmCfg<256, 64, 8, 1, 3>;
 using C128x256 = GemmCfg<128, 256, 2, 4, 3>;
@@ -1053,7 +1096,7 @@ hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
 
 hipError_t launch_up(const UpArgs& a, hipStream_t s) {
   const int N = 2 * a.n;
-  if (a.n % 128 == 0) return run<OpUp<C256x256>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (N / 256)), s);
+  if (a.n % 128 == 0) return run<OpUp<C256x256w>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (N / 256)), s);
   return run<OpUp<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (N / 128)), s);  // n % 64
 }
 
