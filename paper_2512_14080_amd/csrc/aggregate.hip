@@ -12,7 +12,7 @@
 namespace smoe {
 
 constexpr int kAggBatch = 8;  // rows whose loads are in flight together
-constexpr int kColRows = 128;  // tokens per chunk of the dbias column sum
+constexpr int kColRows = 32;  // tokens per chunk of the dbias column sum
 constexpr int kDLPerLane = 4;  // router-gradient row entries per lane collected in registers (E <= 256)
 static_assert(kAggBatch == 8, "lane & 7 picks a batch slot");
 

@@ -264,21 +264,21 @@ __global__ __launch_bounds__(kMTilesThreads) void bwd_lists_kernel(const int32_t
 __global__ __launch_bounds__(256) void dw_reduce_kernel(const int32_t* __restrict__ klist, const float* __restrict__ part,
                                                         uint16_t* __restrict__ dW, int E, int64_t MN) {
   const SMOE_CONST int32_t* h = (const SMOE_CONST int32_t*)klist;
-  const int si = blockIdx.y;
-  if (si >= h[1]) return;
   const SMOE_CONST i32x4* spl = (const SMOE_CONST i32x4*)(klist + kchunks_split_off(E));
-  const i32x4 sp = spl[si];
-  const int e = sp[0], first = sp[1], nc = sp[2];
-  for (int64_t i = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x); i < MN; i += 4 * (int64_t)gridDim.x * 256) {
-    f32x4 a = *(const f32x4*)(part + (size_t)first * MN + i);
-    for (int c = 1; c < nc; ++c) {
-      const f32x4 b = *(const f32x4*)(part + (size_t)(first + c) * MN + i);
-      a[0] += b[0];
-      a[1] += b[1];
-      a[2] += b[2];
-      a[3] += b[3];
+  for (int si = blockIdx.y; si < h[1]; si += gridDim.y) {
+    const i32x4 sp = spl[si];
+    const int e = sp[0], first = sp[1], nc = sp[2];
+    for (int64_t i = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x); i < MN; i += 4 * (int64_t)gridDim.x * 256) {
+      f32x4 a = *(const f32x4*)(part + (size_t)first * MN + i);
+      for (int c = 1; c < nc; ++c) {
+        const f32x4 b = *(const f32x4*)(part + (size_t)(first + c) * MN + i);
+        a[0] += b[0];
+        a[1] += b[1];
+        a[2] += b[2];
+        a[3] += b[3];
+      }
+      *(u32x2*)(dW + (size_t)e * MN + i) = u32x2{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3])};
     }
-    *(u32x2*)(dW + (size_t)e * MN + i) = u32x2{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3])};
   }
 }
 
@@ -286,7 +286,9 @@ hipError_t launch_dw_reduce(const int32_t* klist, const float* part, uint16_t* d
                             hipStream_t s) {
   if (slabs <= 0) return hipSuccess;
   const int gx = (int)std::min<int64_t>((MN / 4 + 255) / 256, 64);
-  dw_reduce_kernel<<<dim3(gx, slabs / 2), dim3(256), 0, s>>>(klist, part, dW, E, MN);
+  // split experts are looped over: most calls have none, and a grid sized for
+  // every possible one would mostly launch workgroups that exit at once
+  dw_reduce_kernel<<<dim3(gx, std::min(slabs / 2, 8)), dim3(256), 0, s>>>(klist, part, dW, E, MN);
   return hipGetLastError();
 }
 
@@ -1078,7 +1080,7 @@ static int mtiles_bound(int capacity, int E, int BM) { return capacity / BM + E;
 
 // tile configurations <BM, BN, WM, WN, STAGES>; varlen-M GEMMs use BM = 256
 using C256x256 = GemmCfg<256, 256, 2, 4, 2>;
-using C256x256w = GemmCfg<256, 256, 4, 2, 2>;  // 64 x 128 per wave
+using C256x256w = GemmCfg<256, 256, 4, 2, 2>;  // 64 x 128 per wave (up, dH, dX~: measured faster)
 using C256x128 = GemmCfg<256, 128, 4, 2, 3>;
 using C256x64 = GemmCfg<256, 64, 8, 1, 3>;
 using C128x256 = GemmCfg<128, 256, 2, 4, 3>;
@@ -1111,14 +1113,14 @@ int dh_n_tiles(int n) { return n / dh_bn(n); }
 hipError_t launch_dh(const DHArgs& a, hipStream_t s) {
   const int grid = pad8(mtiles_bound(a.capacity, a.E, 256) * dh_n_tiles(a.n));
   switch (dh_bn(a.n)) {
-    case 256: return run<OpDH<C256x256>>({a}, grid, s);
+    case 256: return run<OpDH<C256x256w>>({a}, grid, s);
     case 128: return run<OpDH<C256x128>>({a}, grid, s);
     default: return run<OpDH<C256x64>>({a}, grid, s);
   }
 }
 
 hipError_t launch_dxt(const DXtArgs& a, hipStream_t s) {
-  if (a.d % 256 == 0) return run<OpDXt<C256x256>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
+  if (a.d % 256 == 0) return run<OpDXt<C256x256w>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
   return run<OpDXt<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 128)), s);
 }
 
