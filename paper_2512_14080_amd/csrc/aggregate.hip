@@ -204,16 +204,6 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
   }
 }
 
-// out[i] = sum_s part[s * n + i] (fixed order)
-__global__ __launch_bounds__(256) void reduce_splits_kernel(const float* __restrict__ part, float* __restrict__ out, int n,
-                                                            int parts) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  float s = 0.f;
-  for (int k = 0; k < parts; ++k) s += part[(size_t)k * n + i];
-  out[i] = s;
-}
-
 // out[i] = sum_k part[i * parts + k] (fixed order)
 __global__ __launch_bounds__(256) void reduce_rowparts_kernel(const float* __restrict__ part, float* __restrict__ out,
                                                               int n, int parts) {
@@ -224,18 +214,10 @@ __global__ __launch_bounds__(256) void reduce_rowparts_kernel(const float* __res
   out[i] = s;
 }
 
-// WrT[e][i] = W_r[i][e] (bf16 copy)
-__global__ __launch_bounds__(256) void transpose_wr_kernel(const uint16_t* __restrict__ Wr, uint16_t* __restrict__ WrT,
-                                                           int d, int E) {
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= d * E) return;
-  const int e = idx / d, i = idx % d;
-  WrT[idx] = Wr[(size_t)i * E + e];
-}
-
 // dbias[e] = sum_t dL[t][e] in two fixed-order passes: per chunk of
 // kColRows tokens a column sum (reads of a row are contiguous across the
-// block), then one block per expert reduces the chunk sums with a fixed tree.
+// block), then one block per expert reduces the chunk sums with a fixed tree
+// (in router_grad_reduce_kernel).
 __global__ __launch_bounds__(128) void colsum_rows_kernel(const uint16_t* __restrict__ dL, float* __restrict__ part,
                                                           int T, int E) {
   const int r0 = blockIdx.x * kColRows, r1 = min(T, r0 + kColRows);
@@ -247,16 +229,29 @@ __global__ __launch_bounds__(128) void colsum_rows_kernel(const uint16_t* __rest
   }
 }
 
-__global__ __launch_bounds__(256) void colsum_parts_kernel(const float* __restrict__ part, float* __restrict__ out,
-                                                           int chunks, int E) {
+// The router gradients' last reductions in one launch: workgroups [0, nr)
+// sum the dW_r split-K partials (fixed split order), the next ne the dbias
+// chunk sums of one expert each (fixed tree).
+__global__ __launch_bounds__(256) void router_grad_reduce_kernel(const float* __restrict__ dwr_part,
+                                                                 float* __restrict__ dWr, int n, int splits, int nr,
+                                                                 const float* __restrict__ cs_part,
+                                                                 float* __restrict__ dbias, int chunks, int E) {
+  if ((int)blockIdx.x < nr) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    if (i >= n) return;
+    float s = 0.f;
+    for (int k = 0; k < splits; ++k) s += dwr_part[(size_t)k * n + i];
+    dWr[i] = s;
+    return;
+  }
   __shared__ float red[4];
-  const int e = blockIdx.x;
+  const int e = blockIdx.x - nr;
   float s = 0.f;
-  for (int i = threadIdx.x; i < chunks; i += 256) s += part[(size_t)i * E + e];
+  for (int i = threadIdx.x; i < chunks; i += 256) s += cs_part[(size_t)i * E + e];
   s = wave_sum(s);
   if (lane_id() == 0) red[threadIdx.x >> 6] = s;
   __syncthreads();
-  if (threadIdx.x == 0) out[e] = (red[0] + red[1]) + (red[2] + red[3]);
+  if (threadIdx.x == 0) dbias[e] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
 hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s) {
@@ -291,27 +286,25 @@ hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const uint16_t* W
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_rows(const float* part, float* out, int rows, int parts, hipStream_t s) {
-  reduce_splits_kernel<<<dim3((rows + 255) / 256), dim3(256), 0, s>>>(part, out, rows, parts);
-  return hipGetLastError();
-}
-
 hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s) {
   reduce_rowparts_kernel<<<dim3((rows + 255) / 256), dim3(256), 0, s>>>(part, out, rows, parts);
   return hipGetLastError();
 }
 
-hipError_t launch_transpose_wr(const uint16_t* Wr, uint16_t* WrT, int d, int E, hipStream_t s) {
-  transpose_wr_kernel<<<dim3((d * E + 255) / 256), dim3(256), 0, s>>>(Wr, WrT, d, E);
+int colsum_chunks(int T) { return (T + kColRows - 1) / kColRows; }
+
+hipError_t launch_colsum_rows(const uint16_t* dL, float* part, int T, int E, hipStream_t s) {
+  const int chunks = colsum_chunks(T);
+  if (chunks > 0) colsum_rows_kernel<<<dim3(chunks), dim3(128), 0, s>>>(dL, part, T, E);
   return hipGetLastError();
 }
 
-int colsum_chunks(int T) { return (T + kColRows - 1) / kColRows; }
-
-hipError_t launch_colsum_bf16(const uint16_t* dL, float* part, float* dbias, int T, int E, hipStream_t s) {
-  const int chunks = colsum_chunks(T);
-  if (chunks > 0) colsum_rows_kernel<<<dim3(chunks), dim3(128), 0, s>>>(dL, part, T, E);
-  colsum_parts_kernel<<<dim3(E), dim3(256), 0, s>>>(part, dbias, chunks, E);
+hipError_t launch_router_grad_reduce(const float* dwr_part, float* dWr, int n, int splits, const float* cs_part,
+                                     float* dbias, int T, int E, hipStream_t s) {
+  const int nr = dWr ? (n + 255) / 256 : 0, ne = dbias ? E : 0;
+  if (nr + ne == 0) return hipSuccess;
+  router_grad_reduce_kernel<<<dim3(nr + ne), dim3(256), 0, s>>>(dwr_part, dWr, n, splits, nr, cs_part, dbias,
+                                                               colsum_chunks(T), E);
   return hipGetLastError();
 }
 

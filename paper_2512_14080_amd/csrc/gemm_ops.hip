@@ -248,16 +248,25 @@ static_assert(kMTilesThreads == kKChunksThreads, "one workgroup size");
 __global__ __launch_bounds__(kMTilesThreads) void bwd_lists_kernel(const int32_t* __restrict__ offsets, int E,
                                                                   int32_t* __restrict__ mtiles, int tpe2, int slabs2,
                                                                   int32_t* __restrict__ klist2, int tpe1, int slabs1,
-                                                                  int32_t* __restrict__ klist1) {
+                                                                  int32_t* __restrict__ klist1,
+                                                                  const uint16_t* __restrict__ Wr,
+                                                                  uint16_t* __restrict__ WrT, int d) {
   __shared__ int lds[2 * 4097];
   __shared__ int scan_lds[kMTilesThreads / 64];
   __shared__ int sh_kc;
-  if (blockIdx.x == 0)
+  if (blockIdx.x == 0) {
     mtiles_body(offsets, E, mtiles, lds, lds + 4097, scan_lds);
-  else if (blockIdx.x == 1)
+  } else if (blockIdx.x == 1) {
     kchunks_body(offsets, E, tpe2, slabs2, klist2, lds, scan_lds, &sh_kc);
-  else
+  } else if (blockIdx.x == 2) {
     kchunks_body(offsets, E, tpe1, slabs1, klist1, lds, scan_lds, &sh_kc);
+  } else {  // W_r transpose, one element per thread
+    const int idx = (blockIdx.x - 3) * kMTilesThreads + threadIdx.x;
+    if (idx < d * E) {
+      const int e = idx / d, i = idx % d;
+      WrT[idx] = Wr[(size_t)i * E + e];
+    }
+  }
 }
 
 // partials of split experts -> bf16 dW: chunk slabs summed in chunk order
@@ -1153,14 +1162,15 @@ static void dw1_tile(int d, int n, int* bm, int* bn) {
 }
 
 hipError_t launch_bwd_lists(const int32_t* offsets, int E, int d, int n, int32_t* mtiles, int32_t* klist2,
-                            int32_t* klist1, hipStream_t s) {
+                            int32_t* klist1, const uint16_t* Wr, uint16_t* WrT, hipStream_t s) {
   if (E > 4096) return hipErrorInvalidValue;
   int bm2, bn2, bm1, bn1;
   dw2_tile(d, n, &bm2, &bn2);
   dw1_tile(d, n, &bm1, &bn1);
   const int tpe2 = (n / bm2) * (d / bn2), tpe1 = (d / bm1) * (2 * n / bn1);
-  bwd_lists_kernel<<<3, kMTilesThreads, 0, s>>>(offsets, E, mtiles, tpe2, dw_slabs((int64_t)n * d), klist2, tpe1,
-                                                dw_slabs((int64_t)d * 2 * n), klist1);
+  const int tr_blocks = Wr ? (d * E + kMTilesThreads - 1) / kMTilesThreads : 0;
+  bwd_lists_kernel<<<3 + tr_blocks, kMTilesThreads, 0, s>>>(offsets, E, mtiles, tpe2, dw_slabs((int64_t)n * d), klist2,
+                                                           tpe1, dw_slabs((int64_t)d * 2 * n), klist1, Wr, WrT, d);
   return hipGetLastError();
 }
 
@@ -1211,8 +1221,7 @@ hipError_t launch_dwr(const DWrArgs& a, hipStream_t s) {
     err = run<OpDWr<C128x128>>({a}, a.splits * mtn, s);
   else
     err = run<OpDWr<C128x256>>({a}, a.splits * mtn * ((a.E + 255) / 256), s);
-  if (err != hipSuccess) return err;
-  return launch_reduce_rows(a.part, a.dWr, a.d * a.E, a.splits, s);
+  return err;  // the partials are summed by launch_router_grad_reduce
 }
 
 }  // namespace smoe

@@ -12,9 +12,10 @@ namespace smoe {
 hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
                              uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s);
 hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, bool counts_only, hipStream_t s);
-hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, hipStream_t s);
+// counted: r.mask_prefix and r.counts are already written (by launch_round)
+hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, bool counted, hipStream_t s);
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
-                        hipStream_t s);
+                        bool* counted, hipStream_t s);
 
 // GEMMs (all bf16 in, fp32 accumulation)
 struct RouterGemmArgs {
@@ -63,9 +64,10 @@ size_t kchunks_bytes(int E);
 size_t dw_part_bytes(int d, int n);
 int dw_slabs(int64_t mn);
 // the backward's m-tile list (as launch_mtiles) and the k-chunk lists of dW2
-// and dW1, in one launch
+// and dW1, in one launch; with Wr non-null the same launch writes WrT[e][i] =
+// Wr[i][e] (the dX aggregation's router term reads W_r by expert)
 hipError_t launch_bwd_lists(const int32_t* offsets, int E, int d, int n, int32_t* mtiles, int32_t* klist2,
-                            int32_t* klist1, hipStream_t s);
+                            int32_t* klist1, const uint16_t* Wr, uint16_t* WrT, hipStream_t s);
 
 struct DW2Args {
   const uint16_t* Ap; const uint16_t* dO; const int32_t* offsets; const int32_t* row_token; uint16_t* dW2;
@@ -91,12 +93,14 @@ hipError_t launch_dwr(const DWrArgs& a, hipStream_t s);
 hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s);
 hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const uint16_t* WrT, const moe_routing& r, uint16_t* dX,
                          uint16_t* dL, int T, int d, int E, hipStream_t s);
-hipError_t launch_reduce_rows(const float* part, float* out, int rows, int parts, hipStream_t s);
 hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s);
-hipError_t launch_transpose_wr(const uint16_t* Wr, uint16_t* WrT, int d, int E, hipStream_t s);
-// dbias = column sums of dL [T][E]; part holds colsum_chunks(T) * E floats
+// dbias = column sums of dL [T][E]: per-chunk sums into part (colsum_chunks(T)
+// * E floats), then router_grad_reduce sums them; it also sums the dW_r
+// split-K partials (dwr_part: splits x n floats).  Either output may be null.
 int colsum_chunks(int T);
-hipError_t launch_colsum_bf16(const uint16_t* dL, float* part, float* dbias, int T, int E, hipStream_t s);
+hipError_t launch_colsum_rows(const uint16_t* dL, float* part, int T, int E, hipStream_t s);
+hipError_t launch_router_grad_reduce(const float* dwr_part, float* dWr, int n, int splits, const float* cs_part,
+                                     float* dbias, int T, int E, hipStream_t s);
 
 // timing hooks (moe_abi.cpp)
 void prof_begin(int kernel_class, hipStream_t s);

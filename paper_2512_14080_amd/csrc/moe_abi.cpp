@@ -318,8 +318,9 @@ int moe_round_tokens(moe_dims m, int32_t m_tile, int mode, const float* u, const
   if (tr == tc || tr->mask == tc->mask) return fail(MOE_ERR_INVALID_ARG, "tr must not alias tc");
   hipStream_t stream = (hipStream_t)stream_;
   smoe::prof_begin(MOE_KC_ROUND, stream);
-  hipError_t e = smoe::launch_round(*tc, *tr, u, m.T, m.E, m_tile, mode, stream);
-  if (e == hipSuccess) e = smoe::launch_metadata(*tr, tc->scores_t, m.T, m.E, stream);
+  bool counted = false;
+  hipError_t e = smoe::launch_round(*tc, *tr, u, m.T, m.E, m_tile, mode, &counted, stream);
+  if (e == hipSuccess) e = smoe::launch_metadata(*tr, tc->scores_t, m.T, m.E, counted, stream);
   smoe::prof_end(MOE_KC_ROUND, stream);
   if (e != hipSuccess) return hip_fail(e, "token rounding");
   return MOE_OK;
@@ -380,7 +381,9 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   hipStream_t stream = (hipStream_t)stream_;
   float* dS_out = dS ? dS : w.dS;
   const int nnt = smoe::dh_n_tiles(m.n);
-  HIP_TRY(smoe::launch_bwd_lists(r->offsets, m.E, m.d, m.n, w.mtiles, w.klist2, w.klist1, stream), "tile lists");
+  HIP_TRY(smoe::launch_bwd_lists(r->offsets, m.E, m.d, m.n, w.mtiles, w.klist2, w.klist1, Wr, Wr ? w.WrT : nullptr,
+                                 stream),
+          "tile lists and W_r transpose");
   LAUNCH(MOE_KC_DH,
          smoe::launch_dh({dO, W2, H, r->offsets, r->row_token, r->row_w, w.dH, w.Ap, dS_out, w.dS_part, m.d, m.n, m.E,
                           r->capacity, w.mtiles},
@@ -391,15 +394,14 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   LAUNCH(MOE_KC_DXT, smoe::launch_dxt({w.dH, W1, r->offsets, w.dXt, m.d, m.n, m.E, r->capacity, w.mtiles}, stream),
          "dX~");
   LAUNCH(MOE_KC_DW1, smoe::launch_dw1({X, w.dH, r->offsets, r->row_token, dW1, m.d, m.n, m.E, w.klist1, w.dw_part}, stream), "dW1");
-  if (Wr) HIP_TRY(smoe::launch_transpose_wr(Wr, w.WrT, m.d, m.E, stream), "W_r transpose");
   LAUNCH(MOE_KC_AGG_DX,
          smoe::launch_agg_dx(w.dXt, dS_out, Wr ? w.WrT : nullptr, *r, dX, Wr ? w.dL : nullptr, m.T, m.d, m.E, stream),
          "dX aggregation");
-  if (dWr) {
-    const int splits = smoe::dwr_splits(m.T, m.d, m.E);
-    LAUNCH(MOE_KC_DWR, smoe::launch_dwr({X, w.dL, w.dWr_part, dWr, m.T, m.d, m.E, splits}, stream), "dW_r");
-  }
-  if (dbias) HIP_TRY(smoe::launch_colsum_bf16(w.dL, w.dbias_part, dbias, m.T, m.E, stream), "dbias");
+  const int splits = smoe::dwr_splits(m.T, m.d, m.E);
+  if (dWr) LAUNCH(MOE_KC_DWR, smoe::launch_dwr({X, w.dL, w.dWr_part, dWr, m.T, m.d, m.E, splits}, stream), "dW_r");
+  if (dbias) HIP_TRY(smoe::launch_colsum_rows(w.dL, w.dbias_part, m.T, m.E, stream), "dbias");
+  HIP_TRY(smoe::launch_router_grad_reduce(w.dWr_part, dWr, m.d * m.E, splits, w.dbias_part, dbias, m.T, m.E, stream),
+          "router gradient reduction");
   return MOE_OK;
 }
 

@@ -108,7 +108,8 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
                                                                 const int32_t* __restrict__ need_arr,
                                                                 const int32_t* __restrict__ counts,
                                                                 const float* __restrict__ u, int M, int mode, int T,
-                                                                int W) {
+                                                                int W, int32_t* __restrict__ prefix_out,
+                                                                int32_t* __restrict__ counts_out) {
   constexpr int kWaves = kSelThreads / 64;
   __shared__ int lds[kWaves];
   __shared__ int cnt_lds[2][kWaves];  // per-wave counts of a pass, double-buffered by pass parity
@@ -125,8 +126,23 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     tr_decide_one(counts[e], mode == MOE_ROUND_STOCHASTIC ? u[e] : 0.f, T, M, mode, &dir, &need);
     if (threadIdx.x == 0) round_dir[e] = dir;
   }
+  // With KPT > 0 (W <= 16 * KPT <= 1024 words) the block also writes the
+  // rounded row's word prefix counts and the expert's row count, which are
+  // otherwise a pass of their own.
+  auto write_prefix = [&](int pc) {
+    int total;
+    const int ex = block_excl_scan<kSelThreads>(pc, &total, lds);
+    if ((int)threadIdx.x < W) prefix_out[(size_t)e * W + threadIdx.x] = ex;
+    if (threadIdx.x == 0) counts_out[e] = total;
+  };
   if (dir == 0 || need == 0) {
-    for (int w = threadIdx.x; w < W; w += kSelThreads) dst[w] = src[w];
+    if constexpr (KPT > 0) {
+      const uint64_t v = (int)threadIdx.x < W ? src[threadIdx.x] : 0ull;
+      if ((int)threadIdx.x < W) dst[threadIdx.x] = v;
+      write_prefix(__popcll(v));
+    } else {
+      for (int w = threadIdx.x; w < W; w += kSelThreads) dst[w] = src[w];
+    }
     return;
   }
   const float* S = scores_t + (size_t)e * T;
@@ -322,6 +338,7 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     // Register form: all tie counts first (flat index slot * waves + wave),
     // one block scan for every tie's rank base, then all flips.
     __shared__ int tie_base[KPT * kWaves];
+    __shared__ int word_pc[KPT * kWaves];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const uint64_t ties = __ballot((tie_mask >> i) & 1u);
@@ -343,8 +360,14 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
       const int rank = tie_base[w] + __popcll(ties & lanemask_lt());
       const bool flip = gt || (tie && rank >= first_tie && rank < last_tie);
       const uint64_t flips = __ballot(flip);
-      if (w < W && lane == 0) dst[w] = src[w] ^ flips;
+      if (w < W && lane == 0) {
+        const uint64_t v = src[w] ^ flips;
+        dst[w] = v;
+        word_pc[w] = __popcll(v);
+      }
     }
+    __syncthreads();
+    write_prefix((int)threadIdx.x < W ? word_pc[threadIdx.x] : 0);
   } else {
     for (int i = 0; i < slots; ++i) {
       bool c;
@@ -355,7 +378,7 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
 }
 
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
-                        hipStream_t s) {
+                        bool* counted, hipStream_t s) {
   // Balance-f is sequential over experts: its own pass decides; the other
   // subroutines are decided inside the selection workgroups
   int32_t* need = nullptr;
@@ -366,8 +389,9 @@ hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, 
   const int slots = (T + kSelThreads - 1) / kSelThreads;
   auto select = [&](auto kernel) {
     kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, tc.counts, u, M,
-                                                 mode, T, tr.words);
+                                                 mode, T, tr.words, tr.mask_prefix, tr.counts);
   };
+  *counted = slots <= 32;
   if (slots <= 4)
     select(tr_select_kernel<4>);
   else if (slots <= 16)

@@ -754,11 +754,11 @@ hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, bool co
   return hipGetLastError();
 }
 
-hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, hipStream_t s) {
+hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, bool counted, hipStream_t s) {
   const int W = r.words;
   int32_t* word_sum = r.scratch + E + 64;  // [W]
   int32_t* word_base = word_sum + W + 1;   // [W + 1]
-  expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
+  if (!counted) expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
   // one extra workgroup turns the expert counts into offsets
   token_count_kernel<<<dim3(W + 1), dim3(64), 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, word_sum, r.counts,
                                                       r.offsets, T, E, W);
