@@ -243,7 +243,9 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     auto wave_sum_u = [&](uint32_t x) { return dpp_reduce(x, [](uint32_t a, uint32_t b) { return a + b; }); };
     // two bits per pass: block counts of the alive keys whose next digit is
     // 3, 2 and 1 decide the digit of tau (16 passes, one barrier each)
-    __shared__ int cnt3_lds[2][3][kWaves];
+    // per-wave counts of a pass: digit 1, and digits 3 (low half) and 2 (high
+    // half) packed (block totals stay below 2^16), read back four waves at a time
+    __shared__ __attribute__((aligned(16))) uint32_t cnt3_lds[2][2][kWaves];
 #pragma unroll
     for (int sh = 30; sh >= 0; sh -= 2) {
       const uint32_t hi = plane[sh + 1], lo = plane[sh];
@@ -252,18 +254,19 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
       const uint32_t c32 = wave_sum_u((uint32_t)__popc(a3) | ((uint32_t)__popc(a2) << 16));
       const uint32_t c1 = wave_sum_u((uint32_t)__popc(a1));
       if (lane == 0) {
-        cnt3_lds[parity][0][wave] = (int)c1;
-        cnt3_lds[parity][1][wave] = (int)(c32 >> 16);
-        cnt3_lds[parity][2][wave] = (int)(c32 & 0xffffu);
+        cnt3_lds[parity][0][wave] = c1;
+        cnt3_lds[parity][1][wave] = c32;
       }
       __syncthreads();
-      int t1 = 0, t2 = 0, t3 = 0;
+      uint32_t s1 = 0, s32 = 0;
 #pragma unroll
-      for (int q = 0; q < kWaves; ++q) {
-        t1 += cnt3_lds[parity][0][q];
-        t2 += cnt3_lds[parity][1][q];
-        t3 += cnt3_lds[parity][2][q];
+      for (int q = 0; q < kWaves; q += 4) {
+        const u32x4 x = *(const u32x4*)&cnt3_lds[parity][0][q];
+        const u32x4 y = *(const u32x4*)&cnt3_lds[parity][1][q];
+        s1 += (x[0] + x[1]) + (x[2] + x[3]);
+        s32 += (y[0] + y[1]) + (y[2] + y[3]);
       }
+      const int t1 = (int)s1, t2 = (int)(s32 >> 16), t3 = (int)(s32 & 0xffffu);
       parity ^= 1;
       if (t3 >= remaining) {
         prefix |= 3u << sh;
