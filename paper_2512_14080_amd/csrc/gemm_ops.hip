@@ -1102,6 +1102,8 @@ hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
   // 128-row tiles while 256-row tiles would leave CUs idle
   if (a.E <= 128 && mt < 2 * cu_count()) return run<OpRouter<C128x128>>({a}, (a.T + 127) / 128, s);
   if (a.E <= 128) return run<OpRouter<C256x128>>({a}, mt, s);
+  if (mt * ((a.E + 255) / 256) < cu_count())
+    return run<OpRouter<C128x256>>({a}, (a.T + 127) / 128 * ((a.E + 255) / 256), s);
   return run<OpRouter<C256x256>>({a}, mt * ((a.E + 255) / 256), s);
 }
 
@@ -1205,7 +1207,8 @@ hipError_t launch_dw1(const DW1Args& a, hipStream_t s) {
 }
 
 int dwr_splits(int T, int d, int E) {
-  const int tiles = (d / 128) * ((E + 127) / 128);
+  // the output tiles of launch_dwr's configuration: 128 x 64, 128 x 128 or 128 x 256
+  const int tiles = (d / 128) * (E <= 128 ? 1 : (E + 255) / 256);
   int s = 256 / tiles;  // at most one tile per CU: a second round would double the time
   const int max_s = (T + 255) / 256;  // at least 256 tokens per split
   if (s > max_s) s = max_s;
