@@ -1098,6 +1098,7 @@ using C128x64 = GemmCfg<128, 64, 4, 2, 3>;
 
 hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
   const int mt = (a.T + 255) / 256;
+  if (a.E <= 64 && mt < cu_count()) return run<OpRouter<C128x64>>({a}, (a.T + 127) / 128, s);
   if (a.E <= 64) return run<OpRouter<C256x64>>({a}, mt, s);
   // 128-row tiles while 256-row tiles would leave CUs idle
   if (a.E <= 128 && mt < 2 * cu_count()) return run<OpRouter<C128x128>>({a}, (a.T + 127) / 128, s);
