@@ -38,15 +38,20 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the HIP/C++ sources of the library (sorted by file name)."""
+    """sha256 over the HIP/C++ sources of the library (sorted by file name), with comments and runs of
+    whitespace removed, so that an edit of comments alone keeps a profile of unchanged kernels valid."""
     import hashlib
+    import re
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2512_14080_amd", "csrc")
     for f in sorted(os.listdir(d)):
         if f.endswith((".hip", ".h", ".cpp")):
             h.update(f.encode())
-            with open(os.path.join(d, f), "rb") as fh:
-                h.update(fh.read())
+            with open(os.path.join(d, f), encoding="utf-8") as fh:
+                text = fh.read()
+            text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+            text = re.sub(r"//[^\n]*", " ", text)
+            h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 

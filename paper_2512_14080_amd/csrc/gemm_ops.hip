@@ -446,9 +446,10 @@ struct OpRouter {
 // 16-byte chunk c of staged row r sits at chunk c ^ ((r >> 1) & 7), which
 // keeps both the writes (one chunk of 16 rows) and the reads (two whole
 // rows per 16 lanes) free of bank conflicts.  The stores are nontemporal:
-// these outputs (Y, dX~, the weight gradients) are consumed by a later
-// kernel that streams them once, and left in the cache as dirty lines they
-// only add write-back traffic at the end of the producing kernel.
+// these outputs (H and A, Y, dH and A', dX~, the weight gradients) are
+// consumed by a later kernel that streams them once, and left in the cache
+// as dirty lines they only add write-back traffic at the end of the
+// producing kernel (plain stores measured slower for up and no better for dH).
 constexpr int kStageBytesPerWave = 16 * 128;
 template <class Cfg>
 constexpr bool kStagedStores = Cfg::RN % 2 == 0 && Cfg::LDS_BYTES + Cfg::NW * kStageBytesPerWave + 256 <= 160 * 1024;
