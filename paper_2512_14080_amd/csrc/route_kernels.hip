@@ -217,6 +217,24 @@ __device__ __forceinline__ void topk_cex(uint64_t& a, uint64_t& b) {  // a >= b 
   b = sw ? a : b;
   a = hi;
 }
+// bitonic sort of KM pairs, largest first (KM a power of two)
+template <int KM>
+__device__ __forceinline__ void topk_sort(uint64_t (&v)[KM]) {
+#pragma unroll
+  for (int k = 2; k <= KM; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < KM; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          if ((i & k) == 0)
+            topk_cex<KM>(v[i], v[l]);
+          else
+            topk_cex<KM>(v[l], v[i]);
+        }
+      }
+}
 template <int KM>
 __device__ __forceinline__ void topk_merge(uint64_t (&a)[KM], const uint64_t (&b)[KM]) {
 #pragma unroll
@@ -287,27 +305,45 @@ __global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, flo
   uint64_t top[KM];
 #pragma unroll
   for (int k = 0; k < KM; ++k) top[k] = 0;  // below every (key, ~expert) pair
-  for (int g = 0; g < Gq; ++g) {
-    f32x4 p = cols[g * 64 + lane];
-    const int eg = e0 + 4 * g;
-    if (do_softmax) {
+  // Pairs are taken in groups of KM: each group is sorted by a bitonic network
+  // and merged into the running top-KM list, i.e. independent compare-exchanges
+  // instead of a serial insertion chain per pair.  One step covers G2 float4s
+  // (KM = 8: two); slots past the slice and lanes past T hold 0, below every
+  // real pair.
+  constexpr int G2 = KM >= 4 ? KM / 4 : 1;
+  for (int g0 = 0; g0 < Gq; g0 += G2) {
+    uint64_t pr[4 * G2];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) p[c] = p[c] / s;
-      cols[g * 64 + lane] = p;
-      if (live) *(f32x4*)(scores + (size_t)t * E + eg) = p;
-    }
-    if (scores_t && live) {
+    for (int gg = 0; gg < G2; ++gg) {
+      const int g = g0 + gg;
+      if (g < Gq) {
+        f32x4 p = cols[g * 64 + lane];
+        const int eg = e0 + 4 * g;
+        if (do_softmax) {
 #pragma unroll
-      for (int c = 0; c < 4; ++c) scores_t[(size_t)(eg + c) * T + t] = p[c];
-    }
+          for (int c = 0; c < 4; ++c) p[c] = p[c] / s;
+          cols[g * 64 + lane] = p;
+          if (live) *(f32x4*)(scores + (size_t)t * E + eg) = p;
+        }
+        if (scores_t && live) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const uint64_t x0 = ((uint64_t)topk_key(p[c]) << 32) | (uint32_t)~(uint32_t)(eg + c);
-      if (__ballot(live && x0 > top[KM - 1])) {
-        uint64_t x = x0;
+          for (int c = 0; c < 4; ++c) scores_t[(size_t)(eg + c) * T + t] = p[c];
+        }
 #pragma unroll
-        for (int k = 0; k < KM; ++k) topk_cex<KM>(top[k], x);
+        for (int c = 0; c < 4; ++c)
+          pr[4 * gg + c] = live ? ((uint64_t)topk_key(p[c]) << 32) | (uint32_t)~(uint32_t)(eg + c) : 0ull;
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) pr[4 * gg + c] = 0ull;
       }
+    }
+#pragma unroll
+    for (int h = 0; h < 4 * G2; h += KM) {
+      uint64_t grp[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) grp[k] = pr[h + k];
+      topk_sort<KM>(grp);
+      topk_merge<KM>(top, grp);
     }
   }
   if constexpr (NW > 1) {
