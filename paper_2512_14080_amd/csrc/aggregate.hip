@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256) void reduce_rowparts_kernel(const float* __res
 // dbias[e] = sum_t dL[t][e] in two fixed-order passes: per chunk of
 // kColRows tokens a column sum (reads of a row are contiguous across the
 // block), then one block per expert reduces the chunk sums with a fixed tree
-// (in router_grad_reduce_kernel).
+// (in bwd_final_reduce_kernel).
 __global__ __launch_bounds__(128) void colsum_rows_kernel(const uint16_t* __restrict__ dL, float* __restrict__ part,
                                                           int T, int E) {
   const int r0 = blockIdx.x * kColRows, r1 = min(T, r0 + kColRows);
@@ -227,31 +227,6 @@ __global__ __launch_bounds__(128) void colsum_rows_kernel(const uint16_t* __rest
     for (int r = r0; r < r1; ++r) s += bf2f(dL[(size_t)r * E + c]);
     part[(size_t)blockIdx.x * E + c] = s;
   }
-}
-
-// The router gradients' last reductions in one launch: workgroups [0, nr)
-// sum the dW_r split-K partials (fixed split order), the next ne the dbias
-// chunk sums of one expert each (fixed tree).
-__global__ __launch_bounds__(256) void router_grad_reduce_kernel(const float* __restrict__ dwr_part,
-                                                                 float* __restrict__ dWr, int n, int splits, int nr,
-                                                                 const float* __restrict__ cs_part,
-                                                                 float* __restrict__ dbias, int chunks, int E) {
-  if ((int)blockIdx.x < nr) {
-    const int i = blockIdx.x * 256 + threadIdx.x;
-    if (i >= n) return;
-    float s = 0.f;
-    for (int k = 0; k < splits; ++k) s += dwr_part[(size_t)k * n + i];
-    dWr[i] = s;
-    return;
-  }
-  __shared__ float red[4];
-  const int e = blockIdx.x - nr;
-  float s = 0.f;
-  for (int i = threadIdx.x; i < chunks; i += 256) s += cs_part[(size_t)i * E + e];
-  s = wave_sum(s);
-  if (lane_id() == 0) red[threadIdx.x >> 6] = s;
-  __syncthreads();
-  if (threadIdx.x == 0) dbias[e] = (red[0] + red[1]) + (red[2] + red[3]);
 }
 
 hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s) {
@@ -299,13 +274,5 @@ hipError_t launch_colsum_rows(const uint16_t* dL, float* part, int T, int E, hip
   return hipGetLastError();
 }
 
-hipError_t launch_router_grad_reduce(const float* dwr_part, float* dWr, int n, int splits, const float* cs_part,
-                                     float* dbias, int T, int E, hipStream_t s) {
-  const int nr = dWr ? (n + 255) / 256 : 0, ne = dbias ? E : 0;
-  if (nr + ne == 0) return hipSuccess;
-  router_grad_reduce_kernel<<<dim3(nr + ne), dim3(256), 0, s>>>(dwr_part, dWr, n, splits, nr, cs_part, dbias,
-                                                               colsum_chunks(T), E);
-  return hipGetLastError();
-}
 
 }  // namespace smoe

@@ -270,14 +270,16 @@ __global__ __launch_bounds__(kMTilesThreads) void bwd_lists_kernel(const int32_t
 }
 
 // partials of split experts -> bf16 dW: chunk slabs summed in chunk order
-__global__ __launch_bounds__(256) void dw_reduce_kernel(const int32_t* __restrict__ klist, const float* __restrict__ part,
-                                                        uint16_t* __restrict__ dW, int E, int64_t MN) {
+// workgroup (bx, by) of a gx x gy grid
+__device__ __forceinline__ void dw_reduce_body(const int32_t* __restrict__ klist, const float* __restrict__ part,
+                                               uint16_t* __restrict__ dW, int E, int64_t MN, int bx, int by, int gx,
+                                               int gy) {
   const SMOE_CONST int32_t* h = (const SMOE_CONST int32_t*)klist;
   const SMOE_CONST i32x4* spl = (const SMOE_CONST i32x4*)(klist + kchunks_split_off(E));
-  for (int si = blockIdx.y; si < h[1]; si += gridDim.y) {
+  for (int si = by; si < h[1]; si += gy) {
     const i32x4 sp = spl[si];
     const int e = sp[0], first = sp[1], nc = sp[2];
-    for (int64_t i = 4 * ((int64_t)blockIdx.x * 256 + threadIdx.x); i < MN; i += 4 * (int64_t)gridDim.x * 256) {
+    for (int64_t i = 4 * ((int64_t)bx * 256 + threadIdx.x); i < MN; i += 4 * (int64_t)gx * 256) {
       f32x4 a = *(const f32x4*)(part + (size_t)first * MN + i);
       for (int c = 1; c < nc; ++c) {
         const f32x4 b = *(const f32x4*)(part + (size_t)(first + c) * MN + i);
@@ -291,13 +293,60 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const int32_t* __restric
   }
 }
 
+__global__ __launch_bounds__(256) void dw_reduce_kernel(const int32_t* __restrict__ klist, const float* __restrict__ part,
+                                                        uint16_t* __restrict__ dW, int E, int64_t MN) {
+  dw_reduce_body(klist, part, dW, E, MN, blockIdx.x, blockIdx.y, gridDim.x, gridDim.y);
+}
+
+static void dw_reduce_grid(int64_t MN, int slabs, int* gx, int* gy) {
+  *gx = (int)std::min<int64_t>((MN / 4 + 255) / 256, 64);
+  // split experts are looped over: most calls have none, and a grid sized for
+  // every possible one would mostly launch workgroups that exit at once
+  *gy = slabs > 0 ? std::min(slabs / 2, 8) : 0;
+}
+
+// The backward's last reductions in one launch: workgroups [0, nd) sum the
+// dW1 chunk slabs of split experts (as dw_reduce_kernel), the next nr the dW_r
+// split-K partials (fixed split order), the last ne the dbias chunk sums of
+// one expert each (fixed tree).
+__global__ __launch_bounds__(256) void bwd_final_reduce_kernel(const int32_t* __restrict__ klist1,
+                                                               const float* __restrict__ part1,
+                                                               uint16_t* __restrict__ dW1, int64_t MN1, int gx1,
+                                                               int gy1, const float* __restrict__ dwr_part,
+                                                               float* __restrict__ dWr, int n, int splits, int nr,
+                                                               const float* __restrict__ cs_part,
+                                                               float* __restrict__ dbias, int chunks, int E) {
+  const int nd = gx1 * gy1;
+  int b = blockIdx.x;
+  if (b < nd) {
+    dw_reduce_body(klist1, part1, dW1, E, MN1, b % gx1, b / gx1, gx1, gy1);
+    return;
+  }
+  b -= nd;
+  if (b < nr) {
+    const int i = b * 256 + threadIdx.x;
+    if (i >= n) return;
+    float s = 0.f;
+    for (int k = 0; k < splits; ++k) s += dwr_part[(size_t)k * n + i];
+    dWr[i] = s;
+    return;
+  }
+  __shared__ float red[4];
+  const int e = b - nr;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < chunks; i += 256) s += cs_part[(size_t)i * E + e];
+  s = wave_sum(s);
+  if (lane_id() == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) dbias[e] = (red[0] + red[1]) + (red[2] + red[3]);
+}
+
 hipError_t launch_dw_reduce(const int32_t* klist, const float* part, uint16_t* dW, int E, int64_t MN, int slabs,
                             hipStream_t s) {
   if (slabs <= 0) return hipSuccess;
-  const int gx = (int)std::min<int64_t>((MN / 4 + 255) / 256, 64);
-  // split experts are looped over: most calls have none, and a grid sized for
-  // every possible one would mostly launch workgroups that exit at once
-  dw_reduce_kernel<<<dim3(gx, std::min(slabs / 2, 8)), dim3(256), 0, s>>>(klist, part, dW, E, MN);
+  int gx, gy;
+  dw_reduce_grid(MN, slabs, &gx, &gy);
+  dw_reduce_kernel<<<dim3(gx, gy), dim3(256), 0, s>>>(klist, part, dW, E, MN);
   return hipGetLastError();
 }
 
@@ -1178,14 +1227,14 @@ hipError_t launch_bwd_lists(const int32_t* offsets, int E, int d, int n, int32_t
   return hipGetLastError();
 }
 
-// the GEMM over the k-chunk list, then the partials of split experts
+// the GEMM over the k-chunk list, then (if reduce) the partials of split experts
 template <class Op, class Args>
-static hipError_t run_dw(const Args& a, int M, int N, uint16_t* dW, hipStream_t s) {
+static hipError_t run_dw(const Args& a, int M, int N, uint16_t* dW, bool reduce, hipStream_t s) {
   using Cfg = typename Op::Cfg;
   const int tpe = (M / Cfg::BM) * (N / Cfg::BN);
   const int slabs = dw_slabs((int64_t)M * N);
   hipError_t err = run<Op>({a}, pad8((a.E + slabs) * tpe), s);
-  if (err != hipSuccess) return err;
+  if (err != hipSuccess || !reduce) return err;
   return launch_dw_reduce(a.klist, a.part, dW, a.E, (int64_t)M * N, slabs, s);
 }
 
@@ -1193,19 +1242,34 @@ hipError_t launch_dw2(const DW2Args& a, hipStream_t s) {
   int bm, bn;
   dw2_tile(a.d, a.n, &bm, &bn);
   if (bn == 256) {
-    if (bm == 256) return run_dw<OpDW2<W256x256>>(a, a.n, a.d, a.dW2, s);
-    if (bm == 128) return run_dw<OpDW2<W128x256>>(a, a.n, a.d, a.dW2, s);
-    return run_dw<OpDW2<W64x256>>(a, a.n, a.d, a.dW2, s);
+    if (bm == 256) return run_dw<OpDW2<W256x256>>(a, a.n, a.d, a.dW2, true, s);
+    if (bm == 128) return run_dw<OpDW2<W128x256>>(a, a.n, a.d, a.dW2, true, s);
+    return run_dw<OpDW2<W64x256>>(a, a.n, a.d, a.dW2, true, s);
   }
-  if (bm == 128) return run_dw<OpDW2<W128x128>>(a, a.n, a.d, a.dW2, s);
-  return run_dw<OpDW2<W64x128>>(a, a.n, a.d, a.dW2, s);
+  if (bm == 128) return run_dw<OpDW2<W128x128>>(a, a.n, a.d, a.dW2, true, s);
+  return run_dw<OpDW2<W64x128>>(a, a.n, a.d, a.dW2, true, s);
 }
 
 hipError_t launch_dw1(const DW1Args& a, hipStream_t s) {
   int bm, bn;
   dw1_tile(a.d, a.n, &bm, &bn);
-  if (bm == 256) return run_dw<OpDW1<W256x256>>(a, a.d, 2 * a.n, a.dW1, s);
-  return run_dw<OpDW1<W128x128>>(a, a.d, 2 * a.n, a.dW1, s);
+  // its split experts are summed by launch_bwd_final_reduce
+  if (bm == 256) return run_dw<OpDW1<W256x256>>(a, a.d, 2 * a.n, a.dW1, false, s);
+  return run_dw<OpDW1<W128x128>>(a, a.d, 2 * a.n, a.dW1, false, s);
+}
+
+hipError_t launch_bwd_final_reduce(const int32_t* klist1, const float* part1, uint16_t* dW1, int d, int n,
+                                   const float* dwr_part, float* dWr, int splits, const float* cs_part, float* dbias,
+                                   int T, int E, hipStream_t s) {
+  const int64_t MN1 = (int64_t)d * 2 * n;
+  int gx1, gy1;
+  dw_reduce_grid(MN1, dw_slabs(MN1), &gx1, &gy1);
+  const int nr = dWr ? (d * E + 255) / 256 : 0, ne = dbias ? E : 0;
+  const int blocks = gx1 * gy1 + nr + ne;
+  if (blocks == 0) return hipSuccess;
+  bwd_final_reduce_kernel<<<dim3(blocks), dim3(256), 0, s>>>(klist1, part1, dW1, MN1, gx1, gy1, dwr_part, dWr, d * E,
+                                                             splits, nr, cs_part, dbias, colsum_chunks(T), E);
+  return hipGetLastError();
 }
 
 int dwr_splits(int T, int d, int E) {
@@ -1226,7 +1290,7 @@ hipError_t launch_dwr(const DWrArgs& a, hipStream_t s) {
     err = run<OpDWr<C128x128>>({a}, a.splits * mtn, s);
   else
     err = run<OpDWr<C128x256>>({a}, a.splits * mtn * ((a.E + 255) / 256), s);
-  return err;  // the partials are summed by launch_router_grad_reduce
+  return err;  // the partials are summed by launch_bwd_final_reduce
 }
 
 }  // namespace smoe

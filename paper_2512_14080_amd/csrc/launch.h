@@ -95,12 +95,14 @@ hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const uint16_t* W
                          uint16_t* dL, int T, int d, int E, hipStream_t s);
 hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s);
 // dbias = column sums of dL [T][E]: per-chunk sums into part (colsum_chunks(T)
-// * E floats), then router_grad_reduce sums them; it also sums the dW_r
-// split-K partials (dwr_part: splits x n floats).  Either output may be null.
+// * E floats), then launch_bwd_final_reduce sums them.  That launch also sums
+// the dW1 chunk slabs of split experts (launch_dw1 leaves them) and the dW_r
+// split-K partials (dwr_part: splits x d x E floats); dWr and dbias may be null.
 int colsum_chunks(int T);
 hipError_t launch_colsum_rows(const uint16_t* dL, float* part, int T, int E, hipStream_t s);
-hipError_t launch_router_grad_reduce(const float* dwr_part, float* dWr, int n, int splits, const float* cs_part,
-                                     float* dbias, int T, int E, hipStream_t s);
+hipError_t launch_bwd_final_reduce(const int32_t* klist1, const float* part1, uint16_t* dW1, int d, int n,
+                                   const float* dwr_part, float* dWr, int splits, const float* cs_part, float* dbias,
+                                   int T, int E, hipStream_t s);
 
 // timing hooks (moe_abi.cpp)
 void prof_begin(int kernel_class, hipStream_t s);

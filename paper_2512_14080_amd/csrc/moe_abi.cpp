@@ -400,8 +400,9 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   const int splits = smoe::dwr_splits(m.T, m.d, m.E);
   if (dWr) LAUNCH(MOE_KC_DWR, smoe::launch_dwr({X, w.dL, w.dWr_part, dWr, m.T, m.d, m.E, splits}, stream), "dW_r");
   if (dbias) HIP_TRY(smoe::launch_colsum_rows(w.dL, w.dbias_part, m.T, m.E, stream), "dbias");
-  HIP_TRY(smoe::launch_router_grad_reduce(w.dWr_part, dWr, m.d * m.E, splits, w.dbias_part, dbias, m.T, m.E, stream),
-          "router gradient reduction");
+  HIP_TRY(smoe::launch_bwd_final_reduce(w.klist1, w.dw_part, dW1, m.d, m.n, w.dWr_part, dWr, splits, w.dbias_part,
+                                        dbias, m.T, m.E, stream),
+          "final reductions (dW1 split experts, dW_r, dbias)");
   return MOE_OK;
 }
 
