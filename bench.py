@@ -331,6 +331,82 @@ def measure(args, cfg, cpu):
     return out
 
 
+def ablation(args):
+    """Evidence for two design choices at the layer's shape (one JSON line each, not the benchmark record):
+    the fused top-K router kernel against softmax + top-K in torch on the same logits, and the gathered inputs
+    of up-proj, dH and dW1 against the same GEMMs on inputs already laid out per expert (a token-per-row layer
+    with K = 1 whose tokens come sorted by expert, so every gather index is the identity)."""
+    import numpy as np
+    import torch
+
+    from paper_2512_14080_amd import binding as B
+    from paper_2512_14080_amd import workloads as W
+    from paper_2512_14080_amd.layer import DeviceLayer
+
+    cfg = W.CONFIGS[args.config]
+
+    def class_ms(layer, classes, reps=5):
+        out = {}
+        for c in classes:
+            B.moe_prof_select(c)
+            for _ in range(reps):
+                layer.step()
+            ms, nl = B.moe_prof_read()
+            out[c] = round(ms / nl, 5) if nl else None
+        B.moe_prof_select(-1)
+        return out
+
+    layer = DeviceLayer(W.make_inputs(cfg, 0), round_mode="nearest")
+    for _ in range(3):
+        layer.step()
+    P = layer.rows()
+    gathered = class_ms(layer, ["topk", "up_proj", "dH", "dW1"])
+    del layer
+    torch.cuda.empty_cache()
+
+    g = torch.Generator(device="cuda").manual_seed(0)
+    logits = torch.randn(cfg.T, cfg.E, device="cuda", generator=g)
+
+    def torch_route():
+        s = torch.softmax(logits, dim=1)
+        v, i = torch.topk(s, cfg.K, dim=1)
+        return s, v / v.sum(dim=1, keepdim=True), i
+
+    for _ in range(3):
+        torch_route()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(20):
+        torch_route()
+    e1.record()
+    torch.cuda.synchronize()
+    t_torch = e0.elapsed_time(e1) / 20
+    rd = cfg.T * cfg.E * 4 / 1e9
+    print(json.dumps({"ablation": "top-K router", "workload": f"T={cfg.T} E={cfg.E} K={cfg.K} fp32 logits",
+                      "fused_kernel_ms": gathered["topk"], "torch_softmax_topk_ms": round(t_torch, 5),
+                      "fused_logit_read_GBps": round(rd / (gathered["topk"] * 1e-3), 1),
+                      "torch_logit_read_GBps": round(rd / (t_torch * 1e-3), 1),
+                      "note": "the fused kernel also writes the transposed scores and the membership bitmap"}),
+          flush=True)
+    del logits
+    torch.cuda.empty_cache()
+
+    # the same GEMM work on inputs laid out per expert: P tokens, one expert each, sorted by expert
+    per_e = max(cfg.m_tile, round(P / cfg.E / cfg.m_tile) * cfg.m_tile)
+    cc = W.MoEConfig("contiguous", T=per_e * cfg.E, d=cfg.d, n=cfg.n, E=cfg.E, K=1, m_tile=cfg.m_tile)
+    S = np.zeros((cc.T, cc.E), dtype=np.float32)
+    S[np.arange(cc.T), np.arange(cc.T) // per_e] = 1.0
+    layer = DeviceLayer(W.make_inputs(cc, 0), round_mode=None, scores_in=S)
+    for _ in range(3):
+        layer.step()
+    contiguous = class_ms(layer, ["up_proj", "dH", "dW1"])
+    print(json.dumps({"ablation": "gathered vs contiguous inputs", "workload": f"{cfg.name}: P={P} rows "
+                      f"(contiguous: {cc.T} tokens, K=1, {per_e} per expert)",
+                      "gathered_ms": {c: gathered[c] for c in contiguous}, "contiguous_ms": contiguous}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -340,6 +416,8 @@ def main():
     ap.add_argument("--round", default="nearest", help="rounding mode, or 'none' for token-choice routing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown", action="store_true", help="also time every kernel class")
+    ap.add_argument("--ablation", action="store_true",
+                    help="fused top-K vs torch, gathered vs contiguous GEMM inputs (JSON lines, not the record)")
     ap.add_argument("--sweep", default=None,
                     help="measure every layer of a named sweep (e.g. 'paper': the paper's benchmark shapes), "
                          "one JSON line each, no CPU baseline")
@@ -373,6 +451,9 @@ def main():
     from paper_2512_14080_amd import workloads as W
 
     B.lib()  # fail loudly if the library is missing
+    if args.ablation:
+        ablation(args)
+        return
     if args.sweep:
         for name in W.SWEEPS[args.sweep]:
             out = measure(args, W.CONFIGS[name], cpu=False)
