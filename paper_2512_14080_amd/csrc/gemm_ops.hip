@@ -773,6 +773,38 @@ struct OpUp {
   }
 };
 
+// As store_rows_bf16, for ops whose last stage buffer is idle during the
+// epilogue (no DMA writes it before the next tile's first barrier): each 32 x
+// 64 block pair goes through the wave's 4 KB share of it in one round
+// (stage_block32 twice, then store_staged32) instead of two 16-row rounds
+// through the 2 KB epilogue area.
+template <class Cfg>
+__device__ __forceinline__ void store_rows_bf16_stage(uint16_t* out, int64_t ld, int row_base, int mrows, int n0,
+                                                      Acc<Cfg>& t, char* epi) {
+  static_assert(Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 4096, "a 4 KB share of the last stage per wave");
+  char* st = epi - Cfg::STAGE_BYTES + (threadIdx.x >> 6) * 4096;
+  const int wm0 = t.m_of(0) - (threadIdx.x & 31);
+#pragma unroll
+  for (int i = 0; i < Cfg::RM; ++i) {
+    const int m0 = wm0 + 32 * i;  // first tile row of the block
+    if (m0 >= mrows) continue;
+#pragma unroll
+    for (int j = 0; j + 1 < Cfg::RN; j += 2) {
+      u32x2 v0[4], v1[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        v0[g] = pack_bf16x4(t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2], t.acc[i][j][4 * g + 3]);
+        v1[g] = pack_bf16x4(t.acc[i][j + 1][4 * g], t.acc[i][j + 1][4 * g + 1], t.acc[i][j + 1][4 * g + 2],
+                            t.acc[i][j + 1][4 * g + 3]);
+      }
+      const int col = n0 + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1);
+      stage_block32(st, 0, v0);
+      stage_block32(st, 1, v1);
+      store_staged32(st, out + (size_t)(row_base + m0) * ld + col, ld, mrows - m0);
+    }
+  }
+}
+
 // ================================================================== down-proj
 template <class Cfg_>
 struct OpDown {
@@ -798,7 +830,10 @@ struct OpDown {
     s.init(w, p.a.d, nullptr, 0, p.a.n, p.a.d, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
-    store_rows_bf16<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    if constexpr (Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 4096)
+      store_rows_bf16_stage<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    else
+      store_rows_bf16<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
   }
 };
 
@@ -998,7 +1033,10 @@ struct OpDXt {
     s.init(p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, nullptr, ti.n0, Cfg::BN);
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
-    store_rows_bf16<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    if constexpr (Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 4096)
+      store_rows_bf16_stage<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    else
+      store_rows_bf16<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
   }
 };
 
