@@ -733,9 +733,23 @@ struct OpUp {
               ha[q][g] = pack_bf16x4(av[0], av[1], av[2], av[3]);
             }
           const int rv = ti.mrows - m0;
-          store_rows64_staged(wl, p.a.H + r0 * (2 * n) + col, 2 * n, rv, hg[0], hg[1]);
-          store_rows64_staged(wl, p.a.H + r0 * (2 * n) + n + col, 2 * n, rv, hu[0], hu[1]);
-          store_rows64_staged(wl, p.a.A + r0 * n + col, n, rv, ha[0], ha[1]);
+          if constexpr (Cfg::STAGE_BYTES >= Cfg::NW * 8192) {
+            // one round per output through the wave's 8 KB of the idle last stage buffer
+            char* st = epi - Cfg::STAGE_BYTES + (threadIdx.x >> 6) * 8192;
+            stage_block32(st, 0, hg[0]);
+            stage_block32(st, 1, hg[1]);
+            store_staged32(st, p.a.H + r0 * (2 * n) + col, 2 * n, rv);
+            stage_block32(st + 4096, 0, hu[0]);
+            stage_block32(st + 4096, 1, hu[1]);
+            store_staged32(st + 4096, p.a.H + r0 * (2 * n) + n + col, 2 * n, rv);
+            stage_block32(st, 0, ha[0]);
+            stage_block32(st, 1, ha[1]);
+            store_staged32(st, p.a.A + r0 * n + col, n, rv);
+          } else {
+            store_rows64_staged(wl, p.a.H + r0 * (2 * n) + col, 2 * n, rv, hg[0], hg[1]);
+            store_rows64_staged(wl, p.a.H + r0 * (2 * n) + n + col, 2 * n, rv, hu[0], hu[1]);
+            store_rows64_staged(wl, p.a.A + r0 * n + col, n, rv, ha[0], ha[1]);
+          }
         }
       }
       return;
