@@ -819,6 +819,16 @@ __device__ __forceinline__ void store_rows_bf16_stage(uint16_t* out, int64_t ld,
   }
 }
 
+// the one-round form where the last stage buffer allows it
+template <class Cfg>
+__device__ __forceinline__ void store_rows_bf16_any(uint16_t* out, int64_t ld, int row_base, int mrows, int n0,
+                                                    Acc<Cfg>& t, char* epi) {
+  if constexpr (Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 4096)
+    store_rows_bf16_stage<Cfg>(out, ld, row_base, mrows, n0, t, epi);
+  else
+    store_rows_bf16<Cfg>(out, ld, row_base, mrows, n0, t, epi);
+}
+
 // ================================================================== down-proj
 template <class Cfg_>
 struct OpDown {
@@ -844,10 +854,7 @@ struct OpDown {
     s.init(w, p.a.d, nullptr, 0, p.a.n, p.a.d, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
-    if constexpr (Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 4096)
-      store_rows_bf16_stage<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
-    else
-      store_rows_bf16<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    store_rows_bf16_any<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
   }
 };
 
@@ -1047,10 +1054,7 @@ struct OpDXt {
     s.init(p.a.W1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, nullptr, ti.n0, Cfg::BN);
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
-    if constexpr (Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 4096)
-      store_rows_bf16_stage<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
-    else
-      store_rows_bf16<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    store_rows_bf16_any<Cfg>(p.a.dXt, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
   }
 };
 
@@ -1079,7 +1083,7 @@ struct OpDW2 {
     if (ti.row_base >= 0)
       store_part_f32<Cfg>(p.a.part + (size_t)ti.row_base * p.a.n * p.a.d, p.a.d, ti.m0, ti.n0, t);
     else
-      store_rows_bf16<Cfg>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti.m0, Cfg::BM, ti.n0, t, epi);
+      store_rows_bf16_any<Cfg>(p.a.dW2 + (size_t)ti.e * p.a.n * p.a.d, p.a.d, ti.m0, Cfg::BM, ti.n0, t, epi);
   }
 };
 
@@ -1107,7 +1111,7 @@ struct OpDW1 {
     if (ti.row_base >= 0)
       store_part_f32<Cfg>(p.a.part + (size_t)ti.row_base * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, ti.n0, t);
     else
-      store_rows_bf16<Cfg>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, Cfg::BM, ti.n0, t, epi);
+      store_rows_bf16_any<Cfg>(p.a.dW1 + (size_t)ti.e * p.a.d * (2 * p.a.n), 2 * p.a.n, ti.m0, Cfg::BM, ti.n0, t, epi);
   }
 };
 
