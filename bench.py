@@ -23,6 +23,7 @@ if ROOT not in sys.path:
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+FLUSH_BYTES = 512 << 20     # scratch written before each timed step: more than L2 (8 x 4 MB) + Infinity Cache (256 MB)
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_7b_tr128.md")
 
 # kernel-name fragment -> kernel class (as in the library's timing classes)
@@ -35,6 +36,16 @@ KERNEL_CLASS_OF = [("OpUp<", "up_proj"), ("OpDown<", "down_proj"), ("OpDH<", "dH
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def quantile(sorted_vals, q):
+    """Linear-interpolation quantile of an ascending list."""
+    if not sorted_vals:
+        return float("nan")
+    x = q * (len(sorted_vals) - 1)
+    i = int(x)
+    j = min(i + 1, len(sorted_vals) - 1)
+    return sorted_vals[i] + (sorted_vals[j] - sorted_vals[i]) * (x - i)
 
 
 def kernel_source_hash() -> str:
@@ -206,10 +217,25 @@ def padding_rows(layer):
     return int(((counts + 127) // 128 * 128 - counts).sum())
 
 
-def cpu_baseline(cfg, round_mode, inp, budget_s=15.0):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(cfg, round_mode, inp, budget_s=8.0, repeats=3):
     """Time the CPU oracle (route + round + fwd + bwd, fp32) on a token sample of the workload.
 
-    The sample is the first T' tokens of the same seeded inputs (full d, n, E, K)."""
+    The sample is the first T' tokens of the same seeded inputs (full d, n, E, K), sized so one run takes
+    about budget_s; the reported time is the median of `repeats` runs."""
+    import statistics
+
     import numpy as np
 
     import oracle
@@ -232,7 +258,11 @@ def cpu_baseline(cfg, round_mode, inp, budget_s=15.0):
     if dt < budget_s / 3 and T < cfg.T:
         T = int(min(cfg.T, max(T, T * budget_s / max(dt, 1e-3) * 0.8)))
         T = max(64, T // 64 * 64)
+    times = []
+    for _ in range(repeats):
         dt, P = run(T)
+        times.append(dt)
+    dt = statistics.median(times)
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
@@ -240,9 +270,11 @@ def cpu_baseline(cfg, round_mode, inp, budget_s=15.0):
         threads = os.cpu_count()
     tflops = cfg.model_flops(P) / dt / 1e12
     return {"value": round(tflops, 6), "unit": "TFLOPS", "cores": int(threads), "kind": "oracle",
+            "host_cpus": os.cpu_count(), "blas_threads": int(threads), "cpu_model": cpu_model(),
+            "runs_s": [round(t, 3) for t in times],
             "sample": f"{T} of {cfg.T} tokens of the {cfg.name} layer (full d, n, E, K), "
-                      f"route+{'round+' if round_mode else ''}fwd+bwd in fp32 NumPy, {dt:.2f} s, "
-                      f"{T / dt:.1f} tokens/s"}
+                      f"route+{'round+' if round_mode else ''}fwd+bwd in fp32 NumPy, median of {repeats} runs "
+                      f"{dt:.2f} s, {T / dt:.1f} tokens/s"}
 
 
 def measure(args, cfg, cpu):
@@ -280,21 +312,39 @@ def measure(args, cfg, cpu):
     dominant = max(cands, key=cands.get)
     log("[bench] per-launch ms: " + ", ".join(f"{c}={t:.4f}" for c, t in per.items()))
 
-    # timed region: K steps, events around the dominant kernel's launches
-    B.moe_prof_select(dominant)
+    # back-to-back steps without any timing hooks (the caches keep what the previous step left)
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    ev0.record(stream)
+    eb0, eb1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    eb0.record(stream)
     for _ in range(args.steps):
         layer.step()
-    ev1.record(stream)
+    eb1.record(stream)
+    torch.cuda.synchronize()
+    ms_b2b = eb0.elapsed_time(eb1) / args.steps
+
+    # timed region: K steps, each after a write of FLUSH_BYTES of scratch (L2 and the Infinity Cache start
+    # cold) and bracketed by its own events; the dominant kernel's launches are bracketed by the library's
+    # events on the launch stream
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device="cuda")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    B.moe_prof_select(dominant)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        flush.fill_(i)
+        evs[i][0].record(stream)
+        layer.step()
+        evs[i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     dom_ms, dom_n = B.moe_prof_read()
     B.moe_prof_select(-1)
-    ms_step = ev0.elapsed_time(ev1) / args.steps
-    log(f"[bench] timed {args.steps} steps: {ms_step:.4f} ms/step (wall {wall * 1e3 / args.steps:.4f} ms/step)")
+    del flush
+    step_ms = sorted(a.elapsed_time(b) for a, b in evs)
+    ms_step = quantile(step_ms, 0.5)
+    log(f"[bench] timed {args.steps} flushed steps: median {ms_step:.4f} ms/step, p10 {quantile(step_ms, 0.1):.4f}, "
+        f"p90 {quantile(step_ms, 0.9):.4f} (wall incl. flushes {wall * 1e3 / args.steps:.4f} ms/step); "
+        f"back-to-back without hooks {ms_b2b:.4f} ms/step")
 
     flops = cfg.model_flops(P)
     tflops = flops / (ms_step * 1e-3) / 1e12
@@ -309,7 +359,13 @@ def measure(args, cfg, cpu):
     out = {
         "metric": "MoE layer fwd+bwd TFLOPS and tokens/s on 1 MI355X (% of bf16 MFMA peak)",
         "value": round(tflops, 3), "unit": "TFLOPS", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "ms_per_step": round(ms_step, 4),
+        "step_ms": {"median": round(ms_step, 4), "mean": round(sum(step_ms) / len(step_ms), 4),
+                    "p10": round(quantile(step_ms, 0.1), 4), "p90": round(quantile(step_ms, 0.9), 4),
+                    "min": round(step_ms[0], 4), "max": round(step_ms[-1], 4),
+                    "timing": f"each step after a {FLUSH_BYTES >> 20} MiB scratch write, own HIP events",
+                    "back_to_back_mean": round(ms_b2b, 4)},
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{cfg.name}: T={cfg.T} d={cfg.d} n={cfg.n} E={cfg.E} K={cfg.K} "
                                f"{'token rounding ' + round_mode + ' M_tile=' + str(cfg.m_tile) if round_mode else 'token choice'}",

@@ -68,6 +68,10 @@ enum {
 typedef struct {
   int32_t capacity;      /* rows the row_* / tok_rows arrays can hold          */
   int32_t words;         /* W = ceil(T/64), 64-bit words per expert in mask    */
+  int32_t state;         /* host-side build state, MOE_ROUTING_STATE_*: set by
+                            moe_routing_init / moe_route / moe_round_tokens
+                            (what has been enqueued), checked by the consumers */
+  int32_t reserved;      /* zero                                               */
   float *logits;         /* [T,E] router logits (nullable: MOE_ROUTING_LOGITS)  */
   float *scores;         /* [T,E] S_full = softmax over all E experts          */
   float *scores_t;       /* [E,T] transposed S_full (nullable: MOE_ROUTING_SCORES_T;
@@ -87,7 +91,23 @@ typedef struct {
   float *tok_denom;      /* [T]   sum of the token's selected scores           */
   int32_t *round_dir;    /* [E]   -1 dropped / 0 kept / +1 padded (rounding)   */
   int32_t *scratch;      /* internal scan scratch                              */
+  int32_t *status;       /* [1]   device word: 0 once the metadata kernels have
+                            run on a consistent selection; otherwise the OR of
+                            MOE_STATUS_* bits, and the rows are not valid
+                            (every index written is still in bounds)        */
 } moe_routing;
+
+/* moe_routing.state */
+enum {
+  MOE_ROUTING_STATE_EMPTY = 0,  /* laid out by moe_routing_init; nothing written  */
+  MOE_ROUTING_STATE_COUNTS = 1, /* mask, mask_prefix, counts (MOE_ROUTE_COUNTS_ONLY) */
+  MOE_ROUTING_STATE_BUILT = 2   /* complete metadata: moe_fwd / moe_bwd accept it */
+};
+
+/* bits of the device status word */
+enum {
+  MOE_STATUS_DUPLICATE_EXPERT = 1 /* a token's topk_idx lists an expert twice   */
+};
 
 enum {
   MOE_ROUTING_LOGITS = 1,   /* carve the logits array                 */
@@ -98,12 +118,14 @@ enum {
 size_t moe_routing_bytes(moe_dims dims, int32_t capacity, int flags);
 
 /* Lays out the routing arrays inside `buf` (device, 256-byte aligned, at least
- * moe_routing_bytes() bytes) and fills `*r` (host struct).  Enqueues nothing. */
+ * moe_routing_bytes() bytes) and fills `*r` (host struct, state
+ * MOE_ROUTING_STATE_EMPTY).  Enqueues nothing. */
 int moe_routing_init(moe_dims dims, int32_t capacity, int flags, void *buf, size_t bytes,
                      moe_routing *r);
 
 /* Smallest capacity that token rounding to multiples of m_tile may need:
- * min(T*E, T*K + E*(m_tile-1)). */
+ * min(T*E, T*K + E*(m_tile-1)); -1 for invalid dims or an m_tile outside
+ * the powers of two in [8, 256]. */
 int32_t moe_round_capacity(moe_dims dims, int32_t m_tile);
 
 /* moe_route flags */
@@ -115,7 +137,9 @@ enum {
   MOE_ROUTE_COUNTS_ONLY = 8     /* metadata stops at mask, mask_prefix and
                                    counts: enough for moe_round_tokens, which
                                    builds the rounded routing's own metadata;
-                                   offsets and the row lists are not written */
+                                   offsets and the row lists are not written,
+                                   and r->state becomes MOE_ROUTING_STATE_COUNTS,
+                                   which moe_fwd and moe_bwd refuse          */
 };
 
 /*
@@ -129,7 +153,9 @@ enum {
  * rows (row_token, row_expert, row_w), token-major CSR (tok_offsets, tok_rows).
  *   X     [T,d] bf16;  Wr [d,E] bf16 (unused with MOE_ROUTE_SCORES_IN)
  *   bias  [E] fp32, nullable
- * r->capacity must be >= T*K.
+ * r->capacity must be >= T*K.  On success r->state is MOE_ROUTING_STATE_BUILT
+ * (MOE_ROUTING_STATE_COUNTS with MOE_ROUTE_COUNTS_ONLY) and the device word
+ * r->status is cleared by the metadata kernels.
  * Scores are compared through the order-preserving image of their fp32 bit
  * pattern, which is the float order for numbers (+0 = -0) and extends it to
  * NaN (sign clear: above +Inf; sign set: below -Inf), so non-finite scores
@@ -156,11 +182,13 @@ enum {
  * highest-scored non-TC tokens; |f^TR_e - f_e| < m_tile.  An expert whose
  * ceiling exceeds T is rounded down.  Weights are renormalised over each
  * token's new expert set.
- *   tc     routing written by moe_route (needs tc->scores_t written, i.e.
- *          MOE_ROUTE_WRITE_SCORES_T, and tc->mask/counts)
+ *   tc     routing written by moe_route (state at least
+ *          MOE_ROUTING_STATE_COUNTS; needs tc->scores_t written, i.e.
+ *          MOE_ROUTE_WRITE_SCORES_T)
  *   tr     output routing; tr->capacity >= moe_round_capacity(dims, m_tile);
- *          tr->scores may alias tc->scores (it is read, not written)
- *   m_tile power of two in [8, 256]
+ *          tr->scores may alias tc->scores (it is read, not written); on
+ *          success tr->state is MOE_ROUTING_STATE_BUILT
+ *   m_tile power of two in [8, 256] (otherwise MOE_ERR_INVALID_ARG)
  *   u      [E] fp32 uniforms in [0,1), device, required by MOE_ROUND_STOCHASTIC
  */
 int moe_round_tokens(moe_dims dims, int32_t m_tile, int mode, const float *u, const moe_routing *tc,
@@ -178,6 +206,7 @@ size_t moe_workspace_bytes(moe_dims dims, int32_t capacity, int which);
  *   A = SiLU(H_gate) * H_up       (workspace)
  *   Y = A W2_e                    (workspace)
  *   O_t = sum_{rows of t} s * Y   -> O [T,d] bf16 (zero for a token without experts)
+ *   r   routing in state MOE_ROUTING_STATE_BUILT (otherwise MOE_ERR_INVALID_ARG)
  *   ws  device workspace of moe_workspace_bytes(dims, r->capacity, MOE_WS_FWD)
  */
 int moe_fwd(moe_dims dims, const moe_bf16 *X, const moe_bf16 *W1, const moe_bf16 *W2,
@@ -193,6 +222,7 @@ int moe_fwd(moe_dims dims, const moe_bf16 *X, const moe_bf16 *W1, const moe_bf16
  * where the router gradient on each token's selected set is
  *   dl_j = s_j (dS_j - sum_k s_k dS_k)  (softmax over the selected logits),
  *   dW_r = X^T dL, dbias = column sums of dL.
+ *   r    routing in state MOE_ROUTING_STATE_BUILT (otherwise MOE_ERR_INVALID_ARG)
  *   dO   [T,d] bf16           H [capacity,2n] bf16 from moe_fwd
  *   Wr   [d,E] bf16, nullable: then no router gradient is formed and dX holds
  *        only the expert part

@@ -8,6 +8,13 @@ computes (Section 2.2 and the forward algorithm of Section 3):
     y = a W2_e
     O_t = sum over the rows of token t of s_{t,e} * y
 
+Optional expert biases (the footnote of the "Gradient computation" appendix):
+b1_e [2n] is added to h and b2_e [d] to y.  Then dS_{t,e} = <dO_t, y> gains
+<dO_t, b2_e> next to <dA', a>, and db1_e = sum of dH over the expert's rows,
+db2_e = sum of s * dO_t over them.  (The footnote prints the extra term with
+a garbled second operand; the down-projection bias is the one that makes
+<dO_t, y> differ from <dA', a>.)
+
 The backward follows the "Gradient computation" appendix: with
 dA' = dO_t W2_e^T, dS_{t,e} = <dA', a> (boxed identity), dA = s * dA',
 dH = dSwiGLU(dA, h), A' = s * a, dW2_e = A'^T dO_e, dX~ = dH W1_e^T,
@@ -48,16 +55,20 @@ def dswiglu(dA, H):
     return np.concatenate([dg, du], axis=1)
 
 
-def forward(X, W1, W2, R, dtype=np.float32):
+def forward(X, W1, W2, R, dtype=np.float32, b1=None, b2=None):
     """MoE forward over routing ``R`` (up-proj A kernel, down-proj Y kernel,
     expert aggregation O kernel of the forward algorithm, Section 3).
 
-    Returns dict with O [T,d] and the per-row intermediates H [P,2n],
-    A [P,n], Y [P,d] (the layer caches only X and H, Section 3.2).
+    b1 [E,2n] and b2 [E,d] are optional expert biases of the up- and
+    down-projection.  Returns dict with O [T,d] and the per-row
+    intermediates H [P,2n], A [P,n], Y [P,d] (the layer caches only X and H,
+    Section 3.2).
     """
     X = np.asarray(X, dtype)
     W1 = np.asarray(W1, dtype)
     W2 = np.asarray(W2, dtype)
+    b1 = None if b1 is None else np.asarray(b1, dtype)
+    b2 = None if b2 is None else np.asarray(b2, dtype)
     T, d = X.shape
     E, _, n2 = W1.shape
     P = R.P
@@ -70,10 +81,15 @@ def forward(X, W1, W2, R, dtype=np.float32):
             continue
         Xe = X[R.row_token[r0:r1]]           # gather
         He = Xe @ W1[e]
+        if b1 is not None:
+            He = He + b1[e]
         Ae = swiglu(He)
         H[r0:r1] = He
         A[r0:r1] = Ae
-        Y[r0:r1] = Ae @ W2[e]
+        Ye = Ae @ W2[e]
+        if b2 is not None:
+            Ye = Ye + b2[e]
+        Y[r0:r1] = Ye
     O = np.zeros((T, d), dtype)
     # O_t = sum_e pi_{t,e} s_{t,e} Y_{e,t}; np.add.at accumulates rows in
     # row order, i.e. expert-ascending per token
@@ -81,12 +97,15 @@ def forward(X, W1, W2, R, dtype=np.float32):
     return {"O": O, "H": H, "A": A, "Y": Y}
 
 
-def backward(dO, X, H, W1, W2, Wr, R, dtype=np.float32):
+def backward(dO, X, H, W1, W2, Wr, R, dtype=np.float32, b2=None):
     """MoE backward over routing ``R`` given the cached H.
 
     Expert part: the dH and dW2 kernels of the down-projection backward
     (Section 3), the dX~, dW1 and dX kernels of the up-projection backward
     (Appendix E), with dS, dA and A' as in the "Gradient computation" appendix.
+    With a down-projection bias b2 [E,d], dS of a row gains <dO_t, b2_e>.
+    The expert-bias gradients db1 [E,2n] (column sums of the expert's dH rows)
+    and db2 [E,d] (column sums of its s * dO_t rows) are always returned.
 
     Router part (the paper leaves the router to the caller): the weights are a
     softmax over the token's selected logits, so for a selected expert j
@@ -110,6 +129,9 @@ def backward(dO, X, H, W1, W2, Wr, R, dtype=np.float32):
     dXt = np.zeros((P, d), dtype)
     dW1 = np.zeros_like(W1)
     dW2 = np.zeros_like(W2)
+    db1 = np.zeros((E, n2), dtype)
+    db2 = np.zeros((E, d), dtype)
+    b2 = None if b2 is None else np.asarray(b2, dtype)
     for e in range(E):
         r0, r1 = int(R.offsets[e]), int(R.offsets[e + 1])
         if r0 == r1:
@@ -120,11 +142,15 @@ def backward(dO, X, H, W1, W2, Wr, R, dtype=np.float32):
         dAp = dOe @ W2[e].T                   # dA' = dO_e W2_e^T
         Ae = swiglu(He)                       # recompute A from H
         dS[r0:r1] = (dAp * Ae).sum(axis=1)    # dS = <dA', A>
+        if b2 is not None:
+            dS[r0:r1] += dOe @ b2[e]          # + <dO_t, b2_e>
         dA = w[r0:r1, None] * dAp             # dA = s dA'
         dHe = dswiglu(dA, He)
         Ape = w[r0:r1, None] * Ae             # A' = s A
         dH[r0:r1] = dHe
         Ap[r0:r1] = Ape
+        db1[e] = dHe.sum(axis=0)              # db1 = column sums of dH_e
+        db2[e] = (w[r0:r1, None] * dOe).sum(axis=0)  # db2 = column sums of s dO_e
         dW2[e] = Ape.T @ dOe                  # dW2 = A'^T dO_e
         dW1[e] = X[tok].T @ dHe               # dW1 = X_e^T dH
         dXt[r0:r1] = dHe @ W1[e].T            # dX~ = dH W1_e^T
@@ -137,7 +163,7 @@ def backward(dO, X, H, W1, W2, Wr, R, dtype=np.float32):
     dL = np.zeros((T, E), dtype)
     dL[R.row_token, R.row_expert] = dl
     out = {"dX_experts": dX.copy(), "dW1": dW1, "dW2": dW2, "dS": dS, "dH": dH,
-           "Ap": Ap, "dXt": dXt, "dL": dL}
+           "Ap": Ap, "dXt": dXt, "dL": dL, "db1": db1, "db2": db2}
     if Wr is not None:
         Wr = np.asarray(Wr, dtype)
         out["dWr"] = X.T @ dL

@@ -27,6 +27,12 @@ MOE_ROUTE_WRITE_LOGITS = 2
 MOE_ROUTE_WRITE_SCORES_T = 4
 MOE_ROUTE_COUNTS_ONLY = 8
 
+MOE_ROUTING_STATE_EMPTY = 0
+MOE_ROUTING_STATE_COUNTS = 1
+MOE_ROUTING_STATE_BUILT = 2
+
+MOE_STATUS_DUPLICATE_EXPERT = 1
+
 ROUND_MODES = {"nearest": 0, "up": 1, "down": 2, "balance": 3, "stochastic": 4}
 
 MOE_WS_FWD = 1
@@ -50,10 +56,15 @@ _P = ctypes.c_void_p
 
 class MoeRouting(ctypes.Structure):
     _fields_ = [("capacity", ctypes.c_int32), ("words", ctypes.c_int32),
+                ("state", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("logits", _P), ("scores", _P), ("scores_t", _P), ("topk_idx", _P), ("topk_w", _P),
                 ("mask", _P), ("mask_prefix", _P), ("counts", _P), ("offsets", _P), ("row_token", _P),
                 ("row_expert", _P), ("row_w", _P), ("tok_offsets", _P), ("tok_rows", _P), ("tok_count", _P),
-                ("tok_denom", _P), ("round_dir", _P), ("scratch", _P)]
+                ("tok_denom", _P), ("round_dir", _P), ("scratch", _P), ("status", _P)]
+
+    @classmethod
+    def pointer_fields(cls):
+        return [name for name, typ in cls._fields_ if typ is _P]
 
 
 class MoEError(RuntimeError):
@@ -186,6 +197,7 @@ class Routing:
             "row_token": self.view("row_token", i32, (cap,)), "row_expert": self.view("row_expert", i32, (cap,)),
             "row_w": self.view("row_w", f32, (cap,)), "tok_offsets": self.view("tok_offsets", i32, (T + 1,)),
             "tok_rows": self.view("tok_rows", i32, (cap,)), "round_dir": self.view("round_dir", i32, (E,)),
+            "tok_count": self.view("tok_count", i32, (T,)), "status": self.view("status", i32, (1,)),
         }
 
 

@@ -62,9 +62,11 @@ struct TileInfo {
   int k_len;    // reduction length
 };
 
-// One 16-byte-per-lane LDS DMA.  lds_byte must be wave-uniform (it goes to M0).
+// One 16-byte-per-lane LDS DMA.  lds_byte must be wave-uniform: it is the
+// instruction's M0 operand, which the "{m0}" constraint has the compiler
+// load itself (so M0 is an input it knows about, never a hidden clobber).
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds_byte) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_byte), "v"(g) : "memory", "m0");
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds_byte) : "memory");
 }
 // The lane index from a volatile asm: per-lane address arithmetic derived
 // from it is recomputed where it is used instead of being hoisted out of the
@@ -76,7 +78,7 @@ __device__ __forceinline__ int volatile_lane() {
 }
 // One 4-byte-per-lane LDS DMA (lane l's dword lands at lds_byte + 4 l).
 __device__ __forceinline__ void dma4(const void* g, uint32_t lds_byte) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds_byte), "v"(g) : "memory", "m0");
+  asm volatile("global_load_lds_dword %0, off" ::"v"(g), "{m0}"(lds_byte) : "memory");
 }
 // Wait until at most N of this wave's vector-memory ops are outstanding, then
 // workgroup barrier.  LDS reads of the previous step are complete as well.

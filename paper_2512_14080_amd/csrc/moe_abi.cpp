@@ -60,11 +60,24 @@ int check_routing(const moe_dims& m, const moe_routing* r, int64_t min_capacity,
   if ((int64_t)r->capacity < min_capacity)
     return fail(MOE_ERR_CAPACITY, "%s->capacity %d < required %lld", name, r->capacity, (long long)min_capacity);
   const void* req[] = {r->scores, r->mask, r->mask_prefix, r->counts, r->offsets, r->row_token, r->row_expert,
-                       r->row_w, r->tok_offsets, r->tok_rows, r->tok_count, r->tok_denom, r->round_dir, r->scratch};
+                       r->row_w, r->tok_offsets, r->tok_rows, r->tok_count, r->tok_denom, r->round_dir, r->scratch,
+                       r->status};
   for (const void* p : req)
     if (!p) return fail(MOE_ERR_INVALID_ARG, "%s has a null array (initialise it with moe_routing_init)", name);
   return MOE_OK;
 }
+
+// the consumers of a routing (moe_fwd, moe_bwd) need its complete metadata
+int check_built(const moe_routing* r, const char* name) {
+  if (r->state != MOE_ROUTING_STATE_BUILT)
+    return fail(MOE_ERR_INVALID_ARG,
+                "%s is not a complete routing (state %d; moe_route without MOE_ROUTE_COUNTS_ONLY or "
+                "moe_round_tokens builds one)",
+                name, r->state);
+  return MOE_OK;
+}
+
+bool valid_m_tile(int m) { return m >= 8 && m <= 256 && (m & (m - 1)) == 0; }
 
 // ---------------------------------------------------------------- timing
 std::mutex g_prof_mu;
@@ -171,8 +184,12 @@ size_t routing_layout(const moe_dims& m, int64_t cap, int flags, char* base, moe
   o->round_dir = (int32_t*)p;
   take((size_t)(m.E + 64 + 2 * (W + 1)) * 4, &p);  // rounding needs [E], then per-word token sums and bases
   o->scratch = (int32_t*)p;
+  take(4, &p);
+  o->status = (int32_t*)p;
   o->capacity = (int32_t)cap;
   o->words = W;
+  o->state = MOE_ROUTING_STATE_EMPTY;
+  o->reserved = 0;
   return off;
 }
 
@@ -251,7 +268,7 @@ int moe_routing_init(moe_dims dims, int32_t capacity, int flags, void* buf, size
 }
 
 int32_t moe_round_capacity(moe_dims dims, int32_t m_tile) {
-  if (check_dims(dims) != MOE_OK || m_tile < 1) return -1;
+  if (check_dims(dims) != MOE_OK || !valid_m_tile(m_tile)) return -1;
   const int64_t a = (int64_t)dims.T * dims.E;
   const int64_t b = (int64_t)dims.T * dims.K + (int64_t)dims.E * (m_tile - 1);
   const int64_t c = a < b ? a : b;
@@ -297,8 +314,10 @@ int moe_route(moe_dims m, const moe_bf16* X, const moe_bf16* Wr, const float* bi
          smoe::launch_topk_route(in, r->scores, scores_t, r->topk_idx, r->topk_w, r->mask, m.T, m.E, m.K, r->words,
                                  scores_in ? 0 : 1, stream),
          "softmax/top-K");
-  LAUNCH(MOE_KC_META, smoe::launch_tc_metadata(*r, m.T, m.E, m.K, (flags & MOE_ROUTE_COUNTS_ONLY) != 0, stream),
-         "routing metadata");
+  const bool counts_only = (flags & MOE_ROUTE_COUNTS_ONLY) != 0;
+  r->state = MOE_ROUTING_STATE_EMPTY;  // until the metadata launch is enqueued
+  LAUNCH(MOE_KC_META, smoe::launch_tc_metadata(*r, m.T, m.E, m.K, counts_only, stream), "routing metadata");
+  r->state = counts_only ? MOE_ROUTING_STATE_COUNTS : MOE_ROUTING_STATE_BUILT;
   return MOE_OK;
 }
 
@@ -306,23 +325,28 @@ int moe_round_tokens(moe_dims m, int32_t m_tile, int mode, const float* u, const
                      void* stream_) {
   int rc = check_dims(m);
   if (rc) return rc;
-  if (m_tile < 1 || m_tile > 65536) return fail(MOE_ERR_INVALID_ARG, "m_tile must be in [1, 65536] (got %d)", m_tile);
+  if (!valid_m_tile(m_tile))
+    return fail(MOE_ERR_INVALID_ARG, "m_tile must be a power of two in [8, 256] (got %d)", m_tile);
   if (mode < MOE_ROUND_NEAREST || mode > MOE_ROUND_STOCHASTIC)
     return fail(MOE_ERR_INVALID_ARG, "unknown rounding mode %d", mode);
   if (mode == MOE_ROUND_STOCHASTIC) CHECK_PTR(u, 4);
   rc = check_routing(m, tc, (int64_t)m.T * m.K, "tc");
   if (rc) return rc;
   if (!tc->scores_t) return fail(MOE_ERR_INVALID_ARG, "tc->scores_t must be written (MOE_ROUTE_WRITE_SCORES_T)");
+  if (tc->state < MOE_ROUTING_STATE_COUNTS)
+    return fail(MOE_ERR_INVALID_ARG, "tc has no counts yet (state %d): run moe_route on it first", tc->state);
   rc = check_routing(m, tr, moe_round_capacity(m, m_tile), "tr");
   if (rc) return rc;
   if (tr == tc || tr->mask == tc->mask) return fail(MOE_ERR_INVALID_ARG, "tr must not alias tc");
   hipStream_t stream = (hipStream_t)stream_;
+  tr->state = MOE_ROUTING_STATE_EMPTY;
   smoe::prof_begin(MOE_KC_ROUND, stream);
   bool counted = false;
   hipError_t e = smoe::launch_round(*tc, *tr, u, m.T, m.E, m_tile, mode, &counted, stream);
   if (e == hipSuccess) e = smoe::launch_metadata(*tr, tc->scores_t, m.T, m.E, counted, stream);
   smoe::prof_end(MOE_KC_ROUND, stream);
   if (e != hipSuccess) return hip_fail(e, "token rounding");
+  tr->state = MOE_ROUTING_STATE_BUILT;
   return MOE_OK;
 }
 
@@ -331,6 +355,8 @@ int moe_fwd(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W
   int rc = check_dims(m);
   if (rc) return rc;
   rc = check_routing(m, r, 1, "r");
+  if (rc) return rc;
+  rc = check_built(r, "r");
   if (rc) return rc;
   CHECK_PTR(X, 16);
   CHECK_PTR(W1, 16);
@@ -359,6 +385,8 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   int rc = check_dims(m);
   if (rc) return rc;
   rc = check_routing(m, r, 1, "r");
+  if (rc) return rc;
+  rc = check_built(r, "r");
   if (rc) return rc;
   CHECK_PTR(dO, 16);
   CHECK_PTR(X, 16);

@@ -74,8 +74,9 @@ __device__ __forceinline__ uint32_t score_key(float x) {
 
 constexpr int kSelThreads = 1024;
 
-// 32 x 32 bit transpose in registers (recursive block swaps): afterwards
-// A[b] bit i = bit b of the original A[i].
+// 32 x 32 bit transpose in registers by recursive block swaps (the published
+// bit-matrix transpose, H. S. Warren, "Hacker's Delight", section 7-3):
+// afterwards A[b] bit i = bit b of the original A[i].
 __device__ __forceinline__ void transpose32(uint32_t (&A)[32]) {
   uint32_t m = 0x0000FFFFu;
 #pragma unroll

@@ -43,6 +43,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
                                                          int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
                                                          uint64_t* __restrict__ mask, int T, int E, int K, int W,
                                                          int do_softmax) {
+  static_assert(EPL >= 1 && EPL <= 64, "the taken mask holds one bit per value of a lane");
   extern __shared__ __attribute__((aligned(16))) char dyn[];
   unsigned long long* mword = (unsigned long long*)dyn;                  // [E]
   float* st = (float*)(dyn + ((E * 8 + 15) & ~15));                       // STASH: [E][kStashPitch]
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
     // K rounds of wave arg-max over (value desc, expert asc): the wave maximum
     // of the 32-bit keys (a DPP max), then the lowest expert holding it from
     // ballots (expert 64j + l is value j of lane l: lowest j, then lowest lane)
-    uint32_t taken = 0;
+    uint64_t taken = 0;  // bit j: value j of this lane is selected (EPL <= 64)
     int sel_e[16];
     float sel_v[16];
 #pragma unroll
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
 #pragma unroll
         for (int j = 0; j < EPL; ++j) {
           const int e = lane + 64 * j;
-          if (e < E && !((taken >> j) & 1u)) {
+          if (e < E && !((taken >> j) & 1ull)) {
             const uint32_t c = topk_key(v[j]);
             if (bj < 0 || c > best) {
               best = c;
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
           const uint64_t hit = __ballot(bj == j && best == m);
           if (hit && be == 0x7fffffff) be = __ffsll((unsigned long long)hit) - 1 + 64 * j;
         }
-        if (be != 0x7fffffff && (be & 63) == lane) taken |= 1u << (be >> 6);
+        if (be != 0x7fffffff && (be & 63) == lane) taken |= 1ull << (be >> 6);
         sel_e[k] = be;
         sel_v[k] = topk_value(m);
       }
@@ -145,7 +146,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
     float denom = 0.f;
 #pragma unroll
     for (int j = 0; j < EPL; ++j) {
-      uint64_t sel = __ballot((taken >> j) & 1u);
+      uint64_t sel = __ballot((taken >> j) & 1ull);
       while (sel) {
         const int l = __ffsll((unsigned long long)sel) - 1;
         denom += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[j]), l));
@@ -442,8 +443,9 @@ __global__ __launch_bounds__(256) void expert_scan_kernel(const uint64_t* __rest
 // out[0..n] = exclusive scan of cnt[0..n-1] (one block of 1024 threads, four
 // values per thread per pass).
 __global__ __launch_bounds__(1024) void scan_kernel(const int32_t* __restrict__ cnt, int32_t* __restrict__ out,
-                                                    int n) {
+                                                    int n, int32_t* __restrict__ status) {
   __shared__ int lds[16];
+  if (status && threadIdx.x == 0) *status = 0;  // cleared before the placement that may flag it
   int running = 0;
   for (int c0 = 0; c0 < n; c0 += 4096) {
     const int i0 = c0 + threadIdx.x * 4;
@@ -479,7 +481,7 @@ __global__ __launch_bounds__(256) void tc_place_kernel(const int32_t* __restrict
                                                        int32_t* __restrict__ tok_offsets, int32_t* __restrict__ tok_count,
                                                        int32_t* __restrict__ tok_rows, int32_t* __restrict__ row_token,
                                                        int32_t* __restrict__ row_expert, float* __restrict__ row_w, int T,
-                                                       int K, int W) {
+                                                       int K, int W, int32_t* __restrict__ status) {
   const int t = blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
   const int w = t >> 6, b = t & 63;
@@ -504,7 +506,15 @@ __global__ __launch_bounds__(256) void tc_place_kernel(const int32_t* __restrict
           wv = wt[k];
         }
       last = e;
-      if (e == 0x7fffffff) break;  // fewer than K distinct experts: cannot happen with a valid top-K
+      if (e == 0x7fffffff) {
+        // Fewer than K distinct experts in topk_idx (never from moe_route's
+        // top-K).  The mask then holds fewer rows than T*K: flag the routing
+        // as invalid and point the token's remaining slots at row 0, so a
+        // later kernel that ignores the flag still reads in bounds.
+        atomicOr(status, MOE_STATUS_DUPLICATE_EXPERT);
+        tok_rows[(size_t)t * K + r] = 0;
+        continue;
+      }
       const int row = expert_row(mask, prefix, offsets, e, W, w, below);
       tok_rows[(size_t)t * K + r] = row;
       row_token[row] = t;
@@ -559,10 +569,12 @@ __global__ __launch_bounds__(64) void token_count_kernel(const uint64_t* __restr
                                                          const float* __restrict__ scores_t, int32_t* __restrict__ cnt,
                                                          float* __restrict__ denom, int32_t* __restrict__ word_sum,
                                                          const int32_t* __restrict__ counts,
-                                                         int32_t* __restrict__ offsets, int T, int E, int W) {
+                                                         int32_t* __restrict__ offsets, int T, int E, int W,
+                                                         int32_t* __restrict__ status) {
   const int w = blockIdx.x;
   const int lane = lane_id();
   if (w == W) {
+    if (lane == 0) *status = 0;  // membership from the bitmap: always consistent
     // the extra workgroup: offsets = exclusive scan of the expert counts
     int running = 0;
     for (int e0 = 0; e0 < E; e0 += 64) {
@@ -783,10 +795,10 @@ hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, bool co
   const int W = r.words;
   expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
   if (counts_only) return hipGetLastError();
-  scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.counts, r.offsets, E);
+  scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(r.counts, r.offsets, E, r.status);
   tc_place_kernel<<<dim3((T + 255) / 256), dim3(256), 0, s>>>(r.topk_idx, r.topk_w, r.mask, r.mask_prefix, r.offsets,
                                                               r.tok_offsets, r.tok_count, r.tok_rows, r.row_token,
-                                                              r.row_expert, r.row_w, T, K, W);
+                                                              r.row_expert, r.row_w, T, K, W, r.status);
   return hipGetLastError();
 }
 
@@ -797,11 +809,11 @@ hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, i
   if (!counted) expert_scan_kernel<<<dim3(E), dim3(256), 0, s>>>(r.mask, r.mask_prefix, r.counts, W);
   // one extra workgroup turns the expert counts into offsets
   token_count_kernel<<<dim3(W + 1), dim3(64), 0, s>>>(r.mask, scores_t, r.tok_count, r.tok_denom, word_sum, r.counts,
-                                                      r.offsets, T, E, W);
+                                                      r.offsets, T, E, W, r.status);
   // up to kPlaceSumWords words every placement workgroup sums the word sums
   // before it itself; beyond that a scan kernel provides the bases
   const bool scan_words = W > kPlaceSumWords;
-  if (scan_words) scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(word_sum, word_base, W);
+  if (scan_words) scan_kernel<<<dim3(1), dim3(1024), 0, s>>>(word_sum, word_base, W, nullptr);
   token_place_kernel<<<dim3(W), dim3(64 * kPlaceWaves), 0, s>>>(r.mask, r.mask_prefix, r.offsets, r.tok_count,
                                                                 scan_words ? word_base : nullptr, word_sum,
                                                                 r.tok_offsets, scores_t, r.tok_denom, r.tok_rows,

@@ -58,7 +58,7 @@ CONFIGS = {
     "coarse": MoEConfig("coarse", T=16384, d=4096, n=14336, E=8, K=2, m_tile=128),
 }
 
-# The paper's benchmark layers (Appendix G, the H100 table): four model sizes,
+# The paper's benchmark layers (Appendix H, the H100 table): four model sizes,
 # each at three granularities with equal FLOPs (n * K fixed).
 PAPER_SHAPES = [
     ("1.4b", 40960, 768, [(256, 128, 8), (512, 64, 4), (1024, 32, 2)]),
@@ -70,7 +70,7 @@ for _size, _T, _d, _rows in PAPER_SHAPES:
     for _n, _E, _K in _rows:
         _name = f"paper-{_size}-e{_E}k{_K}"
         CONFIGS[_name] = MoEConfig(_name, T=_T, d=_d, n=_n, E=_E, K=_K, m_tile=128)
-# The paper's token-rounding speed sweeps (Appendix G): four (T, d, n, K)
+# The paper's token-rounding speed sweeps (Appendix H): four (T, d, n, K)
 # families, each over a range of E, with M_tile = 128.
 TR_SWEEPS = [
     (16384, 1536, 256, 8, [64, 128, 256, 512]),

@@ -69,7 +69,8 @@ def _fake_routing(D, capacity):
     r = B.MoeRouting()
     r.capacity = capacity
     r.words = (D.T + 63) // 64
-    for i, (name, _) in enumerate(B.MoeRouting._fields_[2:]):
+    r.state = B.MOE_ROUTING_STATE_BUILT
+    for i, name in enumerate(B.MoeRouting.pointer_fields()):
         setattr(r, name, 0x10000000 + 0x1000 * i)
     return r
 
@@ -144,7 +145,8 @@ def test_routing_init_layout():
     base = 0x7f0000000000
     assert B.lib().moe_routing_init(D, 4000, B.MOE_ROUTING_SCORES_T, base, nbytes, ctypes.byref(r)) == 0
     assert r.words == 16 and r.capacity == 4000 and r.logits is None and r.scores_t
-    ptrs = sorted(getattr(r, f) for f, _ in B.MoeRouting._fields_[2:] if getattr(r, f))
+    assert r.state == B.MOE_ROUTING_STATE_EMPTY
+    ptrs = sorted(getattr(r, f) for f in B.MoeRouting.pointer_fields() if getattr(r, f))
     assert all(p % 256 == 0 for p in ptrs)
     assert ptrs[0] >= base and ptrs[-1] < base + nbytes
     assert B.lib().moe_routing_init(D, 4000, 0, base, 10, ctypes.byref(r)) == B.MOE_ERR_INVALID_ARG
@@ -154,3 +156,44 @@ def test_routing_init_layout():
 def test_prof_select_validation():
     assert B.lib().moe_prof_select(99) == B.MOE_ERR_INVALID_ARG
     assert B.lib().moe_prof_select(-1) == 0
+
+
+def test_consumers_need_a_built_routing():
+    """moe_fwd and moe_bwd refuse a routing whose metadata was never written
+    (fresh from moe_routing_init) or stops at the counts
+    (MOE_ROUTE_COUNTS_ONLY); moe_round_tokens needs at least the counts."""
+    D = B.dims(256, 128, 64, 8, 2)
+    L = B.lib()
+    a = 0x100000
+    need = B.moe_workspace_bytes(D, 512, B.MOE_WS_FWD)
+    needb = B.moe_workspace_bytes(D, 512, B.MOE_WS_BWD)
+    for state in (B.MOE_ROUTING_STATE_EMPTY, B.MOE_ROUTING_STATE_COUNTS):
+        r = _fake_routing(D, 512)
+        r.state = state
+        assert L.moe_fwd(D, a, a, a, ctypes.byref(r), a, a, a, need, None) == B.MOE_ERR_INVALID_ARG
+        assert "not a complete routing" in B.moe_last_error()
+        args = [D, a, a, a, a, a, a, ctypes.byref(r), a, a, a, a, a, a, a, needb, None]
+        assert L.moe_bwd(*args) == B.MOE_ERR_INVALID_ARG
+        assert "not a complete routing" in B.moe_last_error()
+    tc = _fake_routing(D, 512)
+    tc.state = B.MOE_ROUTING_STATE_EMPTY
+    tr = _fake_routing(D, B.moe_round_capacity(D, 16))
+    assert L.moe_round_tokens(D, 16, 0, None, ctypes.byref(tc), ctypes.byref(tr), None) == B.MOE_ERR_INVALID_ARG
+    assert "counts" in B.moe_last_error()
+
+
+@pytest.mark.parametrize("m_tile", [0, 1, 4, 12, 24, 100, 512, 65536])
+def test_m_tile_must_be_power_of_two_in_range(m_tile):
+    """m_tile is a power of two in [8, 256], as the header states."""
+    D = B.dims(256, 128, 64, 8, 2)
+    assert B.moe_round_capacity(D, m_tile) == -1
+    tc = _fake_routing(D, 512)
+    tr = _fake_routing(D, 256 * 8)
+    rc = B.lib().moe_round_tokens(D, m_tile, 0, None, ctypes.byref(tc), ctypes.byref(tr), None)
+    assert rc == B.MOE_ERR_INVALID_ARG and "power of two" in B.moe_last_error()
+
+
+@pytest.mark.parametrize("m_tile", [8, 16, 32, 64, 128, 256])
+def test_m_tile_accepted(m_tile):
+    D = B.dims(256, 128, 64, 8, 2)
+    assert B.moe_round_capacity(D, m_tile) == min(256 * 8, 256 * 2 + 8 * (m_tile - 1))

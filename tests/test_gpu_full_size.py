@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import oracle
-from dense_reference import rel_err
+from dense_reference import rel_err, rel_fro
 from paper_2512_14080_amd import workloads as W
 from test_gpu_parity import TOL, check_routing, oracle_routing, oracle_scores
 
@@ -41,20 +41,24 @@ def _full_size(name, mode="nearest"):
     X, W1, W2, Wr, dO = (inp.f32(k) for k in ("X", "W1", "W2", "Wr", "dO"))
     fw = oracle.forward(X, W1, W2, R)
     P = R.P
-    errs = {"O": rel_err(layer.O.float().cpu().numpy(), fw["O"]),
-            "H": rel_err(layer.H[:P].float().cpu().numpy(), fw["H"])}
+    errs, fro = {}, {}
+
+    def cmp(k, got, ref):
+        errs[k] = rel_err(got, ref)
+        fro[k] = rel_fro(got, ref)
+
+    cmp("O", layer.O.float().cpu().numpy(), fw["O"])
+    cmp("H", layer.H[:P].float().cpu().numpy(), fw["H"])
     bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R)
     del fw
-    errs.update({
-        "dX": rel_err(layer.dX.float().cpu().numpy(), bw["dX"]),
-        "dW1": rel_err(layer.dW1.float().cpu().numpy(), bw["dW1"]),
-        "dW2": rel_err(layer.dW2.float().cpu().numpy(), bw["dW2"]),
-        "dWr": rel_err(layer.dWr.cpu().numpy(), bw["dWr"]),
-        "dS": rel_err(layer.dS[:P].cpu().numpy(), bw["dS"]),
-        "dbias": rel_err(layer.dbias.cpu().numpy(), bw["dbias"]),
-    })
-    print(f"{name} full-size errors", {k: f"{v:.2e}" for k, v in errs.items()}, f"after {time.time() - t0:.1f}s",
-          flush=True)
+    cmp("dX", layer.dX.float().cpu().numpy(), bw["dX"])
+    cmp("dW1", layer.dW1.float().cpu().numpy(), bw["dW1"])
+    cmp("dW2", layer.dW2.float().cpu().numpy(), bw["dW2"])
+    cmp("dWr", layer.dWr.cpu().numpy(), bw["dWr"])
+    cmp("dS", layer.dS[:P].cpu().numpy(), bw["dS"])
+    cmp("dbias", layer.dbias.cpu().numpy(), bw["dbias"])
+    print(f"{name} {mode} full-size errors, max-normalised", {k: f"{v:.2e}" for k, v in errs.items()},
+          "Frobenius", {k: f"{v:.2e}" for k, v in fro.items()}, f"after {time.time() - t0:.1f}s", flush=True)
     for k, v in errs.items():
         assert v <= TOL, (k, v, errs)
     return inp, L, S
@@ -79,6 +83,13 @@ def test_other_configs_full_size(name):
     shape (T=32768, d=2048, n=128, E=256, K=8, Zipf(1.1) expert popularity),
     token rounding with M_tile=128, every element against the oracle."""
     _full_size(name)
+
+
+@pytest.mark.parametrize("name", ["1b", "7b"])
+def test_token_choice_full_size(name):
+    """Token-choice routing without rounding (ragged expert counts) at the
+    full 1B and 7B shapes, every element against the oracle."""
+    _full_size(name, mode=None)
 
 
 def test_coarse_sampled():

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 
 import oracle
-from dense_reference import rel_err
+from dense_reference import rel_err, rel_fro
 from paper_2512_14080_amd import workloads as W
 
 pytestmark = pytest.mark.gpu
@@ -69,6 +69,8 @@ def check_routing(layer, R, idx=None, rdir=None):
         np.testing.assert_array_equal(tc["topk_idx"], idx)
     if rdir is not None:
         np.testing.assert_array_equal(a["round_dir"], rdir)
+    # the metadata kernels found a consistent selection
+    assert int(a["status"][0]) == 0
 
 
 def run_layer(cfg, seed=0, T=None, round_mode=None, u=None, router_grad=True, bias=None):
@@ -101,7 +103,9 @@ def check_layer(cfg, seed=0, T=None, round_mode=None, u=None, bias=None):
     ref = {"O": fw["O"], "H": fw["H"], "dX": bw["dX"], "dW1": bw["dW1"], "dW2": bw["dW2"],
            "dWr": bw["dWr"], "dbias": bw["dbias"], "dS": bw["dS"]}
     errs = {k: rel_err(got[k], ref[k]) for k in ref}
-    print(cfg.name, T, round_mode, {k: f"{v:.2e}" for k, v in errs.items()}, flush=True)
+    fro = {k: rel_fro(got[k], ref[k]) for k in ref}
+    print(cfg.name, T, round_mode, "max-normalised", {k: f"{v:.2e}" for k, v in errs.items()},
+          "Frobenius", {k: f"{v:.2e}" for k, v in fro.items()}, flush=True)
     for k, v in errs.items():
         assert v <= TOL, (k, v, errs)
     return layer, R
@@ -279,3 +283,65 @@ def test_routing_with_nonfinite_scores():
         rt, re_ = a["row_token"][:P], a["row_expert"][:P]
         assert ((rt >= 0) & (rt < cfg.T)).all() and ((re_ >= 0) & (re_ < cfg.E)).all()
         assert sorted(a["tok_rows"][:P].tolist()) == list(range(P))
+
+
+# Shapes at the limits the ABI accepts (E <= 4096, K <= 16) and the
+# wave-per-token top-K instantiations behind them: values per lane EPL =
+# ceil(E / 64) of 4 (E = 256), 16 (E = 1024), 64 (E = 2056 and 4096: lane
+# values 32 .. 63 exercise the upper half of the selection mask).
+@pytest.mark.parametrize("E,K", [(256, 16), (1024, 8), (2056, 16), (4096, 16)])
+def test_wide_expert_counts_route(E, K):
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    cfg = W.MoEConfig(f"e{E}k{K}", T=700, d=128, n=64, E=E, K=K, m_tile=16)
+    inp = W.make_inputs(cfg, 21)
+    _, S = oracle_scores(inp)
+    for mode in (None, "nearest"):
+        layer = DeviceLayer(inp, round_mode=mode, scores_in=S)
+        layer.route()
+        torch.cuda.synchronize()
+        idx, rdir, R = oracle_routing(S, K, mode, cfg.m_tile)
+        check_routing(layer, R, idx, rdir)
+
+
+@pytest.mark.parametrize("E,K", [(256, 16), (1024, 8)])
+def test_wide_expert_counts_layer(E, K):
+    """The whole layer on the K = 16 / E = 256 shape of the paper's finest
+    30B and 120B benchmark layers, and at E = 1024, at reduced T and d."""
+    check_layer(W.MoEConfig(f"l{E}k{K}", T=600, d=128, n=64, E=E, K=K, m_tile=16), seed=22)
+    check_layer(W.MoEConfig(f"l{E}k{K}", T=600, d=128, n=64, E=E, K=K, m_tile=16), seed=23, round_mode="nearest")
+
+
+@pytest.mark.parametrize("mode", ["balance", "stochastic"])
+def test_sequential_rounding_modes_many_experts(mode):
+    """Balance-f carries its running residual over all experts in order; SR-f
+    draws per expert.  Both at E = 128 and T = 32768 (the 7B routing shape),
+    route only, bit-exact."""
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    cfg = W.MoEConfig("seq", T=32768, d=128, n=64, E=128, K=8, m_tile=128)
+    inp = W.make_inputs(cfg, 24)
+    _, S = oracle_scores(inp)
+    u = np.random.default_rng(25).random(cfg.E).astype(np.float32) if mode == "stochastic" else None
+    layer = DeviceLayer(inp, round_mode=mode, scores_in=S, u=u)
+    layer.route()
+    torch.cuda.synchronize()
+    idx, rdir, R = oracle_routing(S, cfg.K, mode, cfg.m_tile, u)
+    check_routing(layer, R, idx, rdir)
+    assert (R.counts % cfg.m_tile == 0).all()
+
+
+def test_routing_beyond_word_scan_limit():
+    """T > 262144 (more than 4096 bitmap words): the rounded routing's
+    placement takes its word bases from a separate scan kernel."""
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    cfg = W.MoEConfig("long", T=270000, d=128, n=64, E=8, K=2, m_tile=128)
+    inp = W.make_inputs(cfg, 26)
+    _, S = oracle_scores(inp)
+    for mode in (None, "nearest"):
+        layer = DeviceLayer(inp, round_mode=mode, scores_in=S)
+        layer.route()
+        torch.cuda.synchronize()
+        idx, rdir, R = oracle_routing(S, cfg.K, mode, cfg.m_tile)
+        check_routing(layer, R, idx, rdir)

@@ -149,11 +149,86 @@ def test_fp32_oracle_close_to_fp64():
     assert rel_err(f32["O"], f64["O"]) < 1e-5
 
 
-def test_cached_bytes_is_X_plus_H():
-    T, d, n, K = 128, 64, 32, 4
-    P = T * K
-    # bf16 X [T,d] and H [P,2n]: two bytes per element
-    assert oracle.cached_bytes(T, d, n, P) == 2 * (T * d) + 2 * (P * 2 * n)
+def test_cached_bytes_equals_the_arrays_backward_consumes():
+    """The bytes are those of the activations the oracle's backward takes
+    (X and the forward's H), stored as bf16 (2-byte) arrays: measured with
+    nbytes on the arrays themselves, not from a formula."""
+    X, Wr, W1, W2, dO, b = _case(71, 40, 16, 8, 6, 3)
+    R, fw, _ = _run_oracle(X, Wr, W1, W2, dO, b, 3)
+    as_bf16 = lambda a: np.zeros(a.shape, np.uint16)  # noqa: E731  (2 bytes per element)
+    T, d = X.shape
+    n = W2.shape[1]
+    assert oracle.cached_bytes(T, d, n, R.P) == as_bf16(X).nbytes + as_bf16(fw["H"]).nbytes
+
+
+def test_cached_bytes_is_a_dense_models_and_granularity_free():
+    """Section 3.2: the cache equals a dense SwiGLU FFN's with the same
+    activated parameters (intermediate width nK: X [T,d] and H [T,2nK] in
+    bf16) and so does not change with granularity at fixed nK.  At the 7B
+    shape (T=32768, d=1536, n=256, K=8) that is 100663296 + 268435456 bytes."""
+    T, d = 32768, 1536
+    dense = np.zeros((T, d), np.uint16).nbytes + np.zeros((T, 2 * 2048), np.uint16).nbytes
+    for n, K in ((256, 8), (512, 4), (1024, 2), (128, 16)):
+        assert oracle.cached_bytes(T, d, n, T * K) == dense
+    assert dense == 100663296 + 268435456
+
+
+@pytest.mark.parametrize("seed,round_mode", [(81, None), (82, "nearest")])
+def test_expert_biases_against_dense_autograd(seed, round_mode):
+    """Expert biases b1 (up-projection) and b2 (down-projection): O, every
+    gradient, db1, db2 and dS (now <dA', A> + <dO, b2_e>) equal the dense
+    masked autograd reference."""
+    X, Wr, W1, W2, dO, b = _case(seed, 36, 8, 4, 5, 2, bias=True)
+    rng = np.random.default_rng(seed + 100)
+    b1 = rng.standard_normal((5, 8)) * 0.4
+    b2 = rng.standard_normal((5, 8)) * 0.4
+    S, idx, R = oracle.route(X, Wr, 2, bias=b, dtype=F64)
+    if round_mode:
+        member, _, _ = oracle.round_tokens(S, R.member, 4, mode=round_mode)
+        R = oracle.routing_from_membership(member, S, dtype=F64)
+    fw = oracle.forward(X, W1, W2, R, dtype=F64, b1=b1, b2=b2)
+    bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R, dtype=F64, b2=b2)
+    ref = dense_moe(X, Wr, W1, W2, R.member, dO, bias=b, b1=b1, b2=b2)
+    for k, got in (("O", fw["O"]), ("dX", bw["dX"]), ("dW1", bw["dW1"]), ("dW2", bw["dW2"]),
+                   ("dWr", bw["dWr"]), ("dbias", bw["dbias"]), ("db1", bw["db1"]), ("db2", bw["db2"])):
+        np.testing.assert_allclose(got, ref[k], rtol=1e-10, atol=1e-12, err_msg=k)
+    np.testing.assert_allclose(bw["dS"], ref["dS"][R.row_token, R.row_expert], rtol=1e-10, atol=1e-12)
+    # the identity extended: dS = <dO_t, Y_{e,t}> with the biased Y
+    np.testing.assert_allclose(bw["dS"], (dO[R.row_token] * fw["Y"]).sum(axis=1), rtol=1e-10, atol=1e-12)
+    # without b2 in the backward the bias term is missing: the pin sees it
+    bw0 = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R, dtype=F64)
+    assert np.abs(bw0["dS"] - bw["dS"]).max() > 1e-3
+
+
+def test_expert_bias_finite_differences():
+    X, Wr, W1, W2, dO, b = _case(91, 16, 8, 4, 4, 2, bias=True)
+    rng = np.random.default_rng(5)
+    b1 = rng.standard_normal((4, 8)) * 0.4
+    b2 = rng.standard_normal((4, 8)) * 0.4
+    S, idx, R = oracle.route(X, Wr, 2, bias=b, dtype=F64)
+    member = R.member
+
+    def loss(b1_, b2_, Wr_):
+        S_ = oracle.softmax_scores(oracle.router_logits(X, Wr_, b, F64))
+        R_ = oracle.routing_from_membership(member, S_, dtype=F64)
+        return float((oracle.forward(X, W1, W2, R_, dtype=F64, b1=b1_, b2=b2_)["O"] * dO).sum())
+
+    fw = oracle.forward(X, W1, W2, R, dtype=F64, b1=b1, b2=b2)
+    bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R, dtype=F64, b2=b2)
+    h = 1e-6
+    for name in ("b1", "b2", "Wr"):
+        P = {"b1": b1, "b2": b2, "Wr": Wr}[name]
+        g = {"b1": bw["db1"], "b2": bw["db2"], "Wr": bw["dWr"]}[name]
+        for i in [tuple(rng.integers(0, s) for s in P.shape) for _ in range(6)]:
+            args_p = {"b1_": b1, "b2_": b2, "Wr_": Wr}
+            args_m = dict(args_p)
+            Pp, Pm = P.copy(), P.copy()
+            Pp[i] += h
+            Pm[i] -= h
+            args_p[name + "_"] = Pp
+            args_m[name + "_"] = Pm
+            fd = (loss(**args_p) - loss(**args_m)) / (2 * h)
+            assert abs(fd - g[i]) < 1e-6 * max(1.0, abs(fd)), (name, i, fd, g[i])
 
 
 def test_weight_grad_columns_match_dense_autograd():
