@@ -388,8 +388,9 @@ def measure(args, cfg, cpu):
 
 
 def ablation(args):
-    """Evidence for two design choices at the layer's shape (one JSON line each, not the benchmark record):
-    the fused top-K router kernel against softmax + top-K in torch on the same logits, and the gathered inputs
+    """Evidence for three design choices at the layer's shape (one JSON line each, not the benchmark record):
+    gather-and-sum aggregation against a scatter-fused store + contiguous sum and fp32 atomics, the fused top-K
+    router kernel against softmax + top-K in torch on the same logits, and the gathered inputs
     of up-proj, dH and dW1 against the same GEMMs on inputs already laid out per expert (a token-per-row layer
     with K = 1 whose tokens come sorted by expert, so every gather index is the identity)."""
     import numpy as np
@@ -417,7 +418,32 @@ def ablation(args):
         layer.step()
     P = layer.rows()
     gathered = class_ms(layer, ["topk", "up_proj", "dH", "dW1"])
-    del layer
+
+    # expert-aggregation strategies: down-projection epilogue + aggregation kernel(s) per forward
+    from paper_2512_14080_amd.layer import _aligned_empty
+    ws = _aligned_empty(B.moe_workspace_bytes(layer.D, layer.routing.capacity, B.MOE_WS_FWD_AGG_ABLATION))
+    O = torch.empty_like(layer.O)
+    agg = {}
+    for name in B.AGG_STRATEGIES:
+        def fwd():
+            B.moe_fwd_aggregation_ablation(layer.D, layer.X, layer.W1, layer.W2, layer.routing, layer.H, O, name, ws)
+        for _ in range(3):
+            fwd()
+        t = {}
+        for c in ("down_proj", "aggregate_O"):
+            B.moe_prof_select(c)
+            for _ in range(10):
+                fwd()
+            ms, nl = B.moe_prof_read()
+            t[c] = ms / nl
+        B.moe_prof_select(-1)
+        agg[name] = {"down_ms": round(t["down_proj"], 5), "aggregation_ms": round(t["aggregate_O"], 5),
+                     "total_ms": round(t["down_proj"] + t["aggregate_O"], 5)}
+    print(json.dumps({"ablation": "expert aggregation", "workload": f"{cfg.name}: P={P} rows, d={cfg.d}",
+                      "strategies": agg,
+                      "note": "down_ms of scatter_sum includes the slot-map launch, of atomic_f32 the fp32 fill; "
+                              "aggregation_ms of atomic_f32 is the fp32 -> bf16 conversion"}), flush=True)
+    del ws, O, layer
     torch.cuda.empty_cache()
 
     g = torch.Generator(device="cuda").manual_seed(0)

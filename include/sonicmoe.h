@@ -194,23 +194,46 @@ enum {
 int moe_round_tokens(moe_dims dims, int32_t m_tile, int mode, const float *u, const moe_routing *tc,
                      moe_routing *tr, void *stream);
 
-/* Workspace bytes for moe_fwd (which = 1) and moe_bwd (which = 2). */
-enum { MOE_WS_FWD = 1, MOE_WS_BWD = 2 };
+/*
+ * Optional per-expert biases of the two projections (the expert-bias footnote
+ * of the "Gradient computation" appendix).  With them the expert computes
+ *   h = x W1_e + b1_e,  y = SwiGLU(h) W2_e + b2_e,
+ * and the score gradient dS_{t,e} = <dO_t, y> becomes <dA', A> + <dO_t, b2_e>.
+ * Every pointer is a device pointer, fp32, 16-byte aligned, and nullable:
+ *   b1   [E,2n] up-projection bias (gate columns first, as W1)
+ *   b2   [E,d]  down-projection bias
+ *   db1  [E,2n] out of moe_bwd: column sums of dH over the expert's rows
+ *   db2  [E,d]  out of moe_bwd: column sums of s * dO_t over the expert's rows
+ * Experts without rows get zero bias gradients.  moe_fwd reads b1 and b2;
+ * moe_bwd reads b2 (for dS) and writes db1 and db2 where they are given.
+ */
+typedef struct {
+  const float *b1;
+  const float *b2;
+  float *db1;
+  float *db2;
+} moe_expert_bias;
+
+/* Workspace bytes for moe_fwd (which = 1), moe_bwd (which = 2) and
+ * moe_fwd_aggregation_ablation (which = 3). */
+enum { MOE_WS_FWD = 1, MOE_WS_BWD = 2, MOE_WS_FWD_AGG_ABLATION = 3 };
 size_t moe_workspace_bytes(moe_dims dims, int32_t capacity, int which);
 
 /*
  * Forward (Section 3, forward algorithm: up-proj A kernel, down-proj Y kernel,
  * expert aggregation O kernel):
- *   H = gather(X) W1_e            -> H [capacity,2n] bf16 (cached for backward;
+ *   H = gather(X) W1_e (+ b1_e)   -> H [capacity,2n] bf16 (cached for backward;
  *                                    the first P rows are written)
  *   A = SiLU(H_gate) * H_up       (workspace)
- *   Y = A W2_e                    (workspace)
+ *   Y = A W2_e (+ b2_e)           (workspace)
  *   O_t = sum_{rows of t} s * Y   -> O [T,d] bf16 (zero for a token without experts)
+ *   eb  expert biases, nullable (b1 and b2 are read; see moe_expert_bias)
  *   r   routing in state MOE_ROUTING_STATE_BUILT (otherwise MOE_ERR_INVALID_ARG)
  *   ws  device workspace of moe_workspace_bytes(dims, r->capacity, MOE_WS_FWD)
  */
 int moe_fwd(moe_dims dims, const moe_bf16 *X, const moe_bf16 *W1, const moe_bf16 *W2,
-            const moe_routing *r, moe_bf16 *H, moe_bf16 *O, void *ws, size_t ws_bytes, void *stream);
+            const moe_expert_bias *eb, const moe_routing *r, moe_bf16 *H, moe_bf16 *O, void *ws,
+            size_t ws_bytes, void *stream);
 
 /*
  * Backward (down-projection backward algorithm of Section 3; up-projection
@@ -222,6 +245,8 @@ int moe_fwd(moe_dims dims, const moe_bf16 *X, const moe_bf16 *W1, const moe_bf16
  * where the router gradient on each token's selected set is
  *   dl_j = s_j (dS_j - sum_k s_k dS_k)  (softmax over the selected logits),
  *   dW_r = X^T dL, dbias = column sums of dL.
+ *   eb   expert biases, nullable: b2 adds <dO_t, b2_e> to dS; db1 and db2 are
+ *        written where given (see moe_expert_bias)
  *   r    routing in state MOE_ROUTING_STATE_BUILT (otherwise MOE_ERR_INVALID_ARG)
  *   dO   [T,d] bf16           H [capacity,2n] bf16 from moe_fwd
  *   Wr   [d,E] bf16, nullable: then no router gradient is formed and dX holds
@@ -233,9 +258,29 @@ int moe_fwd(moe_dims dims, const moe_bf16 *X, const moe_bf16 *W1, const moe_bf16
  *   ws   device workspace of moe_workspace_bytes(dims, r->capacity, MOE_WS_BWD)
  */
 int moe_bwd(moe_dims dims, const moe_bf16 *dO, const moe_bf16 *X, const moe_bf16 *H,
-            const moe_bf16 *W1, const moe_bf16 *W2, const moe_bf16 *Wr, const moe_routing *r,
+            const moe_bf16 *W1, const moe_bf16 *W2, const moe_expert_bias *eb, const moe_bf16 *Wr,
+            const moe_routing *r,
             moe_bf16 *dX, moe_bf16 *dW1, moe_bf16 *dW2, float *dWr, float *dbias, float *dS, void *ws,
             size_t ws_bytes, void *stream);
+
+/*
+ * Expert-aggregation ablation (Appendix F.3 and the expert-aggregation
+ * figure of the "Referenced tables" appendix): the forward of moe_fwd with
+ * the down-projection and the aggregation done by one of three strategies.
+ * Not on the layer's path; it exists to measure the choice.
+ *   MOE_AGG_GATHER_SUM   Y stored expert-major, each token gathers and sums
+ *                        its rows (what moe_fwd does; deterministic)
+ *   MOE_AGG_SCATTER_SUM  the down-projection epilogue scatters each Y row to
+ *                        its token-major slot, then a contiguous weighted sum
+ *   MOE_AGG_ATOMIC_F32   the epilogue adds s * bf16(Y) into an fp32 O with
+ *                        atomics (order-dependent rounding), then O -> bf16
+ * No expert biases.  ws: moe_workspace_bytes(dims, r->capacity,
+ * MOE_WS_FWD_AGG_ABLATION) bytes; other arguments as moe_fwd.
+ */
+enum { MOE_AGG_GATHER_SUM = 0, MOE_AGG_SCATTER_SUM = 1, MOE_AGG_ATOMIC_F32 = 2 };
+int moe_fwd_aggregation_ablation(moe_dims dims, const moe_bf16 *X, const moe_bf16 *W1, const moe_bf16 *W2,
+                                 const moe_routing *r, moe_bf16 *H, moe_bf16 *O, int strategy, void *ws,
+                                 size_t ws_bytes, void *stream);
 
 /* Static description of an error code. */
 const char *moe_strerror(int code);

@@ -37,13 +37,16 @@ ROUND_MODES = {"nearest": 0, "up": 1, "down": 2, "balance": 3, "stochastic": 4}
 
 MOE_WS_FWD = 1
 MOE_WS_BWD = 2
+MOE_WS_FWD_AGG_ABLATION = 3
+
+AGG_STRATEGIES = {"gather_sum": 0, "scatter_sum": 1, "atomic_f32": 2}
 
 KERNEL_CLASSES = ["router_gemm", "topk", "routing_meta", "token_round", "up_proj", "down_proj", "aggregate_O",
                   "dH", "dW2", "dXtilde", "dW1", "aggregate_dX", "dWr"]
 
 EXPORTS = ["moe_routing_bytes", "moe_routing_init", "moe_round_capacity", "moe_route", "moe_round_tokens",
            "moe_workspace_bytes", "moe_fwd", "moe_bwd", "moe_strerror", "moe_last_error", "moe_prof_select",
-           "moe_prof_read", "moe_kernel_class_name"]
+           "moe_prof_read", "moe_kernel_class_name", "moe_fwd_aggregation_ablation"]
 
 
 class MoeDims(ctypes.Structure):
@@ -67,6 +70,10 @@ class MoeRouting(ctypes.Structure):
         return [name for name, typ in cls._fields_ if typ is _P]
 
 
+class MoeExpertBias(ctypes.Structure):
+    _fields_ = [("b1", _P), ("b2", _P), ("db1", _P), ("db2", _P)]
+
+
 class MoEError(RuntimeError):
     def __init__(self, fn, code, detail):
         super().__init__(f"{fn} failed with {code}: {detail}")
@@ -85,7 +92,7 @@ def lib():
         raise ImportError(f"{LIB_PATH} is missing: build it with paper_2512_14080_amd.build.build()")
     L = ctypes.CDLL(LIB_PATH)
     sz, i32, vp = ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p
-    D, R = MoeDims, ctypes.POINTER(MoeRouting)
+    D, R, EB = MoeDims, ctypes.POINTER(MoeRouting), ctypes.POINTER(MoeExpertBias)
     sig = {
         "moe_routing_bytes": (sz, [D, i32, ctypes.c_int]),
         "moe_routing_init": (ctypes.c_int, [D, i32, ctypes.c_int, vp, sz, R]),
@@ -93,8 +100,9 @@ def lib():
         "moe_route": (ctypes.c_int, [D, vp, vp, vp, ctypes.c_int, R, vp]),
         "moe_round_tokens": (ctypes.c_int, [D, i32, ctypes.c_int, vp, R, R, vp]),
         "moe_workspace_bytes": (sz, [D, i32, ctypes.c_int]),
-        "moe_fwd": (ctypes.c_int, [D, vp, vp, vp, R, vp, vp, vp, sz, vp]),
-        "moe_bwd": (ctypes.c_int, [D, vp, vp, vp, vp, vp, vp, R, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "moe_fwd": (ctypes.c_int, [D, vp, vp, vp, EB, R, vp, vp, vp, sz, vp]),
+        "moe_bwd": (ctypes.c_int, [D, vp, vp, vp, vp, vp, EB, vp, R, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "moe_fwd_aggregation_ablation": (ctypes.c_int, [D, vp, vp, vp, R, vp, vp, ctypes.c_int, vp, sz, vp]),
         "moe_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "moe_last_error": (ctypes.c_char_p, []),
         "moe_prof_select": (ctypes.c_int, [ctypes.c_int]),
@@ -213,15 +221,33 @@ def moe_round_tokens(D, m_tile, mode, u, tc: Routing, tr: Routing, stream=None):
                                                       ctypes.byref(tr.struct), _stream(stream)))
 
 
-def moe_fwd(D, X, W1, W2, r: Routing, H, O, ws, stream=None):
-    _check("moe_fwd", lib().moe_fwd(D, _ptr(X), _ptr(W1), _ptr(W2), ctypes.byref(r.struct), _ptr(H), _ptr(O),
-                                    _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+def expert_bias(b1=None, b2=None, db1=None, db2=None):
+    """A moe_expert_bias struct from device tensors (or None), or None if all are None."""
+    if b1 is None and b2 is None and db1 is None and db2 is None:
+        return None
+    return MoeExpertBias(*(None if t is None else t.data_ptr() for t in (b1, b2, db1, db2)))
 
 
-def moe_bwd(D, dO, X, H, W1, W2, Wr, r: Routing, dX, dW1, dW2, dWr, dbias, dS, ws, stream=None):
-    _check("moe_bwd", lib().moe_bwd(D, _ptr(dO), _ptr(X), _ptr(H), _ptr(W1), _ptr(W2), _ptr(Wr),
+def _eb(eb):
+    return None if eb is None else ctypes.byref(eb)
+
+
+def moe_fwd(D, X, W1, W2, r: Routing, H, O, ws, stream=None, eb=None):
+    _check("moe_fwd", lib().moe_fwd(D, _ptr(X), _ptr(W1), _ptr(W2), _eb(eb), ctypes.byref(r.struct), _ptr(H),
+                                    _ptr(O), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def moe_bwd(D, dO, X, H, W1, W2, Wr, r: Routing, dX, dW1, dW2, dWr, dbias, dS, ws, stream=None, eb=None):
+    _check("moe_bwd", lib().moe_bwd(D, _ptr(dO), _ptr(X), _ptr(H), _ptr(W1), _ptr(W2), _eb(eb), _ptr(Wr),
                                     ctypes.byref(r.struct), _ptr(dX), _ptr(dW1), _ptr(dW2), _ptr(dWr), _ptr(dbias),
                                     _ptr(dS), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+def moe_fwd_aggregation_ablation(D, X, W1, W2, r: Routing, H, O, strategy, ws, stream=None):
+    if isinstance(strategy, str):
+        strategy = AGG_STRATEGIES[strategy]
+    _check("moe_fwd_aggregation_ablation",
+           lib().moe_fwd_aggregation_ablation(D, _ptr(X), _ptr(W1), _ptr(W2), ctypes.byref(r.struct), _ptr(H),
+                                              _ptr(O), strategy, _ptr(ws), ws.numel() * ws.element_size(),
+                                              _stream(stream)))
 
 
 def moe_prof_select(kernel_class):

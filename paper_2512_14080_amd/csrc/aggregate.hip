@@ -29,7 +29,9 @@ __device__ __forceinline__ float bcast_f(float v, int l) {
 // accumulated, so a lane keeps NC * kAggBatch HBM reads in flight.  Every Y
 // row is read exactly once and O is not read again here: both go through the
 // caches as nontemporal accesses.
-template <int NC>
+// CONTIG (the aggregation ablation's scatter + sum): Y holds the rows in
+// token-major order, so the token's rows are Y[j0 .. j1) themselves.
+template <int NC, bool CONTIG = false>
 __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__ Y, const int32_t* __restrict__ tok_offsets,
                                                     const int32_t* __restrict__ tok_rows, const float* __restrict__ row_w,
                                                     uint16_t* __restrict__ O, int T, int d, int c0) {
@@ -51,7 +53,7 @@ __global__ __launch_bounds__(256) void agg_o_kernel(const uint16_t* __restrict__
     float w[kAggBatch];
 #pragma unroll
     for (int u = 0; u < kAggBatch; ++u) {
-      r[u] = bcast_i(rl, u);
+      r[u] = CONTIG ? min(jb + u, j1 - 1) : bcast_i(rl, u);
       w[u] = bcast_f(wl, u);
     }
     u32x4 v[NC][kAggBatch];
@@ -229,6 +231,82 @@ __global__ __launch_bounds__(128) void colsum_rows_kernel(const uint16_t* __rest
   }
 }
 
+// ---------------------------------------------------------------- expert biases
+// B2s[k][e] = hi(b2[e][k]) and B2s[k][E + e] = bf16(b2[e][k] - hi), hi = the
+// round-to-nearest bf16 of b2[e][k]: the layout of W_r [d][E'] with E' = 2E,
+// so the router GEMM forms dO B2s, i.e. <dO_t, hi_e> and <dO_t, lo_e>.
+__global__ __launch_bounds__(256) void bias_split_kernel(const float* __restrict__ b2, int E, int d,
+                                                         uint16_t* __restrict__ B2s) {
+  const int i = blockIdx.x * 256 + threadIdx.x;  // over d x E, e fastest
+  if (i >= d * E) return;
+  const int k = i / E, e = i % E;
+  const float v = b2[(size_t)e * d + k];
+  const uint16_t hi = f2bf(v);
+  B2s[(size_t)k * 2 * E + e] = hi;
+  B2s[(size_t)k * 2 * E + E + e] = f2bf(v - bf2f(hi));
+}
+
+// One workgroup per (expert, 512-column chunk).  Wave w sums the expert's
+// rows w, w + 4, w + 8, ... (four rows' loads in flight per step), lane l owns
+// columns 8l .. 8l + 7 of the chunk; the four wave sums are added in wave
+// order through LDS, so the result does not depend on timing.
+constexpr int kColsumWaves = 4;
+__global__ __launch_bounds__(64 * kColsumWaves) void expert_colsum_kernel(
+    const uint16_t* __restrict__ src, int64_t ld, int cols, const int32_t* __restrict__ offsets,
+    const int32_t* __restrict__ row_token, const float* __restrict__ row_w, float* __restrict__ out) {
+  __shared__ float red[kColsumWaves][512];
+  const int e = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = lane_id();
+  const int c = blockIdx.y * 512 + lane * 8;
+  const bool live = c < cols;
+  const int r0 = offsets[e], r1 = offsets[e + 1];
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  constexpr int kU = 4;
+  for (int rb = r0 + wave; rb < r1; rb += kColsumWaves * kU) {
+    u32x4 v[kU];
+    float w[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int r = rb + u * kColsumWaves;
+      const bool ok = r < r1 && live;
+      const int g = ok ? (row_token ? row_token[r] : r) : 0;
+      w[u] = ok ? (row_w ? row_w[r] : 1.f) : 0.f;
+      v[u] = ok ? *(const u32x4*)(src + (size_t)g * ld + c) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += w[u] * bf_lo(v[u][q]);
+        acc[2 * q + 1] += w[u] * bf_hi(v[u][q]);
+      }
+  }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) red[wave][lane * 8 + q] = acc[q];
+  __syncthreads();
+  for (int i = threadIdx.x; i < 512; i += 64 * kColsumWaves) {
+    const int cc = blockIdx.y * 512 + i;
+    if (cc >= cols) continue;
+    float t = 0.f;
+#pragma unroll
+    for (int w2 = 0; w2 < kColsumWaves; ++w2) t += red[w2][i];
+    out[(size_t)e * cols + cc] = t;
+  }
+}
+
+hipError_t launch_bias_split(const float* b2, int E, int d, uint16_t* B2s, hipStream_t s) {
+  bias_split_kernel<<<dim3((d * E + 255) / 256), dim3(256), 0, s>>>(b2, E, d, B2s);
+  return hipGetLastError();
+}
+
+hipError_t launch_expert_colsum(const uint16_t* src, int64_t ld, int cols, const int32_t* offsets,
+                                const int32_t* row_token, const float* row_w, int E, float* out, hipStream_t s) {
+  if (cols % 8) return hipErrorInvalidValue;  // 16-byte column groups
+  expert_colsum_kernel<<<dim3(E, (cols + 511) / 512), dim3(64 * kColsumWaves), 0, s>>>(src, ld, cols, offsets,
+                                                                                        row_token, row_w, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s) {
   const dim3 grid((T + 3) / 4), block(256);
   const int nc = (d + 511) / 512;
@@ -238,6 +316,51 @@ hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, in
   else  // rows wider than 1536: 2048-column slices, one launch each
     for (int c0 = 0; c0 < d; c0 += 2048)
       agg_o_kernel<4><<<grid, block, 0, s>>>(Y, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, c0);
+  return hipGetLastError();
+}
+
+hipError_t launch_agg_o_contig(const uint16_t* Yt, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s) {
+  const dim3 grid((T + 3) / 4), block(256);
+  const int nc = (d + 511) / 512;
+  if (nc <= 1) agg_o_kernel<1, true><<<grid, block, 0, s>>>(Yt, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, 0);
+  else if (nc == 2) agg_o_kernel<2, true><<<grid, block, 0, s>>>(Yt, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, 0);
+  else if (nc == 3) agg_o_kernel<3, true><<<grid, block, 0, s>>>(Yt, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, 0);
+  else
+    for (int c0 = 0; c0 < d; c0 += 2048)
+      agg_o_kernel<4, true><<<grid, block, 0, s>>>(Yt, r.tok_offsets, r.tok_rows, r.row_w, O, T, d, c0);
+  return hipGetLastError();
+}
+
+// dst[tok_rows[j]] = j for the j < tok_offsets[T] (token-major slot of each row)
+__global__ __launch_bounds__(256) void tok_slots_kernel(const int32_t* __restrict__ tok_offsets,
+                                                        const int32_t* __restrict__ tok_rows, int T, int n,
+                                                        int32_t* __restrict__ dst) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < n && j < tok_offsets[T]) dst[tok_rows[j]] = j;
+}
+
+__global__ __launch_bounds__(256) void fill_f32_kernel(float* __restrict__ p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) p[i] = 0.f;
+}
+
+__global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ in, uint16_t* __restrict__ out,
+                                                          size_t n) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) out[i] = f2bf(in[i]);
+}
+
+hipError_t launch_tok_slots(const moe_routing& r, int T, int P_bound, int32_t* dst, hipStream_t s) {
+  if (P_bound > 0) tok_slots_kernel<<<dim3((P_bound + 255) / 256), dim3(256), 0, s>>>(r.tok_offsets, r.tok_rows, T,
+                                                                                     P_bound, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* p, size_t n, hipStream_t s) {
+  fill_f32_kernel<<<dim3(2048), dim3(256), 0, s>>>(p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_f32_to_bf16(const float* in, uint16_t* out, size_t n, hipStream_t s) {
+  f32_to_bf16_kernel<<<dim3(2048), dim3(256), 0, s>>>(in, out, n);
   return hipGetLastError();
 }
 

@@ -446,6 +446,23 @@ struct ColOffset {
   __device__ __forceinline__ int operator()(int c) const { return c0 + c; }
 };
 
+// Adds bias[colmap(c)] to every accumulator of tile-local column c (the
+// expert biases of the projections).  A lane's accumulator block (j, g) holds
+// four consecutive columns, which colmap keeps consecutive.
+template <class Cfg, class ColMap>
+__device__ __forceinline__ void add_col_bias(Acc<Cfg>& t, const float* bias, ColMap colmap) {
+#pragma unroll
+  for (int j = 0; j < Cfg::RN; ++j)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 b = *(const f32x4*)(bias + colmap(t.n_of(j, g)));
+#pragma unroll
+      for (int i = 0; i < Cfg::RM; ++i)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) t.acc[i][j][4 * g + r] += b[r];
+    }
+}
+
 // ================================================================== router
 template <class Cfg_>
 struct OpRouter {
@@ -584,6 +601,23 @@ __device__ __forceinline__ void store_staged32(const char* wl, uint16_t* blk, in
   asm volatile("" ::: "memory");  // and precede the next writes to the area
 }
 
+// The same with every row sent to its own destination row dst[R] of out
+// (columns col .. col + 63): the scatter-fused store of the aggregation
+// ablation.
+__device__ __forceinline__ void store_staged32_scatter(const char* wl, uint16_t* out, int64_t ld, int col,
+                                                       const int32_t* dst, int rows_valid) {
+  asm volatile("" ::: "memory");
+  const int lane = epilogue_lane();
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int R = 8 * t + (lane >> 3), C = lane & 7;
+    const u32x4 x = *(const u32x4*)(wl + R * 128 + ((C ^ ((R >> 1) & 7)) << 4));
+    if (R < rows_valid)
+      __builtin_nontemporal_store(x, (u32x4*)(out + (size_t)dst[R] * ld + col + 8 * C));
+  }
+  asm volatile("" ::: "memory");
+}
+
 // The same for an output whose first block is held in a 2 KB half-row area
 // (32 rows x 64 bytes, chunk c of row r at r * 64 + ((c ^ ((r >> 1) & 3)) <<
 // 4)) and whose second block is in chunks 4..7 of a 4 KB area as above.
@@ -704,6 +738,7 @@ struct OpUp {
     const int n = p.a.n;
     const int j0 = (ti.n0 / Cfg::BN) * (Cfg::BN / 2);
     const int wn = t.wave_n();
+    if (p.a.b1) add_col_bias<Cfg>(t, p.a.b1 + (size_t)ti.e * (2 * n), ColMap{j0, n});
     if constexpr (STAGED) {
       char* wl = epi + (threadIdx.x >> 6) * kStageBytesPerWave;
       const int wm0 = t.m_of(0) - (threadIdx.x & 31);
@@ -830,7 +865,14 @@ __device__ __forceinline__ void store_rows_bf16_any(uint16_t* out, int64_t ld, i
 }
 
 // ================================================================== down-proj
-template <class Cfg_>
+// AGG selects how Y meets the aggregation (the paper's comparison of
+// expert-aggregation strategies): kAggGather stores Y expert-major for the
+// gather-and-sum O kernel (the layer's path); kAggScatter stores each row at
+// its token-major position (a.dst[row]) for a contiguous sum; kAggAtomic adds
+// s * Y into an fp32 O with atomics (a.O32, a.row_token, a.row_w) and
+// stores no Y.  The last two exist for the ablation only.
+enum { kAggGather = 0, kAggScatter = 1, kAggAtomic = 2 };
+template <class Cfg_, int AGG = kAggGather>
 struct OpDown {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
@@ -854,7 +896,53 @@ struct OpDown {
     s.init(w, p.a.d, nullptr, 0, p.a.n, p.a.d, ColOffset{ti.n0});
   }
   static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* epi) {
-    store_rows_bf16_any<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    if (p.a.b2) add_col_bias<Cfg>(t, p.a.b2 + (size_t)ti.e * p.a.d, ColOffset{ti.n0});
+    if constexpr (AGG == kAggGather) {
+      store_rows_bf16_any<Cfg>(p.a.Y, p.a.d, ti.row_base, ti.mrows, ti.n0, t, epi);
+    } else if constexpr (AGG == kAggScatter) {
+      static_assert(Cfg::RN % 2 == 0 && Cfg::STAGE_BYTES >= Cfg::NW * 4096, "staged rows");
+      char* st = epi - Cfg::STAGE_BYTES + (threadIdx.x >> 6) * 4096;
+      const int wm0 = t.m_of(0) - (threadIdx.x & 31);
+#pragma unroll
+      for (int i = 0; i < Cfg::RM; ++i) {
+        const int m0 = wm0 + 32 * i;
+        if (m0 >= ti.mrows) continue;
+#pragma unroll
+        for (int j = 0; j + 1 < Cfg::RN; j += 2) {
+          u32x2 v0[4], v1[4];
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            v0[g] = pack_bf16x4(t.acc[i][j][4 * g], t.acc[i][j][4 * g + 1], t.acc[i][j][4 * g + 2],
+                                t.acc[i][j][4 * g + 3]);
+            v1[g] = pack_bf16x4(t.acc[i][j + 1][4 * g], t.acc[i][j + 1][4 * g + 1], t.acc[i][j + 1][4 * g + 2],
+                                t.acc[i][j + 1][4 * g + 3]);
+          }
+          const int col = ti.n0 + t.n_of(j, 0) - 4 * ((threadIdx.x >> 5) & 1);
+          stage_block32(st, 0, v0);
+          stage_block32(st, 1, v1);
+          store_staged32_scatter(st, p.a.Y, p.a.d, col, p.a.dst + ti.row_base + m0, ti.mrows - m0);
+        }
+      }
+    } else {
+      // fp32 atomics: O32[t][c] += s * bf16(Y) (Y rounded as the stored Y would be)
+#pragma unroll
+      for (int i = 0; i < Cfg::RM; ++i) {
+        const int m = t.m_of(i);
+        if (m >= ti.mrows) continue;
+        const int row = ti.row_base + m;
+        const float w = p.a.row_w[row];
+        float* o = p.a.O32 + (size_t)p.a.row_token[row] * p.a.d + ti.n0;
+#pragma unroll
+        for (int j = 0; j < Cfg::RN; ++j)
+#pragma unroll
+          for (int g = 0; g < 4; ++g)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float y = bf2f(f2bf(t.acc[i][j][4 * g + r]));
+              unsafeAtomicAdd(o + t.n_of(j, g) + r, w * y);
+            }
+      }
+    }
   }
 };
 
@@ -1021,6 +1109,11 @@ struct OpDH {
 #pragma unroll
       for (int w = 0; w < Cfg::WN; ++w) v += red[m * Cfg::WN + w];
       const size_t row = (size_t)(ti.row_base + m);
+      if (p.a.bq && nt == 0) {
+        // + <dO_t, b2_e> (expert bias of the down-projection), high part then low part
+        const float* q = p.a.bq + (size_t)p.a.row_token[row] * (2 * p.a.E);
+        v += q[ti.e] + q[p.a.E + ti.e];
+      }
       if (nnt == 1)
         p.a.dS[row] = v;
       else
@@ -1223,6 +1316,20 @@ hipError_t launch_up(const UpArgs& a, hipStream_t s) {
 hipError_t launch_down(const DownArgs& a, hipStream_t s) {
   if (a.d % 256 == 0) return run<OpDown<C256x256>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
   return run<OpDown<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 128)), s);
+}
+
+hipError_t launch_down_ablation(const DownArgs& a, int strategy, hipStream_t s) {
+  const int g256 = pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256));
+  const int g128 = pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 128));
+  if (strategy == kAggScatter) {
+    if (a.d % 256 == 0) return run<OpDown<C256x256, kAggScatter>>({a}, g256, s);
+    return run<OpDown<C256x128, kAggScatter>>({a}, g128, s);
+  }
+  if (strategy == kAggAtomic) {
+    if (a.d % 256 == 0) return run<OpDown<C256x256, kAggAtomic>>({a}, g256, s);
+    return run<OpDown<C256x128, kAggAtomic>>({a}, g128, s);
+  }
+  return launch_down(a, s);
 }
 
 static int dh_bn(int n) { return n % 256 == 0 ? 256 : (n % 128 == 0 ? 128 : 64); }

@@ -31,19 +31,31 @@ hipError_t launch_mtiles(const int32_t* offsets, int E, int32_t* out, hipStream_
 struct UpArgs {
   const uint16_t* X; const uint16_t* W1; const int32_t* offsets; const int32_t* row_token;
   uint16_t* H; uint16_t* A; int d, n, E, capacity; const int32_t* mtiles;
+  const float* b1;  // [E,2n] expert bias added to H, or null
 };
 hipError_t launch_up(const UpArgs& a, hipStream_t s);
 
 struct DownArgs {
   const uint16_t* A; const uint16_t* W2; const int32_t* offsets; uint16_t* Y; int d, n, E, capacity;
   const int32_t* mtiles;
+  const float* b2;  // [E,d] expert bias added to Y, or null
+  // aggregation ablation only: token-major destination row of each row
+  // (scatter), or the fp32 output and the row tokens / weights (atomics)
+  const int32_t* dst = nullptr; float* O32 = nullptr; const int32_t* row_token = nullptr;
+  const float* row_w = nullptr;
 };
 hipError_t launch_down(const DownArgs& a, hipStream_t s);
+// strategy 0: as launch_down; 1: Y rows scattered to a.dst[row]; 2: fp32
+// atomic accumulation of s * Y into a.O32 (no Y stored)
+hipError_t launch_down_ablation(const DownArgs& a, int strategy, hipStream_t s);
 
 struct DHArgs {
   const uint16_t* dO; const uint16_t* W2; const uint16_t* H; const int32_t* offsets; const int32_t* row_token;
   const float* row_w; uint16_t* dH; uint16_t* Ap; float* dS; float* dS_part; int d, n, E, capacity;
   const int32_t* mtiles;
+  // <dO_t, b2_e> of the expert-bias dS term as two fp32 halves [T][2E]
+  // (columns e and E + e; see launch_bias_split), or null
+  const float* bq;
 };
 int dh_n_tiles(int n);
 hipError_t launch_dh(const DHArgs& a, hipStream_t s);
@@ -89,8 +101,26 @@ struct DWrArgs {
 int dwr_splits(int T, int d, int E);
 hipError_t launch_dwr(const DWrArgs& a, hipStream_t s);
 
+// Expert biases.  The down-projection bias term of dS, <dO_t, b2_e> for every
+// (t, e), is one GEMM dO [T,d] x B2s [d,2E] on the router GEMM's path: B2s
+// holds b2^T split into bf16 high and low parts (columns e and E + e), whose
+// products with the bf16 dO are exact in the fp32 accumulation, so the term
+// keeps about 16 bits of b2.  launch_bias_split writes B2s.
+hipError_t launch_bias_split(const float* b2, int E, int d, uint16_t* B2s, hipStream_t s);
+// out[e][c] = sum over the rows r of expert e of w_r * src[g(r)][c], with
+// g(r) = row_token[r] (or r when row_token is null) and w_r = row_w[r] (or 1);
+// fixed summation order, fp32.
+hipError_t launch_expert_colsum(const uint16_t* src, int64_t ld, int cols, const int32_t* offsets,
+                                const int32_t* row_token, const float* row_w, int E, float* out, hipStream_t s);
+
 // aggregation and small kernels
 hipError_t launch_agg_o(const uint16_t* Y, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s);
+// aggregation ablation: dst[tok_rows[j]] = j (token-major slot of each row);
+// O from token-major (contiguous) Y rows; fp32 buffer fill and fp32 -> bf16
+hipError_t launch_tok_slots(const moe_routing& r, int T, int P_bound, int32_t* dst, hipStream_t s);
+hipError_t launch_agg_o_contig(const uint16_t* Yt, const moe_routing& r, uint16_t* O, int T, int d, hipStream_t s);
+hipError_t launch_fill_f32(float* p, size_t n, hipStream_t s);
+hipError_t launch_f32_to_bf16(const float* in, uint16_t* out, size_t n, hipStream_t s);
 hipError_t launch_agg_dx(const uint16_t* dXt, const float* dS, const uint16_t* WrT, const moe_routing& r, uint16_t* dX,
                          uint16_t* dL, int T, int d, int E, hipStream_t s);
 hipError_t launch_reduce_rowparts(const float* part, float* out, int rows, int parts, hipStream_t s);

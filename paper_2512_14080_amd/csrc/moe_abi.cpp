@@ -105,6 +105,8 @@ struct BwdWs {
   int32_t* klist2;  // k-chunk lists of the weight gradients
   int32_t* klist1;
   float* dw_part;   // fp32 partials of row-chunked experts
+  uint16_t* b2s;    // expert-bias dS term: b2^T as bf16 high/low parts [d][2E]
+  float* bq;        // and <dO_t, b2_e> in those two parts [T][2E]
 };
 
 size_t carve(char* base, size_t off, size_t bytes, void** out) {
@@ -117,6 +119,15 @@ size_t fwd_layout(const moe_dims& m, int64_t cap, char* base, FwdWs* w) {
   off = carve(base, off, (size_t)cap * m.n * 2, w ? (void**)&w->A : nullptr);
   off = carve(base, off, (size_t)cap * m.d * 2, w ? (void**)&w->Y : nullptr);
   off = carve(base, off, smoe::mtiles_bytes(cap, m.E), w ? (void**)&w->mtiles : nullptr);
+  return off;
+}
+
+// the aggregation ablation: the forward workspace, then the token-major slot
+// of every row and an fp32 O
+size_t abl_layout(const moe_dims& m, int64_t cap, char* base, FwdWs* w, int32_t** dst, float** O32) {
+  size_t off = fwd_layout(m, cap, base, w);
+  off = carve(base, off, (size_t)cap * 4, (void**)dst);
+  off = carve(base, off, (size_t)m.T * m.d * 4, (void**)O32);
   return off;
 }
 
@@ -137,6 +148,8 @@ size_t bwd_layout(const moe_dims& m, int64_t cap, char* base, BwdWs* w) {
   off = carve(base, off, smoe::kchunks_bytes(m.E), w ? (void**)&w->klist2 : nullptr);
   off = carve(base, off, smoe::kchunks_bytes(m.E), w ? (void**)&w->klist1 : nullptr);
   off = carve(base, off, smoe::dw_part_bytes(m.d, m.n), w ? (void**)&w->dw_part : nullptr);
+  off = carve(base, off, (size_t)m.d * 2 * m.E * 2, w ? (void**)&w->b2s : nullptr);
+  off = carve(base, off, (size_t)m.T * 2 * m.E * 4, w ? (void**)&w->bq : nullptr);
   return off;
 }
 
@@ -279,6 +292,11 @@ size_t moe_workspace_bytes(moe_dims dims, int32_t capacity, int which) {
   if (check_dims(dims) != MOE_OK || capacity < 0) return 0;
   if (which == MOE_WS_FWD) return fwd_layout(dims, capacity, nullptr, nullptr);
   if (which == MOE_WS_BWD) return bwd_layout(dims, capacity, nullptr, nullptr);
+  if (which == MOE_WS_FWD_AGG_ABLATION) {
+    int32_t* dst;
+    float* o32;
+    return abl_layout(dims, capacity, nullptr, nullptr, &dst, &o32);
+  }
   return 0;
 }
 
@@ -350,8 +368,17 @@ int moe_round_tokens(moe_dims m, int32_t m_tile, int mode, const float* u, const
   return MOE_OK;
 }
 
-int moe_fwd(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W2, const moe_routing* r, moe_bf16* H,
-            moe_bf16* O, void* ws, size_t ws_bytes, void* stream_) {
+int check_expert_bias(const moe_expert_bias* eb) {
+  if (!eb) return MOE_OK;
+  const void* p[] = {eb->b1, eb->b2, eb->db1, eb->db2};
+  const char* name[] = {"eb->b1", "eb->b2", "eb->db1", "eb->db2"};
+  for (int i = 0; i < 4; ++i)
+    if (p[i] && !aligned(p[i], 16)) return fail(MOE_ERR_INVALID_ARG, "%s must be 16-byte aligned", name[i]);
+  return MOE_OK;
+}
+
+int moe_fwd(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W2, const moe_expert_bias* eb,
+            const moe_routing* r, moe_bf16* H, moe_bf16* O, void* ws, size_t ws_bytes, void* stream_) {
   int rc = check_dims(m);
   if (rc) return rc;
   rc = check_routing(m, r, 1, "r");
@@ -363,6 +390,10 @@ int moe_fwd(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W
   CHECK_PTR(W2, 16);
   CHECK_PTR(H, 16);
   CHECK_PTR(O, 16);
+  rc = check_expert_bias(eb);
+  if (rc) return rc;
+  const float* b1 = eb ? eb->b1 : nullptr;
+  const float* b2 = eb ? eb->b2 : nullptr;
   const size_t need = fwd_layout(m, r->capacity, nullptr, nullptr);
   if (ws_bytes < need) return fail(MOE_ERR_WORKSPACE, "forward workspace %zu < required %zu", ws_bytes, need);
   CHECK_PTR(ws, kAlign);
@@ -371,16 +402,74 @@ int moe_fwd(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W
   hipStream_t stream = (hipStream_t)stream_;
   HIP_TRY(smoe::launch_mtiles(r->offsets, m.E, w.mtiles, stream), "m-tile list");
   LAUNCH(MOE_KC_UP,
-         smoe::launch_up({X, W1, r->offsets, r->row_token, H, w.A, m.d, m.n, m.E, r->capacity, w.mtiles}, stream),
+         smoe::launch_up({X, W1, r->offsets, r->row_token, H, w.A, m.d, m.n, m.E, r->capacity, w.mtiles, b1}, stream),
          "up-proj");
-  LAUNCH(MOE_KC_DOWN, smoe::launch_down({w.A, W2, r->offsets, w.Y, m.d, m.n, m.E, r->capacity, w.mtiles}, stream),
+  LAUNCH(MOE_KC_DOWN, smoe::launch_down({w.A, W2, r->offsets, w.Y, m.d, m.n, m.E, r->capacity, w.mtiles, b2}, stream),
          "down-proj");
   LAUNCH(MOE_KC_AGG_O, smoe::launch_agg_o(w.Y, *r, O, m.T, m.d, stream), "aggregation");
   return MOE_OK;
 }
 
+int moe_fwd_aggregation_ablation(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W2,
+                                 const moe_routing* r, moe_bf16* H, moe_bf16* O, int strategy, void* ws,
+                                 size_t ws_bytes, void* stream_) {
+  int rc = check_dims(m);
+  if (rc) return rc;
+  rc = check_routing(m, r, 1, "r");
+  if (rc) return rc;
+  rc = check_built(r, "r");
+  if (rc) return rc;
+  CHECK_PTR(X, 16);
+  CHECK_PTR(W1, 16);
+  CHECK_PTR(W2, 16);
+  CHECK_PTR(H, 16);
+  CHECK_PTR(O, 16);
+  if (strategy < MOE_AGG_GATHER_SUM || strategy > MOE_AGG_ATOMIC_F32)
+    return fail(MOE_ERR_INVALID_ARG, "unknown aggregation strategy %d", strategy);
+  int32_t* dst = nullptr;
+  float* o32 = nullptr;
+  const size_t need = abl_layout(m, r->capacity, nullptr, nullptr, &dst, &o32);
+  if (ws_bytes < need) return fail(MOE_ERR_WORKSPACE, "ablation workspace %zu < required %zu", ws_bytes, need);
+  CHECK_PTR(ws, kAlign);
+  FwdWs w;
+  abl_layout(m, r->capacity, (char*)ws, &w, &dst, &o32);
+  hipStream_t stream = (hipStream_t)stream_;
+  HIP_TRY(smoe::launch_mtiles(r->offsets, m.E, w.mtiles, stream), "m-tile list");
+  LAUNCH(MOE_KC_UP,
+         smoe::launch_up({X, W1, r->offsets, r->row_token, H, w.A, m.d, m.n, m.E, r->capacity, w.mtiles, nullptr},
+                         stream),
+         "up-proj");
+  smoe::DownArgs da{w.A, W2, r->offsets, w.Y, m.d, m.n, m.E, r->capacity, w.mtiles, nullptr};
+  if (strategy == MOE_AGG_GATHER_SUM) {
+    LAUNCH(MOE_KC_DOWN, smoe::launch_down(da, stream), "down-proj");
+    LAUNCH(MOE_KC_AGG_O, smoe::launch_agg_o(w.Y, *r, O, m.T, m.d, stream), "aggregation");
+  } else if (strategy == MOE_AGG_SCATTER_SUM) {
+    da.dst = dst;
+    LAUNCH(MOE_KC_DOWN,
+           [&]() {
+             hipError_t e = smoe::launch_tok_slots(*r, m.T, r->capacity, dst, stream);
+             return e == hipSuccess ? smoe::launch_down_ablation(da, 1, stream) : e;
+           }(),
+           "down-proj (scatter)");
+    LAUNCH(MOE_KC_AGG_O, smoe::launch_agg_o_contig(w.Y, *r, O, m.T, m.d, stream), "contiguous sum");
+  } else {
+    da.O32 = o32;
+    da.row_token = r->row_token;
+    da.row_w = r->row_w;
+    const size_t td = (size_t)m.T * m.d;
+    LAUNCH(MOE_KC_DOWN,
+           [&]() {
+             hipError_t e = smoe::launch_fill_f32(o32, td, stream);
+             return e == hipSuccess ? smoe::launch_down_ablation(da, 2, stream) : e;
+           }(),
+           "down-proj (fp32 atomics)");
+    LAUNCH(MOE_KC_AGG_O, smoe::launch_f32_to_bf16(o32, O, td, stream), "fp32 -> bf16");
+  }
+  return MOE_OK;
+}
+
 int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H, const moe_bf16* W1,
-            const moe_bf16* W2, const moe_bf16* Wr, const moe_routing* r, moe_bf16* dX, moe_bf16* dW1, moe_bf16* dW2,
+            const moe_bf16* W2, const moe_expert_bias* eb, const moe_bf16* Wr, const moe_routing* r, moe_bf16* dX, moe_bf16* dW1, moe_bf16* dW2,
             float* dWr, float* dbias, float* dS, void* ws, size_t ws_bytes, void* stream_) {
   int rc = check_dims(m);
   if (rc) return rc;
@@ -401,6 +490,9 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   if (dWr && !aligned(dWr, 16)) return fail(MOE_ERR_INVALID_ARG, "dWr must be 16-byte aligned");
   if (dbias && !aligned(dbias, 4)) return fail(MOE_ERR_INVALID_ARG, "dbias must be 4-byte aligned");
   if (dS && !aligned(dS, 4)) return fail(MOE_ERR_INVALID_ARG, "dS must be 4-byte aligned");
+  rc = check_expert_bias(eb);
+  if (rc) return rc;
+  const float* b2 = eb ? eb->b2 : nullptr;
   const size_t need = bwd_layout(m, r->capacity, nullptr, nullptr);
   if (ws_bytes < need) return fail(MOE_ERR_WORKSPACE, "backward workspace %zu < required %zu", ws_bytes, need);
   CHECK_PTR(ws, kAlign);
@@ -412,9 +504,14 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   HIP_TRY(smoe::launch_bwd_lists(r->offsets, m.E, m.d, m.n, w.mtiles, w.klist2, w.klist1, Wr, Wr ? w.WrT : nullptr,
                                  stream),
           "tile lists and W_r transpose");
+  if (b2) {
+    // <dO_t, b2_e> for every (t, e): dO times b2^T split into bf16 high and low parts
+    HIP_TRY(smoe::launch_bias_split(b2, m.E, m.d, w.b2s, stream), "expert-bias split");
+    HIP_TRY(smoe::launch_router_gemm({dO, w.b2s, nullptr, w.bq, m.T, m.d, 2 * m.E}, stream), "expert-bias dS term");
+  }
   LAUNCH(MOE_KC_DH,
          smoe::launch_dh({dO, W2, H, r->offsets, r->row_token, r->row_w, w.dH, w.Ap, dS_out, w.dS_part, m.d, m.n, m.E,
-                          r->capacity, w.mtiles},
+                          r->capacity, w.mtiles, b2 ? w.bq : nullptr},
                          stream),
          "dH");
   if (nnt > 1) HIP_TRY(smoe::launch_reduce_rowparts(w.dS_part, dS_out, r->capacity, nnt, stream), "dS reduce");
@@ -431,6 +528,12 @@ int moe_bwd(moe_dims m, const moe_bf16* dO, const moe_bf16* X, const moe_bf16* H
   HIP_TRY(smoe::launch_bwd_final_reduce(w.klist1, w.dw_part, dW1, m.d, m.n, w.dWr_part, dWr, splits, w.dbias_part,
                                         dbias, m.T, m.E, stream),
           "final reductions (dW1 split experts, dW_r, dbias)");
+  if (eb && eb->db1)
+    HIP_TRY(smoe::launch_expert_colsum(w.dH, 2 * m.n, 2 * m.n, r->offsets, nullptr, nullptr, m.E, eb->db1, stream),
+            "expert-bias gradient db1");
+  if (eb && eb->db2)
+    HIP_TRY(smoe::launch_expert_colsum(dO, m.d, m.d, r->offsets, r->row_token, r->row_w, m.E, eb->db2, stream),
+            "expert-bias gradient db2");
   return MOE_OK;
 }
 

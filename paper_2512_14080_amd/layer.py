@@ -42,7 +42,7 @@ class DeviceLayer:
     """
 
     def __init__(self, inputs, round_mode=None, m_tile=None, scores_in=None, u=None, device="cuda",
-                 router_grad=True):
+                 router_grad=True, b1=None, b2=None):
         import torch
         cfg = inputs.cfg
         T, d, n, E, K = inputs.X.shape[0], cfg.d, cfg.n, cfg.E, cfg.K
@@ -81,6 +81,13 @@ class DeviceLayer:
         self.dWr = torch.empty((d, E), dtype=torch.float32, device=device) if router_grad else None
         self.dbias = torch.empty((E,), dtype=torch.float32, device=device) if router_grad else None
         self.dS = torch.empty((cap,), dtype=torch.float32, device=device)
+        # optional expert biases (fp32 [E,2n] and [E,d]) and their gradients
+        f32 = torch.float32
+        self.b1 = None if b1 is None else torch.from_numpy(np.ascontiguousarray(b1, np.float32)).to(device)
+        self.b2 = None if b2 is None else torch.from_numpy(np.ascontiguousarray(b2, np.float32)).to(device)
+        self.db1 = torch.empty((E, 2 * n), dtype=f32, device=device) if b1 is not None else None
+        self.db2 = torch.empty((E, d), dtype=f32, device=device) if b2 is not None else None
+        self.eb = B.expert_bias(self.b1, self.b2, self.db1, self.db2)
 
     @property
     def routing(self):
@@ -92,11 +99,12 @@ class DeviceLayer:
             B.moe_round_tokens(self.D, self.m_tile, self.round_mode, self.u, self.tc, self.tr, stream)
 
     def forward(self, stream=None):
-        B.moe_fwd(self.D, self.X, self.W1, self.W2, self.routing, self.H, self.O, self.ws_f, stream)
+        B.moe_fwd(self.D, self.X, self.W1, self.W2, self.routing, self.H, self.O, self.ws_f, stream, eb=self.eb)
 
     def backward(self, stream=None):
         B.moe_bwd(self.D, self.dO, self.X, self.H, self.W1, self.W2, self.Wr if self.router_grad else None,
-                  self.routing, self.dX, self.dW1, self.dW2, self.dWr, self.dbias, self.dS, self.ws_b, stream)
+                  self.routing, self.dX, self.dW1, self.dW2, self.dWr, self.dbias, self.dS, self.ws_b, stream,
+                  eb=self.eb)
 
     def step(self, stream=None):
         self.route(stream)

@@ -127,13 +127,13 @@ def test_fwd_bwd_validation():
     r = _fake_routing(D, 512)
     need = B.moe_workspace_bytes(D, 512, B.MOE_WS_FWD)
     a = 0x100000
-    assert L.moe_fwd(D, a, a, a, ctypes.byref(r), a, a, a, need - 1, None) == B.MOE_ERR_WORKSPACE
-    assert L.moe_fwd(D, a, None, a, ctypes.byref(r), a, a, a, need, None) == B.MOE_ERR_INVALID_ARG
-    assert L.moe_fwd(D, a, a, a, ctypes.byref(r), a + 2, a, a, need, None) == B.MOE_ERR_INVALID_ARG
+    assert L.moe_fwd(D, a, a, a, None, ctypes.byref(r), a, a, a, need - 1, None) == B.MOE_ERR_WORKSPACE
+    assert L.moe_fwd(D, a, None, a, None, ctypes.byref(r), a, a, a, need, None) == B.MOE_ERR_INVALID_ARG
+    assert L.moe_fwd(D, a, a, a, None, ctypes.byref(r), a + 2, a, a, need, None) == B.MOE_ERR_INVALID_ARG
     needb = B.moe_workspace_bytes(D, 512, B.MOE_WS_BWD)
-    args = [D, a, a, a, a, a, a, ctypes.byref(r), a, a, a, a, a, a, a, needb - 256, None]
+    args = [D, a, a, a, a, a, None, a, ctypes.byref(r), a, a, a, a, a, a, a, needb - 256, None]
     assert L.moe_bwd(*args) == B.MOE_ERR_WORKSPACE
-    args = [D, a, a, a, a, a, None, ctypes.byref(r), a, a, a, a, None, None, a, needb, None]
+    args = [D, a, a, a, a, a, None, None, ctypes.byref(r), a, a, a, a, None, None, a, needb, None]
     assert L.moe_bwd(*args) == B.MOE_ERR_INVALID_ARG  # dWr without Wr
     assert "Wr" in B.moe_last_error()
 
@@ -170,9 +170,9 @@ def test_consumers_need_a_built_routing():
     for state in (B.MOE_ROUTING_STATE_EMPTY, B.MOE_ROUTING_STATE_COUNTS):
         r = _fake_routing(D, 512)
         r.state = state
-        assert L.moe_fwd(D, a, a, a, ctypes.byref(r), a, a, a, need, None) == B.MOE_ERR_INVALID_ARG
+        assert L.moe_fwd(D, a, a, a, None, ctypes.byref(r), a, a, a, need, None) == B.MOE_ERR_INVALID_ARG
         assert "not a complete routing" in B.moe_last_error()
-        args = [D, a, a, a, a, a, a, ctypes.byref(r), a, a, a, a, a, a, a, needb, None]
+        args = [D, a, a, a, a, a, None, a, ctypes.byref(r), a, a, a, a, a, a, a, needb, None]
         assert L.moe_bwd(*args) == B.MOE_ERR_INVALID_ARG
         assert "not a complete routing" in B.moe_last_error()
     tc = _fake_routing(D, 512)
@@ -197,3 +197,19 @@ def test_m_tile_must_be_power_of_two_in_range(m_tile):
 def test_m_tile_accepted(m_tile):
     D = B.dims(256, 128, 64, 8, 2)
     assert B.moe_round_capacity(D, m_tile) == min(256 * 8, 256 * 2 + 8 * (m_tile - 1))
+
+
+def test_expert_bias_alignment_checked():
+    D = B.dims(256, 128, 64, 8, 2)
+    L = B.lib()
+    r = _fake_routing(D, 512)
+    a = 0x100000
+    need = B.moe_workspace_bytes(D, 512, B.MOE_WS_FWD)
+    eb = B.MoeExpertBias(a + 4, None, None, None)
+    assert L.moe_fwd(D, a, a, a, ctypes.byref(eb), ctypes.byref(r), a, a, a, need, None) == B.MOE_ERR_INVALID_ARG
+    assert "eb->b1" in B.moe_last_error()
+    needb = B.moe_workspace_bytes(D, 512, B.MOE_WS_BWD)
+    eb = B.MoeExpertBias(None, None, None, a + 8)
+    args = [D, a, a, a, a, a, ctypes.byref(eb), a, ctypes.byref(r), a, a, a, a, a, a, a, needb, None]
+    assert L.moe_bwd(*args) == B.MOE_ERR_INVALID_ARG
+    assert "eb->db2" in B.moe_last_error()

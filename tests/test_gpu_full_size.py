@@ -13,12 +13,12 @@ import pytest
 import oracle
 from dense_reference import rel_err, rel_fro
 from paper_2512_14080_amd import workloads as W
-from test_gpu_parity import TOL, check_routing, oracle_routing, oracle_scores
+from test_gpu_parity import TOL, check_routing, expert_biases, oracle_routing, oracle_scores
 
 pytestmark = pytest.mark.gpu
 
 
-def _full_size(name, mode="nearest"):
+def _full_size(name, mode="nearest", biases=False):
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
@@ -27,7 +27,8 @@ def _full_size(name, mode="nearest"):
     t0 = time.time()
     inp = W.make_inputs(cfg, 0)
     L, S = oracle_scores(inp)
-    layer = DeviceLayer(inp, round_mode=mode, scores_in=S)
+    b1, b2 = expert_biases(cfg, 0) if biases else (None, None)
+    layer = DeviceLayer(inp, round_mode=mode, scores_in=S, b1=b1, b2=b2)
     layer.step()
     torch.cuda.synchronize()
     print(f"{name}: device step done after {time.time() - t0:.1f}s", flush=True)
@@ -39,7 +40,7 @@ def _full_size(name, mode="nearest"):
     print(f"{name}: routing exact (P={R.P}) after {time.time() - t0:.1f}s", flush=True)
 
     X, W1, W2, Wr, dO = (inp.f32(k) for k in ("X", "W1", "W2", "Wr", "dO"))
-    fw = oracle.forward(X, W1, W2, R)
+    fw = oracle.forward(X, W1, W2, R, b1=b1, b2=b2)
     P = R.P
     errs, fro = {}, {}
 
@@ -49,8 +50,11 @@ def _full_size(name, mode="nearest"):
 
     cmp("O", layer.O.float().cpu().numpy(), fw["O"])
     cmp("H", layer.H[:P].float().cpu().numpy(), fw["H"])
-    bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R)
+    bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R, b2=b2)
     del fw
+    if biases:
+        cmp("db1", layer.db1.cpu().numpy(), bw["db1"])
+        cmp("db2", layer.db2.cpu().numpy(), bw["db2"])
     cmp("dX", layer.dX.float().cpu().numpy(), bw["dX"])
     cmp("dW1", layer.dW1.float().cpu().numpy(), bw["dW1"])
     cmp("dW2", layer.dW2.float().cpu().numpy(), bw["dW2"])
@@ -90,6 +94,12 @@ def test_token_choice_full_size(name):
     """Token-choice routing without rounding (ragged expert counts) at the
     full 1B and 7B shapes, every element against the oracle."""
     _full_size(name, mode=None)
+
+
+def test_7b_expert_biases_full_size():
+    """The 7B shape with expert biases on both projections (token rounding),
+    every element, db1 and db2 included, against the oracle."""
+    _full_size("7b", biases=True)
 
 
 def test_coarse_sampled():

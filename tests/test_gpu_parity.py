@@ -73,26 +73,36 @@ def check_routing(layer, R, idx=None, rdir=None):
     assert int(a["status"][0]) == 0
 
 
-def run_layer(cfg, seed=0, T=None, round_mode=None, u=None, router_grad=True, bias=None):
+def expert_biases(cfg, seed, scale=0.01):
+    """Seeded fp32 expert biases b1 [E,2n], b2 [E,d] ~ N(0, scale)."""
+    rng = np.random.default_rng(1000 + seed)
+    b1 = (rng.standard_normal((cfg.E, 2 * cfg.n)) * scale).astype(np.float32)
+    b2 = (rng.standard_normal((cfg.E, cfg.d)) * scale).astype(np.float32)
+    return b1, b2
+
+
+def run_layer(cfg, seed=0, T=None, round_mode=None, u=None, router_grad=True, bias=None, eb=None):
     torch = _torch()
     from paper_2512_14080_amd.layer import DeviceLayer
     inp = W.make_inputs(cfg, seed, T=T)
     if bias is not None:
         inp.bias = np.asarray(bias, np.float32)
     _, S = oracle_scores(inp)
-    layer = DeviceLayer(inp, round_mode=round_mode, scores_in=S, u=u, router_grad=router_grad)
+    b1, b2 = eb if eb is not None else (None, None)
+    layer = DeviceLayer(inp, round_mode=round_mode, scores_in=S, u=u, router_grad=router_grad, b1=b1, b2=b2)
     layer.step()
     torch.cuda.synchronize()
     return inp, S, layer
 
 
-def check_layer(cfg, seed=0, T=None, round_mode=None, u=None, bias=None):
-    inp, S, layer = run_layer(cfg, seed, T, round_mode, u, bias=bias)
+def check_layer(cfg, seed=0, T=None, round_mode=None, u=None, bias=None, eb=None):
+    inp, S, layer = run_layer(cfg, seed, T, round_mode, u, bias=bias, eb=eb)
     idx, rdir, R = oracle_routing(S, cfg.K, round_mode, cfg.m_tile, u)
     check_routing(layer, R, idx, rdir)
     X, W1, W2, Wr, dO = (inp.f32(k) for k in ("X", "W1", "W2", "Wr", "dO"))
-    fw = oracle.forward(X, W1, W2, R)
-    bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R)
+    b1, b2 = eb if eb is not None else (None, None)
+    fw = oracle.forward(X, W1, W2, R, b1=b1, b2=b2)
+    bw = oracle.backward(dO, X, fw["H"], W1, W2, Wr, R, b2=b2)
     P = R.P
     got = {
         "O": layer.O.float().cpu().numpy(), "H": layer.H[:P].float().cpu().numpy(),
@@ -102,6 +112,9 @@ def check_layer(cfg, seed=0, T=None, round_mode=None, u=None, bias=None):
     }
     ref = {"O": fw["O"], "H": fw["H"], "dX": bw["dX"], "dW1": bw["dW1"], "dW2": bw["dW2"],
            "dWr": bw["dWr"], "dbias": bw["dbias"], "dS": bw["dS"]}
+    if eb is not None:
+        got["db1"], got["db2"] = layer.db1.cpu().numpy(), layer.db2.cpu().numpy()
+        ref["db1"], ref["db2"] = bw["db1"], bw["db2"]
     errs = {k: rel_err(got[k], ref[k]) for k in ref}
     fro = {k: rel_fro(got[k], ref[k]) for k in ref}
     print(cfg.name, T, round_mode, "max-normalised", {k: f"{v:.2e}" for k, v in errs.items()},
@@ -345,3 +358,38 @@ def test_routing_beyond_word_scan_limit():
         torch.cuda.synchronize()
         idx, rdir, R = oracle_routing(S, cfg.K, mode, cfg.m_tile)
         check_routing(layer, R, idx, rdir)
+
+
+@pytest.mark.parametrize("cfg,mode", [(TINY, None), (TINY, "nearest"), (MID, "nearest"), (ODD, None), (WIDE, None)])
+def test_expert_biases(cfg, mode):
+    """Expert biases b1 (up-projection) and b2 (down-projection): H, O, dS
+    with its <dO_t, b2_e> term, every gradient and db1, db2 against the
+    oracle; WIDE (n = 512) has dS summed over two N tiles."""
+    check_layer(cfg, seed=31, round_mode=mode, eb=expert_biases(cfg, 31))
+
+
+@pytest.mark.parametrize("cfg,mode", [(MID, "nearest"), (ODD, None), (SKEW, None)])
+def test_aggregation_strategy_ablation(cfg, mode):
+    """The expert-aggregation strategies of the ablation entry point: the
+    scatter-fused store + contiguous sum gives O bit for bit equal to
+    gather-and-sum (same bf16 Y rows, same order); fp32 atomics agree with the
+    oracle within the tolerance (their rounding depends on arrival order)."""
+    torch = _torch()
+    from paper_2512_14080_amd import binding as B
+    from paper_2512_14080_amd.layer import _aligned_empty
+    inp, S, layer = run_layer(cfg, seed=41, round_mode=mode)
+    idx, rdir, R = oracle_routing(S, cfg.K, mode, cfg.m_tile)
+    X, W1, W2 = (inp.f32(k) for k in ("X", "W1", "W2"))
+    ref = oracle.forward(X, W1, W2, R)["O"]
+    ws = _aligned_empty(B.moe_workspace_bytes(layer.D, layer.routing.capacity, B.MOE_WS_FWD_AGG_ABLATION))
+    outs = {}
+    for name in ("gather_sum", "scatter_sum", "atomic_f32"):
+        O = torch.empty_like(layer.O)
+        B.moe_fwd_aggregation_ablation(layer.D, layer.X, layer.W1, layer.W2, layer.routing, layer.H, O, name, ws)
+        torch.cuda.synchronize()
+        outs[name] = O
+        err = rel_err(O.float().cpu().numpy(), ref)
+        print(cfg.name, name, f"{err:.2e}", flush=True)
+        assert err <= TOL, (name, err)
+    assert torch.equal(outs["gather_sum"], layer.O)
+    assert torch.equal(outs["scatter_sum"], outs["gather_sum"])
