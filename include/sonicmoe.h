@@ -264,6 +264,24 @@ int moe_bwd(moe_dims dims, const moe_bf16 *dO, const moe_bf16 *X, const moe_bf16
             size_t ws_bytes, void *stream);
 
 /*
+ * moe_fwd for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same forward, with its workspace (A, Y and the m-tile list) in a static
+ * device array of moe_fwd_static_max_bytes() = 64 MiB that the library holds
+ * on every GPU it runs on until the process ends.  No allocation happens in
+ * the call.  A routing whose forward workspace
+ * (moe_workspace_bytes(dims, r->capacity, MOE_WS_FWD)) exceeds the array is
+ * refused with MOE_ERR_WORKSPACE before anything is enqueued.  Every call on
+ * one GPU uses that GPU's one array: calls that overlap on a GPU (on
+ * different streams, or from different threads without ordering) race.  The
+ * array belongs to the current device (hipGetDevice), which must be the
+ * stream's.  Other arguments as moe_fwd.
+ */
+size_t moe_fwd_static_max_bytes(void);
+int moe_fwd_static(moe_dims dims, const moe_bf16 *X, const moe_bf16 *W1, const moe_bf16 *W2,
+                   const moe_expert_bias *eb, const moe_routing *r, moe_bf16 *H, moe_bf16 *O, void *stream);
+
+/*
  * Expert-aggregation ablation (Appendix F.3 and the expert-aggregation
  * figure of the "Referenced tables" appendix): the forward of moe_fwd with
  * the down-projection and the aggregation done by one of three strategies.

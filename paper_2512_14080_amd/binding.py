@@ -46,7 +46,8 @@ KERNEL_CLASSES = ["router_gemm", "topk", "routing_meta", "token_round", "up_proj
 
 EXPORTS = ["moe_routing_bytes", "moe_routing_init", "moe_round_capacity", "moe_route", "moe_round_tokens",
            "moe_workspace_bytes", "moe_fwd", "moe_bwd", "moe_strerror", "moe_last_error", "moe_prof_select",
-           "moe_prof_read", "moe_kernel_class_name", "moe_fwd_aggregation_ablation"]
+           "moe_prof_read", "moe_kernel_class_name", "moe_fwd_aggregation_ablation", "moe_fwd_static",
+           "moe_fwd_static_max_bytes"]
 
 
 class MoeDims(ctypes.Structure):
@@ -103,6 +104,8 @@ def lib():
         "moe_fwd": (ctypes.c_int, [D, vp, vp, vp, EB, R, vp, vp, vp, sz, vp]),
         "moe_bwd": (ctypes.c_int, [D, vp, vp, vp, vp, vp, EB, vp, R, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "moe_fwd_aggregation_ablation": (ctypes.c_int, [D, vp, vp, vp, R, vp, vp, ctypes.c_int, vp, sz, vp]),
+        "moe_fwd_static": (ctypes.c_int, [D, vp, vp, vp, EB, R, vp, vp, vp]),
+        "moe_fwd_static_max_bytes": (sz, []),
         "moe_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "moe_last_error": (ctypes.c_char_p, []),
         "moe_prof_select": (ctypes.c_int, [ctypes.c_int]),
@@ -241,6 +244,11 @@ def moe_bwd(D, dO, X, H, W1, W2, Wr, r: Routing, dX, dW1, dW2, dWr, dbias, dS, w
     _check("moe_bwd", lib().moe_bwd(D, _ptr(dO), _ptr(X), _ptr(H), _ptr(W1), _ptr(W2), _eb(eb), _ptr(Wr),
                                     ctypes.byref(r.struct), _ptr(dX), _ptr(dW1), _ptr(dW2), _ptr(dWr), _ptr(dbias),
                                     _ptr(dS), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+def moe_fwd_static(D, X, W1, W2, r: Routing, H, O, stream=None, eb=None):
+    _check("moe_fwd_static", lib().moe_fwd_static(D, _ptr(X), _ptr(W1), _ptr(W2), _eb(eb), ctypes.byref(r.struct),
+                                                  _ptr(H), _ptr(O), _stream(stream)))
+
+
 def moe_fwd_aggregation_ablation(D, X, W1, W2, r: Routing, H, O, strategy, ws, stream=None):
     if isinstance(strategy, str):
         strategy = AGG_STRATEGIES[strategy]

@@ -79,6 +79,35 @@ int check_built(const moe_routing* r, const char* name) {
 
 bool valid_m_tile(int m) { return m >= 8 && m <= 256 && (m & (m - 1)) == 0; }
 
+// ---------------------------------------------------------------- static workspace
+// The forward workspace of moe_fwd_static: a file-scope device array that
+// each GPU holds from the library's load to the end of the process.  In host
+// code `scratch` only names the host-side stand-in of the symbol; its device
+// address comes from hipGetSymbolAddress, once per device, with that device
+// current, and only that address is ever handed to a kernel.
+constexpr size_t kStaticWsBytes = (size_t)64 << 20;
+static __device__ __align__(256) char scratch[kStaticWsBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int static_ws(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(MOE_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(MOE_ERR_HIP, "hipGetSymbolAddress(scratch) returned null");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return MOE_OK;
+}
+
 // ---------------------------------------------------------------- timing
 std::mutex g_prof_mu;
 int g_prof_class = -1;
@@ -408,6 +437,26 @@ int moe_fwd(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W
          "down-proj");
   LAUNCH(MOE_KC_AGG_O, smoe::launch_agg_o(w.Y, *r, O, m.T, m.d, stream), "aggregation");
   return MOE_OK;
+}
+
+size_t moe_fwd_static_max_bytes(void) { return kStaticWsBytes; }
+
+int moe_fwd_static(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W2, const moe_expert_bias* eb,
+                   const moe_routing* r, moe_bf16* H, moe_bf16* O, void* stream) {
+  int rc = check_dims(m);
+  if (rc) return rc;
+  rc = check_routing(m, r, 1, "r");
+  if (rc) return rc;
+  const size_t need = fwd_layout(m, r->capacity, nullptr, nullptr);
+  if (need > kStaticWsBytes)
+    return fail(MOE_ERR_WORKSPACE,
+                "the forward workspace for capacity %d (%zu bytes) exceeds the static workspace of %zu bytes; "
+                "use moe_fwd with a caller workspace",
+                r->capacity, need, kStaticWsBytes);
+  void* ws = nullptr;
+  rc = static_ws(&ws);
+  if (rc) return rc;
+  return moe_fwd(m, X, W1, W2, eb, r, H, O, ws, kStaticWsBytes, stream);
 }
 
 int moe_fwd_aggregation_ablation(moe_dims m, const moe_bf16* X, const moe_bf16* W1, const moe_bf16* W2,

@@ -213,3 +213,15 @@ def test_expert_bias_alignment_checked():
     args = [D, a, a, a, a, a, ctypes.byref(eb), a, ctypes.byref(r), a, a, a, a, a, a, a, needb, None]
     assert L.moe_bwd(*args) == B.MOE_ERR_INVALID_ARG
     assert "eb->db2" in B.moe_last_error()
+
+
+def test_static_forward_refuses_oversized_workspace():
+    """moe_fwd_static refuses, before any HIP call, a routing whose forward
+    workspace exceeds its static array."""
+    D = B.dims(32768, 1536, 256, 128, 8)
+    r = _fake_routing(D, 32768 * 8)
+    assert B.moe_workspace_bytes(D, r.capacity, B.MOE_WS_FWD) > B.lib().moe_fwd_static_max_bytes()
+    a = 0x100000
+    assert B.lib().moe_fwd_static(D, a, a, a, None, ctypes.byref(r), a, a, None) == B.MOE_ERR_WORKSPACE
+    assert "static workspace" in B.moe_last_error()
+    assert B.lib().moe_fwd_static_max_bytes() == 64 << 20
