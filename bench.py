@@ -24,7 +24,7 @@ if ROOT not in sys.path:
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 FLUSH_BYTES = 512 << 20     # scratch written before each timed step: more than L2 (8 x 4 MB) + Infinity Cache (256 MB)
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_7b_tr128.md")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "l2_fabric_traffic_7b_tr128.md")
 
 # kernel-name fragment -> kernel class (as in the library's timing classes)
 KERNEL_CLASS_OF = [("OpUp<", "up_proj"), ("OpDown<", "down_proj"), ("OpDH<", "dH"), ("OpDW2<", "dW2"),
@@ -66,8 +66,8 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def _pmc_per_dispatch(run_dir, counter):
-    """Mean of a rocprofv3 counter per dispatch, by kernel name (KiB for *_SIZE)."""
+def _pmc_per_dispatch(run_dir, counters):
+    """Mean per dispatch of rocprofv3 counters, by kernel name: {kernel: {counter: value}}."""
     import csv
     import glob
     files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
@@ -77,69 +77,104 @@ def _pmc_per_dispatch(run_dir, counter):
     for f in files:
         with open(f) as fh:
             for r in csv.DictReader(fh):
-                if r["Counter_Name"] != counter:
+                if r["Counter_Name"] not in counters:
                     continue
                 k = r["Kernel_Name"]
-                tot[k] = tot.get(k, 0.0) + float(r["Counter_Value"])
+                d = tot.setdefault(k, {})
+                d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
                 disp.setdefault(k, set()).add(r["Dispatch_Id"])
-    return {k: tot[k] / len(disp[k]) for k in tot}
+    return {k: {c: v / len(disp[k]) for c, v in d.items()} for k, d in tot.items()}
 
 
-def traffic_report(fetch_dir, write_dir, copy_fetch_dir, copy_write_dir, copy_bytes):
-    """Markdown summary of measured HBM traffic per launch and kernel class.
+READ_COUNTERS = ["TCC_EA0_RDREQ", "TCC_EA0_RDREQ_32B", "TCC_EA0_RDREQ_64B", "TCC_EA0_RDREQ_128B"]
+WRITE_COUNTERS = ["TCC_EA0_WRREQ", "TCC_EA0_WRREQ_64B"]
 
-    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are each scaled by what the same
-    counter reads for a plain device copy of copy_bytes (read once, written once)."""
-    cf = _pmc_per_dispatch(copy_fetch_dir, "FETCH_SIZE")
-    cw = _pmc_per_dispatch(copy_write_dir, "WRITE_SIZE")
-    ck = [k for k in cf if "copyBuffer" in k]
+
+def _read_bytes(c):
+    return 32.0 * c.get("TCC_EA0_RDREQ_32B", 0) + 64.0 * c.get("TCC_EA0_RDREQ_64B", 0) + \
+        128.0 * c.get("TCC_EA0_RDREQ_128B", 0)
+
+
+def _write_bytes(c):
+    n, n64 = c.get("TCC_EA0_WRREQ", 0), c.get("TCC_EA0_WRREQ_64B", 0)
+    return 64.0 * n64 + 32.0 * (n - n64)
+
+
+def traffic_report(read_dir, write_dir, copy_read_dir, copy_write_dir, copy_bytes):
+    """Markdown summary of the bytes each kernel class moves between the L2 and the memory fabric per launch.
+
+    Reads are the L2's read requests to the fabric by size (TCC_EA0_RDREQ_32B/_64B/_128B), writes its write
+    requests (TCC_EA0_WRREQ, of which TCC_EA0_WRREQ_64B are 64-byte, the rest 32-byte).  These bytes include
+    Infinity Cache (MALL) hits: the L2 counters cannot tell which requests reach DRAM.  A plain device copy of
+    copy_bytes calibrates the sizes (it should read and write copy_bytes)."""
+    cr = _pmc_per_dispatch(copy_read_dir, READ_COUNTERS)
+    cw = _pmc_per_dispatch(copy_write_dir, WRITE_COUNTERS)
+    ck = [k for k in cr if "copyBuffer" in k or "copy" in k.lower()]
     if not ck:
         raise RuntimeError("no copy kernel in the calibration run")
-    f_scale = copy_bytes / (cf[ck[0]] * 1024.0)
-    w_scale = copy_bytes / (cw[ck[0]] * 1024.0)
-    fetch = _pmc_per_dispatch(fetch_dir, "FETCH_SIZE")
-    write = _pmc_per_dispatch(write_dir, "WRITE_SIZE")
+    rd = _pmc_per_dispatch(read_dir, READ_COUNTERS)
+    wr = _pmc_per_dispatch(write_dir, WRITE_COUNTERS)
+    copy_r, copy_w = _read_bytes(cr[ck[0]]), _write_bytes(cw[ck[0]])
+    sized = sum(cr[ck[0]].get(c, 0) for c in READ_COUNTERS[1:])
     rows = []
     for frag, cls in KERNEL_CLASS_OF:
-        ks = [k for k in fetch if frag in k]
+        ks = [k for k in rd if frag in k]
         if not ks:
             continue
-        f = sum(fetch[k] for k in ks) / len(ks)
-        w = sum(write.get(k, 0.0) for k in ks) / len(ks)
-        rows.append((cls, f, w, f * 1024 * f_scale + w * 1024 * w_scale))
+        r = sum(_read_bytes(rd[k]) for k in ks) / len(ks)
+        w = sum(_write_bytes(wr.get(k, {})) for k in ks) / len(ks)
+        rows.append((cls, r, w))
+    run = "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline"
     lines = [
-        "# HBM traffic per launch: 7B layer step (T=32768, d=1536, n=256, E=128, K=8), token rounding "
+        "# L2-to-fabric traffic per launch: 7B layer step (T=32768, d=1536, n=256, E=128, K=8), token rounding "
         "M_tile=128 nearest",
         "",
-        "Commands (repository root, one MI355X; each counter in a run of its own):",
+        "Commands (repository root, one MI355X; each counter set in a run of its own):",
         "",
         "```",
-        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- "
-        "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
-        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- "
-        "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
-        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {copy_fetch_dir} -o run -- "
+        f"rocprofv3 --pmc {' '.join(READ_COUNTERS)} --output-format csv -d {read_dir} -o run -- {run}",
+        f"rocprofv3 --pmc {' '.join(WRITE_COUNTERS)} --output-format csv -d {write_dir} -o run -- {run}",
+        f"rocprofv3 --pmc {' '.join(READ_COUNTERS)} --output-format csv -d {copy_read_dir} -o run -- "
         f"python3 bench.py --copy-calibration {copy_bytes}",
-        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {copy_write_dir} -o run -- "
+        f"rocprofv3 --pmc {' '.join(WRITE_COUNTERS)} --output-format csv -d {copy_write_dir} -o run -- "
         f"python3 bench.py --copy-calibration {copy_bytes}",
-        f"python3 bench.py --traffic-report {fetch_dir} {write_dir} {copy_fetch_dir} {copy_write_dir} {copy_bytes}",
+        f"python3 bench.py --traffic-report {read_dir} {write_dir} {copy_read_dir} {copy_write_dir} {copy_bytes}",
         "```",
         "",
-        f"Calibration: a device copy of {copy_bytes} bytes reads FETCH_SIZE = {cf[ck[0]]:.1f} KiB and "
-        f"WRITE_SIZE = {cw[ck[0]]:.1f} KiB per dispatch, so fetch scale = {f_scale:.4f} and write scale = "
-        f"{w_scale:.4f} (bytes per counted byte).",
+        "Bytes are the L2's requests to the memory fabric, by request size: reads 32 B x RDREQ_32B + 64 B x "
+        "RDREQ_64B + 128 B x RDREQ_128B, writes 64 B x WRREQ_64B + 32 B x the other WRREQ.  They include Infinity "
+        "Cache (MALL) hits, which these counters cannot separate from DRAM accesses: this is L2-miss traffic, an "
+        "upper bound on DRAM traffic.",
         "",
-        "| kernel class | FETCH_SIZE KiB/launch | WRITE_SIZE KiB/launch | scaled HBM bytes/launch |",
+        f"Calibration: a device copy of {copy_bytes} bytes reads {copy_r:.0f} and writes {copy_w:.0f} bytes by "
+        f"these counters (sized read requests {sized:.0f} of {cr[ck[0]].get('TCC_EA0_RDREQ', 0):.0f} total).",
+        "",
+        "| kernel class | read bytes/launch | write bytes/launch | total bytes/launch |",
         "|---|---|---|---|",
     ]
-    for cls, f, w, b in rows:
-        lines.append(f"| {cls} | {f:.1f} | {w:.1f} | {b:.0f} |")
+    for cls, r, w in rows:
+        lines.append(f"| {cls} | {r:.0f} | {w:.0f} | {r + w:.0f} |")
     lines += ["", f"kernel sources sha256: {kernel_source_hash()}", ""]
     return "\n".join(lines)
 
 
+def stats_report(stats_csv, title, command):
+    """Markdown table of a rocprofv3 --stats kernel summary (kernel_stats.csv)."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    out = [f"# {title}", "", "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
+           "| kernel | calls | avg us | min us | max us | % of GPU time |", "|---|---|---|---|---|---|"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name = r["Name"].replace("smoe::", "").replace("|", "/")
+        if len(name) > 80:
+            name = name[:77] + "..."
+        out.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                   f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    return "\n".join(out) + "\n"
+
+
 def measured_traffic(kernel_class):
-    """Scaled HBM bytes per launch from the committed profile, if the kernels are unchanged since."""
+    """L2-to-fabric bytes per launch from the committed profile, if the kernels are unchanged since."""
     try:
         with open(TRAFFIC_PROFILE) as fh:
             text = fh.read()
@@ -505,13 +540,18 @@ def main():
                          "one JSON line each, no CPU baseline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run one plain device copy of BYTES (HBM counter calibration) and exit")
-    ap.add_argument("--traffic-report", nargs=5, metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR",
+    ap.add_argument("--traffic-report", nargs=5, metavar=("READ_DIR", "WRITE_DIR", "COPY_READ_DIR",
                                                           "COPY_WRITE_DIR", "COPY_BYTES"),
-                    help="print the HBM-traffic markdown summary from rocprofv3 counter runs and exit")
+                    help="print the L2-to-fabric traffic markdown summary from rocprofv3 counter runs and exit")
+    ap.add_argument("--stats-report", nargs=3, metavar=("KERNEL_STATS_CSV", "TITLE", "COMMAND"),
+                    help="print a rocprofv3 --stats kernel summary as markdown and exit")
     args = ap.parse_args()
     if args.traffic_report:
         fd, wd, cfd, cwd, nb = args.traffic_report
         print(traffic_report(fd, wd, cfd, cwd, int(nb)))
+        return
+    if args.stats_report:
+        print(stats_report(*args.stats_report), end="")
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the layer is built and measured on a "

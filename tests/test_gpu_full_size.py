@@ -102,17 +102,20 @@ def test_7b_expert_biases_full_size():
     _full_size("7b", biases=True)
 
 
-def test_coarse_sampled():
-    """The coarse shape (T=16384, d=4096, n=14336, E=8, K=2, M_tile=128): the
-    full oracle is too slow here, so routing is compared exactly and outputs on
-    samples the oracle computes one by one -- O and dX of sampled tokens, dS of
-    their rows, H of sampled rows, and whole columns of dW1 / rows of dW2 of
-    two experts."""
+@pytest.mark.parametrize("name", ["coarse", "paper-30b-e256k16"])
+def test_sampled_large_shapes(name):
+    """Shapes where the full oracle is too slow: the coarse layer (T=16384,
+    d=4096, n=14336, E=8, K=2) and the finest 30B benchmark layer of the
+    paper's sweep (T=32768, d=4096, n=256, E=256, K=16, the wave-per-token
+    top-K), both with token rounding M_tile=128.  Routing is compared exactly
+    and outputs on samples the oracle computes one by one -- O and dX of
+    sampled tokens, dS of their rows, H of sampled rows, and whole columns of
+    dW1 / rows of dW2 of two experts."""
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2512_14080_amd.layer import DeviceLayer
-    cfg = W.CONFIGS["coarse"]
+    cfg = W.CONFIGS[name]
     t0 = time.time()
     inp = W.make_inputs(cfg, 0)
     _, S = oracle_scores(inp)
@@ -121,7 +124,7 @@ def test_coarse_sampled():
     torch.cuda.synchronize()
     idx, rdir, R = oracle_routing(S, cfg.K, "nearest", cfg.m_tile)
     check_routing(layer, R, idx, rdir)
-    print(f"coarse: routing exact (P={R.P}) after {time.time() - t0:.1f}s", flush=True)
+    print(f"{name}: routing exact (P={R.P}) after {time.time() - t0:.1f}s", flush=True)
     X, W1, W2, Wr, dO = (inp.f32(k) for k in ("X", "W1", "W2", "Wr", "dO"))
     rng = np.random.default_rng(3)
     toks = sorted(rng.choice(cfg.T, 8, replace=False).tolist()) + [0, cfg.T - 1]
@@ -139,12 +142,12 @@ def test_coarse_sampled():
     }
     dW1 = layer.dW1.float().cpu().numpy()
     dW2 = layer.dW2.float().cpu().numpy()
-    cols = [0, 4099, n - 1]
+    cols = sorted({0, min(4099, n // 2 + 3), n - 1})
     for e in (0, cfg.E - 1):
         c1, r2 = oracle.weight_grad_columns(dO, X, W1, W2, R, e, cols)
         errs[f"dW1[{e}]"] = rel_err(np.stack([dW1[e][:, cols], dW1[e][:, [n + j for j in cols]]], axis=1), c1)
         errs[f"dW2[{e}]"] = rel_err(dW2[e][cols, :], r2)
-    print("coarse sampled errors", {k: f"{v:.2e}" for k, v in errs.items()}, f"after {time.time() - t0:.1f}s",
+    print(f"{name} sampled errors", {k: f"{v:.2e}" for k, v in errs.items()}, f"after {time.time() - t0:.1f}s",
           flush=True)
     for k, v in errs.items():
         assert v <= TOL, (k, v, errs)
