@@ -251,20 +251,22 @@ struct KOuterSide {
 #pragma unroll
     for (int j = 0; j < Q; ++j) asm volatile("" : "+v"(gnext[j]));
   }
+  // The source address is formed without branches: row and leading
+  // dimension are below 2^31 and 2^32, so one 32 x 32 -> 64-bit multiply-add
+  // gives the byte offset, and k rows past the reduction (or masked columns)
+  // select the zero page instead.
   __device__ __forceinline__ void issue(uint32_t lds_side, int k0, int part = 0, int parts = 1) const {
     const uint32_t w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
+    const uint32_t ld32 = (uint32_t)ld_bytes;
 #pragma unroll
     for (int j = 0; j < Q; ++j) {
       if (j % parts != part) continue;
       const int k = k0 + krow[j];
-      const char* src;
-      if (k < k_len && colb[j] >= 0) {
-        const int64_t row = gidx ? (int64_t)gnext[j] : (int64_t)(k_begin + k);
-        src = base + row * ld_bytes + colb[j];
-      } else {
-        src = (const char*)g_zero_page + lane * 16;
-      }
+      const uint32_t row = gidx ? (uint32_t)gnext[j] : (uint32_t)(k_begin + k);
+      const uint64_t off = (uint64_t)row * ld32 + (uint32_t)colb[j];
+      const bool ok = k < k_len && colb[j] >= 0;
+      const char* src = ok ? base + off : (const char*)g_zero_page + lane * 16;
       dma16(src, lds_side + (w + NW * j) * 1024);
     }
   }
@@ -273,18 +275,14 @@ struct KOuterSide {
     const int lane = threadIdx.x & 63;
     const int g = lane >> 4, i = lane & 15;
     const int m = c0 + 16 * (g & 1) + 4 * (i & 3);
-    const int kb = 16 * s + 8 * (g >> 1) + (i >> 2);
-    v4i16 lo, hi;
-    {
-      const int k = kb;
-      const char* p = lds_side + k * (2 * R) + (((m >> 3) ^ swz(k)) << 4) + (m & 7) * 2;
-      lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SMOE_LDS v4i16*)p);
-    }
-    {
-      const int k = kb + 4;
-      const char* p = lds_side + k * (2 * R) + (((m >> 3) ^ swz(k)) << 4) + (m & 7) * 2;
-      hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SMOE_LDS v4i16*)p);
-    }
+    // this lane's first k row within a sub-step; its rows kb + 16 s and kb + 16 s + 4
+    // have the same chunk swizzle (swz depends on bits 0-1 of k, which 16 s and the
+    // carry-free + 4 leave alone), so one per-lane offset serves every read and the
+    // sub-step and second-read steps are constants
+    const int kb = 8 * (g >> 1) + (i >> 2);
+    const char* p = lds_side + kb * (2 * R) + (((m >> 3) ^ swz(kb)) << 4) + (m & 7) * 2 + 16 * s * (2 * R);
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SMOE_LDS v4i16*)p);
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SMOE_LDS v4i16*)(p + 4 * (2 * R)));
     typedef short v8i16 __attribute__((ext_vector_type(8)));
     const v8i16 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     return __builtin_bit_cast(bf16x8, v);
