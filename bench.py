@@ -163,6 +163,7 @@ def stats_report(stats_csv, title, command):
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
     out = [f"# {title}", "", "Command (run from the repository root on one MI355X):", "", "```", command, "```", "",
+           f"Table: `python3 bench.py --stats-report {stats_csv} TITLE COMMAND` (this file's title and command).", "",
            "| kernel | calls | avg us | min us | max us | % of GPU time |", "|---|---|---|---|---|---|"]
     for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
         name = r["Name"].replace("smoe::", "").replace("|", "/")
@@ -410,6 +411,8 @@ def measure(args, cfg, cpu):
         "pct_bf16_peak": round(100.0 * tflops / PEAK_BF16_TFLOPS, 2),
         "roofline": {"kernel": dominant, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
                      "unit": unit, "frac": round(achieved / peak, 4), "traffic": measured_traffic(dominant),
+                     "traffic_note": "bytes per launch between L2 and the memory fabric from the TCC request "
+                                     "counters by size (includes Infinity Cache hits; an upper bound on DRAM bytes)",
                      "launch_ms": round(dom_avg, 5), "launches": dom_n},
         "kernel_ms": {c: round(t, 5) for c, t in per.items()},
         "kernels": kernel_table(per, cfg, P),
