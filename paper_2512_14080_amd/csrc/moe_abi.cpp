@@ -182,6 +182,12 @@ size_t bwd_layout(const moe_dims& m, int64_t cap, char* base, BwdWs* w) {
   return off;
 }
 
+// byte offset of the two-level selection's lists in the routing scratch
+size_t round_lists_offset(const moe_dims& m) {
+  const int W = (m.T + 63) / 64;
+  return ((size_t)(m.E + 64 + 2 * (W + 1)) * 4 + 255) / 256 * 256;
+}
+
 size_t routing_layout(const moe_dims& m, int64_t cap, int flags, char* base, moe_routing* r) {
   const int W = (m.T + 63) / 64;
   const size_t TE = (size_t)m.T * m.E, EW = (size_t)m.E * W, TK = (size_t)m.T * m.K;
@@ -224,7 +230,9 @@ size_t routing_layout(const moe_dims& m, int64_t cap, int flags, char* base, moe
   o->tok_denom = (float*)p;
   take((size_t)m.E * 4, &p);
   o->round_dir = (int32_t*)p;
-  take((size_t)(m.E + 64 + 2 * (W + 1)) * 4, &p);  // rounding needs [E], then per-word token sums and bases
+  // rounding needs [E], then per-word token sums and bases, then the lists of
+  // the two-level selection
+  take(round_lists_offset(m) + smoe::round_scratch_bytes(m.T, m.E), &p);
   o->scratch = (int32_t*)p;
   take(4, &p);
   o->status = (int32_t*)p;
@@ -389,7 +397,8 @@ int moe_round_tokens(moe_dims m, int32_t m_tile, int mode, const float* u, const
   tr->state = MOE_ROUTING_STATE_EMPTY;
   smoe::prof_begin(MOE_KC_ROUND, stream);
   bool counted = false;
-  hipError_t e = smoe::launch_round(*tc, *tr, u, m.T, m.E, m_tile, mode, &counted, stream);
+  uint64_t* list = smoe::round_scratch_bytes(m.T, m.E) ? (uint64_t*)((char*)tr->scratch + round_lists_offset(m)) : nullptr;
+  hipError_t e = smoe::launch_round(*tc, *tr, u, m.T, m.E, m_tile, mode, list, &counted, stream);
   if (e == hipSuccess) e = smoe::launch_metadata(*tr, tc->scores_t, m.T, m.E, counted, stream);
   smoe::prof_end(MOE_KC_ROUND, stream);
   if (e != hipSuccess) return hip_fail(e, "token rounding");

@@ -4,10 +4,12 @@
 // The paper describes the method as a two-step sort (TC top-K, then a sort of
 // each expert's tokens by router score with TC tokens preferred).  Only the
 // last tile changes, so instead of sorting all T tokens per expert this code
-// selects the at most m_tile-1 tokens that change with a bitwise (32-pass)
-// select on an order-preserving integer image of the fp32 score, then breaks
-// ties on the threshold value by token index.  The result is the same set the
-// full sort would give.
+// selects the at most m_tile-1 tokens that change with a bitwise select on an
+// order-preserving integer image of the fp32 score, ties on the threshold
+// value broken by token index.  The result is the same set the full sort
+// would give.  Up to 65536 tokens the select runs in two levels (per
+// 2048-token chunk, then over the chunks' picks); beyond, one block per
+// expert selects from all its tokens.
 #include "device_common.h"
 #include "launch.h"
 
@@ -90,18 +92,15 @@ __device__ __forceinline__ void transpose32(uint32_t (&A)[32]) {
   }
 }
 
-// One block per expert.  Copies the TC mask row of expert e into the rounded
+// The any-T selection, for rows beyond what the two-level form below holds:
+// one block per expert.  Copies the TC mask row of expert e into the rounded
 // mask and flips the `need` selected bits:
 //   pad  (dir > 0): the need best non-TC tokens by (score desc, token asc);
 //   drop (dir < 0): the need worst TC tokens by (score asc, token desc).
 // Both become "the need largest keys" with key = score_key for pads and
 // ~score_key for drops, ties preferring low tokens for pads, high for drops.
-//
-// Token t is owned by thread t % 1024 as its slot t / 1024.  With KPT > 0 the
-// block holds all T <= 1024*KPT keys in registers (read once; KPT <= 32 keeps
-// them within the 128 VGPRs a 1024-thread block allows); KPT == 0 is the
-// any-T form that re-reads the scores from memory on every pass.
-template <int KPT>
+// Token t is owned by thread t % 1024 as its slot t / 1024; every pass of the
+// bitwise select re-reads the scores.
 __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* __restrict__ tc_mask,
                                                                 uint64_t* __restrict__ tr_mask,
                                                                 const float* __restrict__ scores_t,
@@ -109,8 +108,7 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
                                                                 const int32_t* __restrict__ need_arr,
                                                                 const int32_t* __restrict__ counts,
                                                                 const float* __restrict__ u, int M, int mode, int T,
-                                                                int W, int32_t* __restrict__ prefix_out,
-                                                                int32_t* __restrict__ counts_out) {
+                                                                int W) {
   constexpr int kWaves = kSelThreads / 64;
   __shared__ int lds[kWaves];
   __shared__ int cnt_lds[2][kWaves];  // per-wave counts of a pass, double-buffered by pass parity
@@ -127,23 +125,8 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     tr_decide_one(counts[e], mode == MOE_ROUND_STOCHASTIC ? u[e] : 0.f, T, M, mode, &dir, &need);
     if (threadIdx.x == 0) round_dir[e] = dir;
   }
-  // With KPT > 0 (W <= 16 * KPT <= 1024 words) the block also writes the
-  // rounded row's word prefix counts and the expert's row count, which are
-  // otherwise a pass of their own.
-  auto write_prefix = [&](int pc) {
-    int total;
-    const int ex = block_excl_scan<kSelThreads>(pc, &total, lds);
-    if ((int)threadIdx.x < W) prefix_out[(size_t)e * W + threadIdx.x] = ex;
-    if (threadIdx.x == 0) counts_out[e] = total;
-  };
   if (dir == 0 || need == 0) {
-    if constexpr (KPT > 0) {
-      const uint64_t v = (int)threadIdx.x < W ? src[threadIdx.x] : 0ull;
-      if ((int)threadIdx.x < W) dst[threadIdx.x] = v;
-      write_prefix(__popcll(v));
-    } else {
-      for (int w = threadIdx.x; w < W; w += kSelThreads) dst[w] = src[w];
-    }
+    for (int w = threadIdx.x; w < W; w += kSelThreads) dst[w] = src[w];
     return;
   }
   const float* S = scores_t + (size_t)e * T;
@@ -161,34 +144,6 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     const uint32_t k = score_key(S[t]);
     return dir < 0 ? ~k : k;
   };
-  uint32_t keys[KPT > 0 ? KPT : 1];
-  uint64_t cmask = 0;
-  if constexpr (KPT > 0) {
-    // scores and mask words are requested 16 slots at a time before any is used
-    constexpr int kBatch = KPT < 16 ? KPT : 16;
-#pragma unroll
-    for (int i0 = 0; i0 < KPT; i0 += kBatch) {
-      uint64_t words[kBatch];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int i = i0 + u;
-        const int t = i * kSelThreads + threadIdx.x;
-        const int w = __builtin_amdgcn_readfirstlane(i * kWaves + wave);  // the wave's word: a scalar load
-        keys[i] = t < T ? __float_as_uint(S[t]) : 0u;
-        words[u] = w < W ? src[w] : 0ull;
-      }
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int i = i0 + u;
-        const int t = i * kSelThreads + threadIdx.x;
-        const bool c = t < T && ((((words[u] >> lane) & 1ull) != 0) == want_set);
-        const uint32_t k = score_key(__uint_as_float(keys[i]));
-        keys[i] = c ? (dir < 0 ? ~k : k) : 0u;
-        cmask |= (uint64_t)c << i;
-      }
-      asm volatile("" ::: "memory");  // keep the next batch's loads after this one
-    }
-  }
   // number of candidates in the block whose key k has (k >> sh) == v.  One
   // barrier per call: the counts of consecutive calls go to alternating slots,
   // and a slot is only rewritten after the next call's barrier, which every
@@ -196,15 +151,10 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
   int parity = 0;
   auto count_eq = [&](uint32_t v, int sh) -> int {
     int cnt = 0;
-    if constexpr (KPT > 0) {
-#pragma unroll
-      for (int i = 0; i < KPT; ++i) cnt += __popcll(__ballot(((cmask >> i) & 1ull) && (keys[i] >> sh) == v));
-    } else {
-      for (int i = 0; i < slots; ++i) {
-        bool c;
-        const uint32_t k = load_key(i, c);
-        cnt += __popcll(__ballot(c && (k >> sh) == v));
-      }
+    for (int i = 0; i < slots; ++i) {
+      bool c;
+      const uint32_t k = load_key(i, c);
+      cnt += __popcll(__ballot(c && (k >> sh) == v));
     }
     if (lane == 0) cnt_lds[parity][wave] = cnt;
     __syncthreads();
@@ -220,93 +170,14 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
   // hold `remaining` keys, else count them as taken and clear it.
   uint32_t prefix = 0;
   int remaining = need;
-  int nties;
-  uint32_t gt_mask = 0, tie_mask = 0;  // register form: candidates with key > tau / == tau
-  if constexpr (KPT > 0) {
-    // Register form: bit i of `alive` marks key i as a candidate that still
-    // matches the prefix.  The keys are first transposed into bit planes
-    // (plane[b] bit i = bit b of key i), so a pass costs a few mask
-    // operations and popcounts per lane instead of a ballot per key.
-    uint32_t alive = (uint32_t)cmask;
-    uint32_t plane[32];
-#pragma unroll
-    for (int i = 0; i < 32; ++i) plane[i] = i < KPT ? keys[i] : 0u;
-    transpose32(plane);
-    auto block_total = [&](int cnt) {
-      if (lane == 0) cnt_lds[parity][wave] = cnt;
-      __syncthreads();
-      int total = 0;
-#pragma unroll
-      for (int q = 0; q < kWaves; ++q) total += cnt_lds[parity][q];
-      parity ^= 1;
-      return total;
-    };
-    auto wave_sum_u = [&](uint32_t x) { return dpp_reduce(x, [](uint32_t a, uint32_t b) { return a + b; }); };
-    // two bits per pass: block counts of the alive keys whose next digit is
-    // 3, 2 and 1 decide the digit of tau (16 passes, one barrier each)
-    // per-wave counts of a pass: digit 1, and digits 3 (low half) and 2 (high
-    // half) packed (block totals stay below 2^16), read back four waves at a time
-    __shared__ __attribute__((aligned(16))) uint32_t cnt3_lds[2][2][kWaves];
-#pragma unroll
-    for (int sh = 30; sh >= 0; sh -= 2) {
-      const uint32_t hi = plane[sh + 1], lo = plane[sh];
-      const uint32_t a3 = alive & hi & lo, a2 = alive & hi & ~lo, a1 = alive & ~hi & lo;
-      // per-wave counts (each <= 64 * 32): digits 3 and 2 share one word
-      const uint32_t c32 = wave_sum_u((uint32_t)__popc(a3) | ((uint32_t)__popc(a2) << 16));
-      const uint32_t c1 = wave_sum_u((uint32_t)__popc(a1));
-      if (lane == 0) {
-        cnt3_lds[parity][0][wave] = c1;
-        cnt3_lds[parity][1][wave] = c32;
-      }
-      __syncthreads();
-      uint32_t s1 = 0, s32 = 0;
-#pragma unroll
-      for (int q = 0; q < kWaves; q += 4) {
-        const u32x4 x = *(const u32x4*)&cnt3_lds[parity][0][q];
-        const u32x4 y = *(const u32x4*)&cnt3_lds[parity][1][q];
-        s1 += (x[0] + x[1]) + (x[2] + x[3]);
-        s32 += (y[0] + y[1]) + (y[2] + y[3]);
-      }
-      const int t1 = (int)s1, t2 = (int)(s32 >> 16), t3 = (int)(s32 & 0xffffu);
-      parity ^= 1;
-      if (t3 >= remaining) {
-        prefix |= 3u << sh;
-        alive = a3;
-      } else if (t3 + t2 >= remaining) {
-        prefix |= 2u << sh;
-        remaining -= t3;
-        alive = a2;
-      } else if (t3 + t2 + t1 >= remaining) {
-        prefix |= 1u << sh;
-        remaining -= t3 + t2;
-        alive = a1;
-      } else {
-        remaining -= t3 + t2 + t1;
-        alive &= ~(hi | lo);
-      }
-    }
-    // the survivors are exactly the candidate keys equal to tau
-    nties = block_total((int)wave_sum_u((uint32_t)__popc(alive)));
-    tie_mask = alive;
-    // key > tau from the planes (most significant bit first, tau uniform)
-    uint32_t eq = 0xffffffffu;
-#pragma unroll
-    for (int b = 31; b >= 0; --b) {
-      const uint32_t tb = ((prefix >> b) & 1u) ? 0xffffffffu : 0u;
-      gt_mask |= eq & plane[b] & ~tb;
-      eq &= ~(plane[b] ^ tb);
-    }
-    gt_mask &= (uint32_t)cmask;
-  } else {
-    for (int bit = 31; bit >= 0; --bit) {
-      const int total = count_eq((prefix >> bit) | 1u, bit);
-      if (total >= remaining)
-        prefix |= 1u << bit;
-      else
-        remaining -= total;
-    }
-    nties = count_eq(prefix, 0);
+  for (int bit = 31; bit >= 0; --bit) {
+    const int total = count_eq((prefix >> bit) | 1u, bit);
+    if (total >= remaining)
+      prefix |= 1u << bit;
+    else
+      remaining -= total;
   }
+  const int nties = count_eq(prefix, 0);
   const uint32_t tau = prefix;
 
   // Marking pass in ascending token order: slot i of wave w is word 16i + w.
@@ -317,7 +188,9 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
   const int first_tie = dir > 0 ? 0 : nties - remaining;
   const int last_tie = dir > 0 ? remaining : nties;  // flip ranks in [first_tie, last_tie)
   int carry = 0;
-  auto mark = [&](int i, bool cand, uint32_t k) {
+  for (int i = 0; i < slots; ++i) {
+    bool cand;
+    const uint32_t k = load_key(i, cand);
     const int w = i * kWaves + wave;
     const bool gt = cand && k > tau;
     const bool tie = cand && k == tau;
@@ -337,52 +210,303 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
     if (w < W && lane == 0) dst[w] = src[w] ^ flips;
     carry += total;
     __syncthreads();
-  };
-  if constexpr (KPT > 0) {
-    // Register form: all tie counts first (flat index slot * waves + wave),
-    // one block scan for every tie's rank base, then all flips.
-    __shared__ int tie_base[KPT * kWaves];
-    __shared__ int word_pc[KPT * kWaves];
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const uint64_t ties = __ballot((tie_mask >> i) & 1u);
-      if (lane == 0) tie_base[i * kWaves + wave] = __popcll(ties);
-    }
-    __syncthreads();
-    const int cnt = threadIdx.x < KPT * kWaves ? tie_base[threadIdx.x] : 0;
-    int all_ties;
-    const int ex = block_excl_scan<kSelThreads>(cnt, &all_ties, lds);
-    if (threadIdx.x < KPT * kWaves) tie_base[threadIdx.x] = ex;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      if (i >= slots) break;
-      const int w = i * kWaves + wave;
-      const bool gt = (gt_mask >> i) & 1u;
-      const bool tie = (tie_mask >> i) & 1u;
-      const uint64_t ties = __ballot(tie);
-      const int rank = tie_base[w] + __popcll(ties & lanemask_lt());
-      const bool flip = gt || (tie && rank >= first_tie && rank < last_tie);
-      const uint64_t flips = __ballot(flip);
-      if (w < W && lane == 0) {
-        const uint64_t v = src[w] ^ flips;
-        dst[w] = v;
-        word_pc[w] = __popcll(v);
-      }
-    }
-    __syncthreads();
-    write_prefix((int)threadIdx.x < W ? word_pc[threadIdx.x] : 0);
-  } else {
-    for (int i = 0; i < slots; ++i) {
-      bool c;
-      const uint32_t k = load_key(i, c);
-      mark(i, c, k);
-    }
   }
 }
 
+// ------------------------------------------------ two-level selection
+// The need largest candidate keys of an expert, with ties on the key broken by
+// token (low first for pads, high first for drops), form a strict total order
+// on the candidates.  Under a strict order the global top-need set lies in the
+// union of the top-need sets of any partition of the candidates: an element of
+// the global set outranks all but fewer than need candidates, so also within
+// its own part.  Level 1 gives every kTrChunk tokens of an expert one wave,
+// which selects its chunk's top-need with wave reductions only (no workgroup
+// barrier) and lists the chosen (key, token) pairs in token order; level 2
+// selects the top-need of those lists per expert with one wave and writes the
+// rounded mask row, its word prefixes and the count.  The selection work of
+// an expert is spread over T / kTrChunk waves instead of one CU.
+constexpr int kTrChunk = 2048;       // tokens per level-1 wave: 32 slots x 64 lanes
+constexpr int kTrMaxTokens = 65536;  // level 2 keeps the W <= 1024 mask words of a row in LDS
+
+// List space: m_tile <= 256 entries of 8 bytes per chunk of every expert.
+size_t round_scratch_bytes(int T, int E) {
+  if (T > kTrMaxTokens) return 0;
+  const size_t nch = (size_t)(T + kTrChunk - 1) / kTrChunk;
+  return (size_t)E * nch * 256 * 8;
+}
+
+// Packed digit counts of a pass: each lane holds three 10-bit counts; the
+// sum over a group of 16 / G lanes stays below 1024 per field (at most
+// 32 G keys per lane).  DPP adds form the group sums in every lane; the
+// groups' sums are read out and added per field on the scalar unit.
+template <int G>
+__device__ __forceinline__ void wave_counts3(uint32_t x, int* f0, int* f1, int* f2) {
+  auto add = [](uint32_t a, uint32_t b) { return a + b; };
+  x = add(x, dpp_mov<0xB1, 0xf>(x));  // quad_perm [1,0,3,2]
+  x = add(x, dpp_mov<0x4E, 0xf>(x));  // quad_perm [2,3,0,1]
+  x = add(x, dpp_mov<0x141, 0xf>(x));  // row_half_mirror: 8-lane sums
+  if constexpr (G == 1) x = add(x, dpp_mov<0x140, 0xf>(x));  // row_mirror: 16-lane sums
+  constexpr int kStep = 16 / G;
+  int a = 0, b = 0, c = 0;
+#pragma unroll
+  for (int l = 0; l < 64; l += kStep) {
+    const uint32_t v = (uint32_t)__builtin_amdgcn_readlane((int)x, l);
+    a += (int)(v & 1023u);
+    b += (int)((v >> 10) & 1023u);
+    c += (int)(v >> 20);
+  }
+  *f0 = a;
+  *f1 = b;
+  *f2 = c;
+}
+
+// Wave-local selection of the `need` largest candidate keys.  Key (g, i) of
+// lane l sits at position p = (32 g + i) * 64 + l; ties on the key go to the
+// lower positions first when low_first, else to the higher ones.  cm[g] bit i
+// marks a candidate; keys[g][i] is its key (destroyed: the keys become bit
+// planes).  Returns the selected candidates as sel[g] bits.
+//
+// Bitwise select over the planes, two bits per pass, MSB first: `alive`
+// holds the candidates that still match the selected prefix, `taken` those
+// already known to be selected (a higher digit at some pass).  Once the alive
+// keys are exactly as many as are still to take, all of them are taken and
+// the remaining bits are not looked at.
+template <int G>
+__device__ __forceinline__ void wave_select(uint32_t (&keys)[G][32], const uint32_t (&cm)[G], int need,
+                                            bool low_first, uint32_t (&sel)[G]) {
+  uint32_t c = 0;
+#pragma unroll
+  for (int g = 0; g < G; ++g) c += (uint32_t)__popc(cm[g]);
+  int nalive, unused0, unused1;
+  wave_counts3<G>(c, &nalive, &unused0, &unused1);
+  if (nalive <= need) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) sel[g] = cm[g];
+    return;
+  }
+#pragma unroll
+  for (int g = 0; g < G; ++g) transpose32(keys[g]);  // keys[g][b] bit i = bit b of key i
+  uint32_t alive[G], taken[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    alive[g] = cm[g];
+    taken[g] = 0u;
+  }
+  int remaining = need;
+#pragma unroll
+  for (int sh = 30; sh >= 0; sh -= 2) {
+    uint32_t a3[G], a2[G], a1[G], cnt = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const uint32_t hi = keys[g][sh + 1], lo = keys[g][sh];
+      a3[g] = alive[g] & hi & lo;
+      a2[g] = alive[g] & hi & ~lo;
+      a1[g] = alive[g] & ~hi & lo;
+      cnt += (uint32_t)__popc(a3[g]) | ((uint32_t)__popc(a2[g]) << 10) | ((uint32_t)__popc(a1[g]) << 20);
+    }
+    int t3, t2, t1;
+    wave_counts3<G>(cnt, &t3, &t2, &t1);
+    if (t3 >= remaining) {
+      nalive = t3;
+#pragma unroll
+      for (int g = 0; g < G; ++g) alive[g] = a3[g];
+    } else if (t3 + t2 >= remaining) {
+      remaining -= t3;
+      nalive = t2;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        taken[g] |= a3[g];
+        alive[g] = a2[g];
+      }
+    } else if (t3 + t2 + t1 >= remaining) {
+      remaining -= t3 + t2;
+      nalive = t1;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        taken[g] |= a3[g] | a2[g];
+        alive[g] = a1[g];
+      }
+    } else {
+      remaining -= t3 + t2 + t1;
+      nalive -= t3 + t2 + t1;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        taken[g] |= a3[g] | a2[g] | a1[g];
+        alive[g] &= ~(a3[g] | a2[g] | a1[g]);
+      }
+    }
+    if (nalive == remaining) break;
+  }
+  if (nalive == remaining) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) sel[g] = taken[g] | alive[g];
+    return;
+  }
+  // every bit decided: alive holds the nalive keys equal to the threshold,
+  // of which `remaining` are taken by position.  A tie's rank: the ties of
+  // the earlier slots, then of the lower lanes of its own slot.
+  const int lo_rank = low_first ? 0 : nalive - remaining, hi_rank = low_first ? remaining : nalive;
+  int base = 0;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    uint32_t take = 0;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) {
+      const bool tie = (alive[g] >> i) & 1u;
+      const uint64_t b = __ballot(tie);
+      const int rank = base + __popcll(b & lanemask_lt());
+      take |= (uint32_t)(tie && rank >= lo_rank && rank < hi_rank) << i;
+      base += __popcll(b);
+    }
+    sel[g] = taken[g] | take;
+  }
+}
+
+// The rounding decision of expert e (both levels take it the same way).
+__device__ __forceinline__ void tr_decision(int e, const int32_t* round_dir, const int32_t* need_arr,
+                                            const int32_t* counts, const float* u, int T, int M, int mode, int* dir,
+                                            int* need) {
+  if (need_arr) {
+    *dir = round_dir[e];
+    *need = need_arr[e];
+  } else {
+    tr_decide_one(counts[e], mode == MOE_ROUND_STOCHASTIC ? u[e] : 0.f, T, M, mode, dir, need);
+  }
+}
+
+// Level 1: wave (e, c) selects the top-need candidates among tokens
+// [c * kTrChunk, (c + 1) * kTrChunk) of expert e and writes the M list
+// entries of its chunk at list[(e * nch + c) * M]: the chosen ones in token
+// order as (key << 32) | (chunk-local token << 1) | 1, then zeros (entry
+// bit 0 marks a pick).  Token 64 i + l of the chunk is slot i of lane l
+// (slot i is mask word 32 c + i).
+__global__ __launch_bounds__(256) void tr_local_kernel(const uint64_t* __restrict__ tc_mask,
+                                                       const float* __restrict__ scores_t,
+                                                       const int32_t* __restrict__ round_dir,
+                                                       const int32_t* __restrict__ need_arr,
+                                                       const int32_t* __restrict__ counts, const float* __restrict__ u,
+                                                       int M, int mode, int T, int E, int W, int nch,
+                                                       uint64_t* __restrict__ list) {
+  const int gw = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
+  const int e = gw / nch, c = gw - e * nch;
+  if (e >= E) return;
+  int dir, need;
+  tr_decision(e, round_dir, need_arr, counts, u, T, M, mode, &dir, &need);
+  if (dir == 0 || need == 0) return;  // level 2 reads no list for this expert
+  const int lane = lane_id();
+  const bool want_set = dir < 0;  // candidates: TC tokens for drops, non-TC for pads
+  const float* S = scores_t + (size_t)e * T;
+  const uint64_t* src = tc_mask + (size_t)e * W;
+  uint32_t keys[1][32];
+  uint64_t words[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const int t = c * kTrChunk + 64 * i + lane;
+    const int w = c * 32 + i;  // wave-uniform: a scalar load
+    words[i] = w < W ? src[w] : 0ull;
+    keys[0][i] = t < T ? __float_as_uint(S[t]) : 0u;
+  }
+  uint32_t cm[1] = {0u}, kept[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const int t = c * kTrChunk + 64 * i + lane;
+    const bool cnd = t < T && ((((words[i] >> lane) & 1ull) != 0) == want_set);
+    const uint32_t k = score_key(__uint_as_float(keys[0][i]));
+    keys[0][i] = kept[i] = cnd ? (dir < 0 ? ~k : k) : 0u;
+    cm[0] |= (uint32_t)cnd << i;
+  }
+  uint32_t sel[1];
+  wave_select<1>(keys, cm, need, dir > 0, sel);
+  uint64_t* out = list + (size_t)gw * M;
+  int n = 0;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const bool s = (sel[0] >> i) & 1u;
+    const uint64_t b = __ballot(s);
+    if (s) out[n + __popcll(b & lanemask_lt())] = ((uint64_t)kept[i] << 32) | ((uint32_t)(64 * i + lane) << 1) | 1u;
+    n += __popcll(b);
+  }
+  for (int q = n + lane; q < M; q += 64) out[q] = 0ull;
+}
+
+// Level 2, one workgroup of 4 waves per expert.  Wave 0 selects the top-need
+// of the expert's level-1 picks (entry q of chunk c at position c * M + q,
+// i.e. token order; 32 G slots per lane) while the others copy the TC mask
+// row into LDS; the chosen tokens' bits are flipped there, and the row goes
+// out with its word prefixes and count.
+template <int G>
+__global__ __launch_bounds__(256) void tr_merge_kernel(const uint64_t* __restrict__ tc_mask,
+                                                       uint64_t* __restrict__ tr_mask,
+                                                       int32_t* __restrict__ round_dir,
+                                                       const int32_t* __restrict__ need_arr,
+                                                       const int32_t* __restrict__ counts, const float* __restrict__ u,
+                                                       int M, int mode, int T, int W, int nch,
+                                                       const uint64_t* __restrict__ list,
+                                                       int32_t* __restrict__ prefix_out,
+                                                       int32_t* __restrict__ counts_out) {
+  __shared__ uint64_t row[kTrMaxTokens / 64];
+  __shared__ int scan_lds[4];
+  const int e = blockIdx.x;
+  const int wave = threadIdx.x >> 6, lane = lane_id();
+  int dir, need;
+  tr_decision(e, round_dir, need_arr, counts, u, T, M, mode, &dir, &need);
+  if (!need_arr && threadIdx.x == 0) round_dir[e] = dir;
+  const uint64_t* src = tc_mask + (size_t)e * W;
+  const bool select = dir != 0 && need != 0;
+  uint32_t sel[G];
+  int tok[G][32];
+  if (select && wave == 0) {
+    const uint64_t* lst = list + (size_t)e * nch * M;
+    const int np = nch * M;  // positions; entry p of the expert's lists
+    uint32_t keys[G][32], cm[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      cm[g] = 0u;
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const int p = (32 * g + i) * 64 + lane;
+        const uint64_t v = p < np ? lst[p] : 0ull;
+        const int ch = p / M;  // M is a power of two
+        tok[g][i] = ch * kTrChunk + (int)(((uint32_t)v >> 1) & (kTrChunk - 1));
+        keys[g][i] = (uint32_t)(v >> 32);
+        cm[g] |= (uint32_t)(v & 1u) << i;
+      }
+    }
+    wave_select<G>(keys, cm, need, dir > 0, sel);
+  }
+  for (int w = threadIdx.x; w < W; w += 256) row[w] = src[w];
+  __syncthreads();
+  if (select && wave == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int i = 0; i < 32; ++i)
+        if ((sel[g] >> i) & 1u) atomicXor((unsigned long long*)&row[tok[g][i] >> 6], 1ull << (tok[g][i] & 63));
+  }
+  __syncthreads();
+  // four consecutive words per thread (W <= 1024)
+  uint64_t* dst = tr_mask + (size_t)e * W;
+  const int w0 = 4 * threadIdx.x;
+  int pc[4], sum = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint64_t v = w0 + k < W ? row[w0 + k] : 0ull;
+    if (w0 + k < W) dst[w0 + k] = v;
+    pc[k] = __popcll(v);
+    sum += pc[k];
+  }
+  int total;
+  int ex = block_excl_scan<256>(sum, &total, scan_lds);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (w0 + k < W) prefix_out[(size_t)e * W + w0 + k] = ex;
+    ex += pc[k];
+  }
+  if (threadIdx.x == 0) counts_out[e] = total;
+}
+
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
-                        bool* counted, hipStream_t s) {
+                        uint64_t* list, bool* counted, hipStream_t s) {
   // Balance-f is sequential over experts: its own pass decides; the other
   // subroutines are decided inside the selection workgroups
   int32_t* need = nullptr;
@@ -390,20 +514,25 @@ hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, 
     need = tr.scratch;
     tr_decide_kernel<<<dim3(1), dim3(256), 0, s>>>(tc.counts, u, tr.round_dir, need, T, E, M, mode);
   }
-  const int slots = (T + kSelThreads - 1) / kSelThreads;
-  auto select = [&](auto kernel) {
-    kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, tc.counts, u, M,
-                                                 mode, T, tr.words, tr.mask_prefix, tr.counts);
-  };
-  *counted = slots <= 32;
-  if (slots <= 4)
-    select(tr_select_kernel<4>);
-  else if (slots <= 16)
-    select(tr_select_kernel<16>);
-  else if (slots <= 32)
-    select(tr_select_kernel<32>);
-  else
-    select(tr_select_kernel<0>);
+  const int nch = (T + kTrChunk - 1) / kTrChunk;
+  // two levels where the level-2 wave holds every list entry in 64 slots per
+  // lane and the rounding scratch has room for the lists
+  if (T <= kTrMaxTokens && (int64_t)nch * M <= 64 * 64 && list != nullptr) {
+    const int waves = E * nch;
+    tr_local_kernel<<<dim3((waves + 3) / 4), dim3(256), 0, s>>>(tc.mask, tc.scores_t, tr.round_dir, need, tc.counts,
+                                                                u, M, mode, T, E, tr.words, nch, list);
+    if (nch * M <= 64 * 32)
+      tr_merge_kernel<1><<<dim3(E), dim3(256), 0, s>>>(tc.mask, tr.mask, tr.round_dir, need, tc.counts, u, M, mode, T,
+                                                       tr.words, nch, list, tr.mask_prefix, tr.counts);
+    else
+      tr_merge_kernel<2><<<dim3(E), dim3(256), 0, s>>>(tc.mask, tr.mask, tr.round_dir, need, tc.counts, u, M, mode, T,
+                                                       tr.words, nch, list, tr.mask_prefix, tr.counts);
+    *counted = true;
+    return hipGetLastError();
+  }
+  tr_select_kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, tc.counts,
+                                                         u, M, mode, T, tr.words);
+  *counted = false;
   return hipGetLastError();
 }
 

@@ -238,10 +238,10 @@ ROUTE_ONLY = W.MoEConfig("route", T=3000, d=128, n=128, E=16, K=4, m_tile=128)
 @pytest.mark.parametrize("T", [3000, 9000, 20000, 40000])
 @pytest.mark.parametrize("quantised", [False, True])
 def test_rounding_selection_sizes_and_ties(T, quantised):
-    """Token sizes spanning every form of the device's rounding selection
-    (register-resident keys up to 32 per thread, then the re-reading form),
-    with real-valued scores and with scores on a coarse grid, where most
-    candidates tie on the threshold and the token-order tie break decides."""
+    """Token sizes spanning the two-level rounding selection (one and two
+    32-key slot groups per lane in the second level), with real-valued scores
+    and with scores on a coarse grid, where most candidates tie on the
+    threshold and the token-order tie break decides."""
     torch = _torch()
     from paper_2512_14080_amd.layer import DeviceLayer
     inp = W.make_inputs(ROUTE_ONLY, 11, T=T)
@@ -253,6 +253,28 @@ def test_rounding_selection_sizes_and_ties(T, quantised):
         layer.route()
         torch.cuda.synchronize()
         idx, rdir, R = oracle_routing(S, ROUTE_ONLY.K, mode, ROUTE_ONLY.m_tile)
+        check_routing(layer, R, idx, rdir)
+
+
+@pytest.mark.parametrize("T,m_tile", [(5000, 8), (20000, 256), (40000, 256)])
+@pytest.mark.parametrize("quantised", [False, True])
+def test_rounding_selection_tiles(T, m_tile, quantised):
+    """The smallest and largest M_tile: two-level selection with one and two
+    slot groups in the second level (T = 5000 / 20000), and the one-block
+    form for rows whose chunk picks exceed the second level (T = 40000 at
+    M_tile = 256)."""
+    torch = _torch()
+    from paper_2512_14080_amd.layer import DeviceLayer
+    cfg = W.MoEConfig("tiles", T=T, d=128, n=128, E=16, K=4, m_tile=m_tile)
+    inp = W.make_inputs(cfg, 12)
+    _, S = oracle_scores(inp)
+    if quantised:
+        S = (np.round(S * 16.0) / 16.0).astype(np.float32)
+    for mode in ("up", "down", "nearest"):
+        layer = DeviceLayer(inp, round_mode=mode, scores_in=S)
+        layer.route()
+        torch.cuda.synchronize()
+        idx, rdir, R = oracle_routing(S, cfg.K, mode, m_tile)
         check_routing(layer, R, idx, rdir)
 
 
