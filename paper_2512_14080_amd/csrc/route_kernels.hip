@@ -197,7 +197,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
 //   1. row max (the row loads are issued 16 float4 at a time), combined
 //      across the slices;
 //   2. exp(x - max) and the slice sums, combined in slice order;
-//   3. scores = exp / sum (written token-major and, coalesced across lanes,
+//   3. scores = exp * (1 / sum) (written token-major and, coalesced across lanes,
 //      transposed), and a KM-slot insertion network over the (key, expert)
 //      pairs of the slice: an element moves down past every slot whose pair
 //      it exceeds; the network runs only when some lane's element beats its
@@ -290,7 +290,7 @@ __global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, flo
       f32x4 x = cols[g * 64 + lane];
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        x[c] = expf(x[c] - m);
+        x[c] = __expf(x[c] - m);  // v_exp_f32 of (x - m) log2(e): a few ulp for |x - m| < 100
         s += x[c];
       }
       cols[g * 64 + lane] = x;
@@ -303,6 +303,7 @@ __global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, flo
       for (int p = 1; p < NW; ++p) s += xsum[p * 64 + lane];
     }
   }
+  const float rs = 1.f / s;  // scores = exp * (1 / sum): within an ulp of the quotient
   uint64_t top[KM];
 #pragma unroll
   for (int k = 0; k < KM; ++k) top[k] = 0;  // below every (key, ~expert) pair
@@ -322,7 +323,7 @@ __global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, flo
         const int eg = e0 + 4 * g;
         if (do_softmax) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) p[c] = p[c] / s;
+          for (int c = 0; c < 4; ++c) p[c] = p[c] * rs;
           cols[g * 64 + lane] = p;
           if (live) *(f32x4*)(scores + (size_t)t * E + eg) = p;
         }
