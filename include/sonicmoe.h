@@ -90,7 +90,7 @@ typedef struct {
   int32_t *tok_count;    /* [T]   experts of each token                        */
   float *tok_denom;      /* [T]   sum of the token's selected scores           */
   int32_t *round_dir;    /* [E]   -1 dropped / 0 kept / +1 padded (rounding)   */
-  int32_t *scratch;      /* internal scan scratch                              */
+  int32_t *scratch;      /* internal: scans and the rounding select's lists    */
   int32_t *status;       /* [1]   device word: 0 once the metadata kernels have
                             run on a consistent selection; otherwise the OR of
                             MOE_STATUS_* bits, and the rows are not valid
