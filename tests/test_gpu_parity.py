@@ -256,13 +256,15 @@ def test_rounding_selection_sizes_and_ties(T, quantised):
         check_routing(layer, R, idx, rdir)
 
 
-@pytest.mark.parametrize("T,m_tile", [(5000, 8), (20000, 256), (40000, 256)])
+@pytest.mark.parametrize("T,m_tile", [(5000, 8), (20000, 256), (40000, 256), (65536, 128), (65537, 128)])
 @pytest.mark.parametrize("quantised", [False, True])
 def test_rounding_selection_tiles(T, m_tile, quantised):
     """The smallest and largest M_tile: two-level selection with one and two
     slot groups in the second level (T = 5000 / 20000), and the one-block
     form for rows whose chunk picks exceed the second level (T = 40000 at
-    M_tile = 256)."""
+    M_tile = 256).  At M_tile = 128, T = 65536 is the largest row the two-level
+    form takes (1024 mask words in LDS, 4096 list entries) and T = 65537 the
+    smallest the one-block form takes."""
     torch = _torch()
     from paper_2512_14080_amd.layer import DeviceLayer
     cfg = W.MoEConfig("tiles", T=T, d=128, n=128, E=16, K=4, m_tile=m_tile)
