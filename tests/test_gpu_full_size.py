@@ -102,15 +102,19 @@ def test_7b_expert_biases_full_size():
     _full_size("7b", biases=True)
 
 
-@pytest.mark.parametrize("name", ["coarse", "paper-30b-e256k16"])
+@pytest.mark.parametrize("name", ["coarse", "paper-30b-e256k16", "paper-1.4b-e32k2", "paper-7b-e128k8",
+                                  "paper-120b-e64k4", "tr-d1536n256k8-e512"])
 def test_sampled_large_shapes(name):
     """Shapes where the full oracle is too slow: the coarse layer (T=16384,
-    d=4096, n=14336, E=8, K=2) and the finest 30B benchmark layer of the
-    paper's sweep (T=32768, d=4096, n=256, E=256, K=16, the wave-per-token
-    top-K), both with token rounding M_tile=128.  Routing is compared exactly
-    and outputs on samples the oracle computes one by one -- O and dX of
-    sampled tokens, dS of their rows, H of sampled rows, and whole columns of
-    dW1 / rows of dW2 of two experts."""
+    d=4096, n=14336, E=8, K=2); from the paper's benchmark sweep the finest 30B
+    layer (T=32768, d=4096, n=256, E=256, K=16, the wave-per-token top-K), the
+    coarsest 1.4B layer (T=40960, d=768, n=1024, E=32, K=2), the 7B layer at
+    its T=24576 and the coarsest 120B layer (d=4096, n=2048, E=64, K=4); and
+    the E=512 point of the token-rounding sweep (T=16384, d=1536, n=256, K=8).
+    All with token rounding M_tile=128.  Routing is compared exactly and
+    outputs on samples the oracle computes one by one -- O and dX of sampled
+    tokens, dS of their rows, H of sampled rows, and whole columns of dW1 /
+    rows of dW2 of two experts."""
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
