@@ -14,8 +14,8 @@ hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, in
 hipError_t launch_tc_metadata(const moe_routing& r, int T, int E, int K, bool counts_only, hipStream_t s);
 // counted: r.mask_prefix and r.counts are already written (by launch_round)
 hipError_t launch_metadata(const moe_routing& r, const float* scores_t, int T, int E, bool counted, hipStream_t s);
-// list: round_scratch_bytes(T, E) bytes (8-byte aligned) for the two-level
-// selection's lists (null: the one-workgroup-per-expert selection)
+// list: round_scratch_bytes(T, E) bytes (8-byte aligned) for the selection's
+// lists
 size_t round_scratch_bytes(int T, int E);
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
                         uint64_t* list, bool* counted, hipStream_t s);

@@ -182,7 +182,7 @@ size_t bwd_layout(const moe_dims& m, int64_t cap, char* base, BwdWs* w) {
   return off;
 }
 
-// byte offset of the two-level selection's lists in the routing scratch
+// byte offset of the rounding selection's lists in the routing scratch
 size_t round_lists_offset(const moe_dims& m) {
   const int W = (m.T + 63) / 64;
   return ((size_t)(m.E + 64 + 2 * (W + 1)) * 4 + 255) / 256 * 256;
@@ -230,8 +230,8 @@ size_t routing_layout(const moe_dims& m, int64_t cap, int flags, char* base, moe
   o->tok_denom = (float*)p;
   take((size_t)m.E * 4, &p);
   o->round_dir = (int32_t*)p;
-  // rounding needs [E], then per-word token sums and bases, then the lists of
-  // the two-level selection
+  // rounding needs [E], then per-word token sums and bases, then the
+  // selection's lists
   take(round_lists_offset(m) + smoe::round_scratch_bytes(m.T, m.E), &p);
   o->scratch = (int32_t*)p;
   take(4, &p);
@@ -397,7 +397,7 @@ int moe_round_tokens(moe_dims m, int32_t m_tile, int mode, const float* u, const
   tr->state = MOE_ROUTING_STATE_EMPTY;
   smoe::prof_begin(MOE_KC_ROUND, stream);
   bool counted = false;
-  uint64_t* list = smoe::round_scratch_bytes(m.T, m.E) ? (uint64_t*)((char*)tr->scratch + round_lists_offset(m)) : nullptr;
+  uint64_t* list = (uint64_t*)((char*)tr->scratch + round_lists_offset(m));
   hipError_t e = smoe::launch_round(*tc, *tr, u, m.T, m.E, m_tile, mode, list, &counted, stream);
   if (e == hipSuccess) e = smoe::launch_metadata(*tr, tc->scores_t, m.T, m.E, counted, stream);
   smoe::prof_end(MOE_KC_ROUND, stream);

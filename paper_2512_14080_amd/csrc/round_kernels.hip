@@ -7,9 +7,8 @@
 // selects the at most m_tile-1 tokens that change with a bitwise select on an
 // order-preserving integer image of the fp32 score, ties on the threshold
 // value broken by token index.  The result is the same set the full sort
-// would give.  Up to 65536 tokens the select runs in two levels (per
-// 2048-token chunk, then over the chunks' picks); beyond, one block per
-// expert selects from all its tokens.
+// would give.  The select runs in levels: per 2048-token chunk, then over
+// the chunks' picks.
 #include "device_common.h"
 #include "launch.h"
 
@@ -74,8 +73,6 @@ __device__ __forceinline__ uint32_t score_key(float x) {
   return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
-constexpr int kSelThreads = 1024;
-
 // 32 x 32 bit transpose in registers by recursive block swaps (the published
 // bit-matrix transpose, H. S. Warren, "Hacker's Delight", section 7-3):
 // afterwards A[b] bit i = bit b of the original A[i].
@@ -92,128 +89,7 @@ __device__ __forceinline__ void transpose32(uint32_t (&A)[32]) {
   }
 }
 
-// The any-T selection, for rows beyond what the two-level form below holds:
-// one block per expert.  Copies the TC mask row of expert e into the rounded
-// mask and flips the `need` selected bits:
-//   pad  (dir > 0): the need best non-TC tokens by (score desc, token asc);
-//   drop (dir < 0): the need worst TC tokens by (score asc, token desc).
-// Both become "the need largest keys" with key = score_key for pads and
-// ~score_key for drops, ties preferring low tokens for pads, high for drops.
-// Token t is owned by thread t % 1024 as its slot t / 1024; every pass of the
-// bitwise select re-reads the scores.
-__global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* __restrict__ tc_mask,
-                                                                uint64_t* __restrict__ tr_mask,
-                                                                const float* __restrict__ scores_t,
-                                                                int32_t* __restrict__ round_dir,
-                                                                const int32_t* __restrict__ need_arr,
-                                                                const int32_t* __restrict__ counts,
-                                                                const float* __restrict__ u, int M, int mode, int T,
-                                                                int W) {
-  constexpr int kWaves = kSelThreads / 64;
-  __shared__ int lds[kWaves];
-  __shared__ int cnt_lds[2][kWaves];  // per-wave counts of a pass, double-buffered by pass parity
-  const int e = blockIdx.x;
-  const uint64_t* src = tc_mask + (size_t)e * W;
-  uint64_t* dst = tr_mask + (size_t)e * W;
-  // the decision: taken here unless a Balance-f pass (sequential over
-  // experts) made it already (need_arr non-null)
-  int dir, need;
-  if (need_arr) {
-    dir = round_dir[e];
-    need = need_arr[e];
-  } else {
-    tr_decide_one(counts[e], mode == MOE_ROUND_STOCHASTIC ? u[e] : 0.f, T, M, mode, &dir, &need);
-    if (threadIdx.x == 0) round_dir[e] = dir;
-  }
-  if (dir == 0 || need == 0) {
-    for (int w = threadIdx.x; w < W; w += kSelThreads) dst[w] = src[w];
-    return;
-  }
-  const float* S = scores_t + (size_t)e * T;
-  const bool want_set = dir < 0;  // candidates: TC tokens for drops, non-TC for pads
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int slots = (T + kSelThreads - 1) / kSelThreads;
-
-  // key of slot i of this thread; cand tells whether the token is a candidate
-  auto load_key = [&](int i, bool& cand) -> uint32_t {
-    const int t = i * kSelThreads + threadIdx.x;
-    cand = false;
-    if (t >= T) return 0u;
-    cand = (((src[t >> 6] >> (t & 63)) & 1ull) != 0) == want_set;
-    if (!cand) return 0u;
-    const uint32_t k = score_key(S[t]);
-    return dir < 0 ? ~k : k;
-  };
-  // number of candidates in the block whose key k has (k >> sh) == v.  One
-  // barrier per call: the counts of consecutive calls go to alternating slots,
-  // and a slot is only rewritten after the next call's barrier, which every
-  // wave reaches after reading it.
-  int parity = 0;
-  auto count_eq = [&](uint32_t v, int sh) -> int {
-    int cnt = 0;
-    for (int i = 0; i < slots; ++i) {
-      bool c;
-      const uint32_t k = load_key(i, c);
-      cnt += __popcll(__ballot(c && (k >> sh) == v));
-    }
-    if (lane == 0) cnt_lds[parity][wave] = cnt;
-    __syncthreads();
-    int total = 0;
-#pragma unroll
-    for (int q = 0; q < kWaves; ++q) total += cnt_lds[parity][q];
-    parity ^= 1;
-    return total;
-  };
-
-  // Bitwise select (MSB first) of tau, the need-th largest candidate key:
-  // keep a bit set when the candidates extending the prefix with a 1 still
-  // hold `remaining` keys, else count them as taken and clear it.
-  uint32_t prefix = 0;
-  int remaining = need;
-  for (int bit = 31; bit >= 0; --bit) {
-    const int total = count_eq((prefix >> bit) | 1u, bit);
-    if (total >= remaining)
-      prefix |= 1u << bit;
-    else
-      remaining -= total;
-  }
-  const int nties = count_eq(prefix, 0);
-  const uint32_t tau = prefix;
-
-  // Marking pass in ascending token order: slot i of wave w is word 16i + w.
-  // Every candidate with key > tau flips; of the nties ties on tau, the
-  // `remaining` first ones flip for pads and the last ones for drops.  A
-  // tie's ascending rank comes from ballots, a scan over the waves and a
-  // carry over slots.
-  const int first_tie = dir > 0 ? 0 : nties - remaining;
-  const int last_tie = dir > 0 ? remaining : nties;  // flip ranks in [first_tie, last_tie)
-  int carry = 0;
-  for (int i = 0; i < slots; ++i) {
-    bool cand;
-    const uint32_t k = load_key(i, cand);
-    const int w = i * kWaves + wave;
-    const bool gt = cand && k > tau;
-    const bool tie = cand && k == tau;
-    const uint64_t ties = __ballot(tie);
-    if (lane == 0) lds[wave] = __popcll(ties);
-    __syncthreads();
-    int base = carry, total = 0;
-#pragma unroll
-    for (int q = 0; q < kWaves; ++q) {
-      const int c = lds[q];
-      if (q < wave) base += c;
-      total += c;
-    }
-    const int rank = base + __popcll(ties & lanemask_lt());
-    const bool flip = gt || (tie && rank >= first_tie && rank < last_tie);
-    const uint64_t flips = __ballot(flip);
-    if (w < W && lane == 0) dst[w] = src[w] ^ flips;
-    carry += total;
-    __syncthreads();
-  }
-}
-
-// ------------------------------------------------ two-level selection
+// ------------------------------------------------ selection in levels
 // The need largest candidate keys of an expert, with ties on the key broken by
 // token (low first for pads, high first for drops), form a strict total order
 // on the candidates.  Under a strict order the global top-need set lies in the
@@ -221,18 +97,25 @@ __global__ __launch_bounds__(kSelThreads) void tr_select_kernel(const uint64_t* 
 // the global set outranks all but fewer than need candidates, so also within
 // its own part.  Level 1 gives every kTrChunk tokens of an expert one wave,
 // which selects its chunk's top-need with wave reductions only (no workgroup
-// barrier) and lists the chosen (key, token) pairs in token order; level 2
-// selects the top-need of those lists per expert with one wave and writes the
-// rounded mask row, its word prefixes and the count.  The selection work of
-// an expert is spread over T / kTrChunk waves instead of one CU.
-constexpr int kTrChunk = 2048;       // tokens per level-1 wave: 32 slots x 64 lanes
-constexpr int kTrMaxTokens = 65536;  // level 2 keeps the W <= 1024 mask words of a row in LDS
+// barrier) and lists the chosen (key, token) pairs in token order, M entries
+// per chunk.  While an expert's lists hold more than kTrMergeMax entries, a
+// reduce level selects again per kTrChunk entries (positions keep token
+// order).  The final level selects the top-need of the remaining entries per
+// expert with one wave and writes the rounded mask row, its word prefixes and
+// the count.  The selection work of an expert is spread over T / kTrChunk
+// waves instead of one CU.
+constexpr int kTrChunk = 2048;     // tokens (or list entries) per wave: 32 slots x 64 lanes
+constexpr int kTrMergeMax = 4096;  // list entries the final wave holds (64 slots per lane)
+constexpr int kTrRowWords = 1024;  // mask words per pass of the final level's LDS row
 
-// List space: m_tile <= 256 entries of 8 bytes per chunk of every expert.
+// entries of an expert's lists after a level that starts from n entries
+__host__ __device__ inline int64_t tr_level_entries(int64_t n, int M) { return (n + kTrChunk - 1) / kTrChunk * M; }
+
+// List space: two alternating list buffers sized for m_tile = 256 (level 1
+// lists in the first, the first reduce level's in the second).
 size_t round_scratch_bytes(int T, int E) {
-  if (T > kTrMaxTokens) return 0;
-  const size_t nch = (size_t)(T + kTrChunk - 1) / kTrChunk;
-  return (size_t)E * nch * 256 * 8;
+  const int64_t l1 = tr_level_entries(T, 256), l2 = tr_level_entries(l1, 256);
+  return (size_t)E * (size_t)(l1 + l2) * 8;
 }
 
 // Packed digit counts of a pass: each lane holds three 10-bit counts; the
@@ -377,9 +260,9 @@ __device__ __forceinline__ void tr_decision(int e, const int32_t* round_dir, con
 // Level 1: wave (e, c) selects the top-need candidates among tokens
 // [c * kTrChunk, (c + 1) * kTrChunk) of expert e and writes the M list
 // entries of its chunk at list[(e * nch + c) * M]: the chosen ones in token
-// order as (key << 32) | (chunk-local token << 1) | 1, then zeros (entry
-// bit 0 marks a pick).  Token 64 i + l of the chunk is slot i of lane l
-// (slot i is mask word 32 c + i).
+// order as (key << 32) | (token << 1) | 1, then zeros (entry bit 0 marks a
+// pick).  Token 64 i + l of the chunk is slot i of lane l (slot i is mask
+// word 32 c + i).
 __global__ __launch_bounds__(256) void tr_local_kernel(const uint64_t* __restrict__ tc_mask,
                                                        const float* __restrict__ scores_t,
                                                        const int32_t* __restrict__ round_dir,
@@ -423,28 +306,70 @@ __global__ __launch_bounds__(256) void tr_local_kernel(const uint64_t* __restric
   for (int i = 0; i < 32; ++i) {
     const bool s = (sel[0] >> i) & 1u;
     const uint64_t b = __ballot(s);
-    if (s) out[n + __popcll(b & lanemask_lt())] = ((uint64_t)kept[i] << 32) | ((uint32_t)(64 * i + lane) << 1) | 1u;
+    if (s)
+      out[n + __popcll(b & lanemask_lt())] =
+          ((uint64_t)kept[i] << 32) | ((uint32_t)(c * kTrChunk + 64 * i + lane) << 1) | 1u;
     n += __popcll(b);
   }
   for (int q = n + lane; q < M; q += 64) out[q] = 0ull;
 }
 
-// Level 2, one workgroup of 4 waves per expert.  Wave 0 selects the top-need
-// of the expert's level-1 picks (entry q of chunk c at position c * M + q,
-// i.e. token order; 32 G slots per lane) while the others copy the TC mask
-// row into LDS; the chosen tokens' bits are flipped there, and the row goes
-// out with its word prefixes and count.
+// Reduce level: wave (e, c) selects the top-need entries among positions
+// [c * kTrChunk, (c + 1) * kTrChunk) of expert e's nin input entries and
+// writes M output entries at out[(e * ngroups + c) * M], in position order.
+__global__ __launch_bounds__(256) void tr_reduce_kernel(const int32_t* __restrict__ round_dir,
+                                                        const int32_t* __restrict__ need_arr,
+                                                        const int32_t* __restrict__ counts,
+                                                        const float* __restrict__ u, int M, int mode, int T, int E,
+                                                        int64_t nin, int ngroups, const uint64_t* __restrict__ in,
+                                                        uint64_t* __restrict__ out) {
+  const int gw = __builtin_amdgcn_readfirstlane((int)(blockIdx.x * 4 + (threadIdx.x >> 6)));
+  const int e = gw / ngroups, c = gw - e * ngroups;
+  if (e >= E) return;
+  int dir, need;
+  tr_decision(e, round_dir, need_arr, counts, u, T, M, mode, &dir, &need);
+  if (dir == 0 || need == 0) return;
+  const int lane = lane_id();
+  const uint64_t* lst = in + (size_t)e * nin;
+  uint32_t keys[1][32], cm[1] = {0u};
+  uint64_t ent[32];
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const int64_t p = (int64_t)c * kTrChunk + 64 * i + lane;
+    ent[i] = p < nin ? lst[p] : 0ull;
+    keys[0][i] = (uint32_t)(ent[i] >> 32);
+    cm[0] |= (uint32_t)(ent[i] & 1u) << i;
+  }
+  uint32_t sel[1];
+  wave_select<1>(keys, cm, need, dir > 0, sel);
+  uint64_t* o = out + (size_t)gw * M;
+  int n = 0;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    const bool s = (sel[0] >> i) & 1u;
+    const uint64_t b = __ballot(s);
+    if (s) o[n + __popcll(b & lanemask_lt())] = ent[i];
+    n += __popcll(b);
+  }
+  for (int q = n + lane; q < M; q += 64) o[q] = 0ull;
+}
+
+// Final level, one workgroup of 4 waves per expert.  Wave 0 selects the
+// top-need of the expert's nin <= 64 * 32 G remaining entries (position order
+// is token order); then the TC mask row is copied through LDS kTrRowWords
+// words at a time, the chosen tokens' bits are flipped there, and the rounded
+// row goes out with its word prefixes and count.
 template <int G>
 __global__ __launch_bounds__(256) void tr_merge_kernel(const uint64_t* __restrict__ tc_mask,
                                                        uint64_t* __restrict__ tr_mask,
                                                        int32_t* __restrict__ round_dir,
                                                        const int32_t* __restrict__ need_arr,
                                                        const int32_t* __restrict__ counts, const float* __restrict__ u,
-                                                       int M, int mode, int T, int W, int nch,
+                                                       int M, int mode, int T, int W, int nin,
                                                        const uint64_t* __restrict__ list,
                                                        int32_t* __restrict__ prefix_out,
                                                        int32_t* __restrict__ counts_out) {
-  __shared__ uint64_t row[kTrMaxTokens / 64];
+  __shared__ uint64_t row[kTrRowWords];
   __shared__ int scan_lds[4];
   const int e = blockIdx.x;
   const int wave = threadIdx.x >> 6, lane = lane_id();
@@ -452,12 +377,12 @@ __global__ __launch_bounds__(256) void tr_merge_kernel(const uint64_t* __restric
   tr_decision(e, round_dir, need_arr, counts, u, T, M, mode, &dir, &need);
   if (!need_arr && threadIdx.x == 0) round_dir[e] = dir;
   const uint64_t* src = tc_mask + (size_t)e * W;
+  uint64_t* dst = tr_mask + (size_t)e * W;
   const bool select = dir != 0 && need != 0;
   uint32_t sel[G];
   int tok[G][32];
   if (select && wave == 0) {
-    const uint64_t* lst = list + (size_t)e * nch * M;
-    const int np = nch * M;  // positions; entry p of the expert's lists
+    const uint64_t* lst = list + (size_t)e * nin;
     uint32_t keys[G][32], cm[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -465,44 +390,50 @@ __global__ __launch_bounds__(256) void tr_merge_kernel(const uint64_t* __restric
 #pragma unroll
       for (int i = 0; i < 32; ++i) {
         const int p = (32 * g + i) * 64 + lane;
-        const uint64_t v = p < np ? lst[p] : 0ull;
-        const int ch = p / M;  // M is a power of two
-        tok[g][i] = ch * kTrChunk + (int)(((uint32_t)v >> 1) & (kTrChunk - 1));
+        const uint64_t v = p < nin ? lst[p] : 0ull;
+        tok[g][i] = (int)((uint32_t)v >> 1);
         keys[g][i] = (uint32_t)(v >> 32);
         cm[g] |= (uint32_t)(v & 1u) << i;
       }
     }
     wave_select<G>(keys, cm, need, dir > 0, sel);
   }
-  for (int w = threadIdx.x; w < W; w += 256) row[w] = src[w];
-  __syncthreads();
-  if (select && wave == 0) {
+  int carry = 0;
+  for (int w0 = 0; w0 < W; w0 += kTrRowWords) {
+    const int nw = min(kTrRowWords, W - w0);
+    for (int w = threadIdx.x; w < nw; w += 256) row[w] = src[w0 + w];
+    __syncthreads();
+    if (select && wave == 0) {
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+      for (int g = 0; g < G; ++g)
 #pragma unroll
-      for (int i = 0; i < 32; ++i)
-        if ((sel[g] >> i) & 1u) atomicXor((unsigned long long*)&row[tok[g][i] >> 6], 1ull << (tok[g][i] & 63));
+        for (int i = 0; i < 32; ++i) {
+          const int w = (tok[g][i] >> 6) - w0;
+          if (((sel[g] >> i) & 1u) && w >= 0 && w < nw)
+            atomicXor((unsigned long long*)&row[w], 1ull << (tok[g][i] & 63));
+        }
+    }
+    __syncthreads();
+    // four consecutive words per thread
+    const int q0 = 4 * threadIdx.x;
+    int pc[4], sum = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t v = q0 + k < nw ? row[q0 + k] : 0ull;
+      if (q0 + k < nw) dst[w0 + q0 + k] = v;
+      pc[k] = __popcll(v);
+      sum += pc[k];
+    }
+    int total;
+    int ex = carry + block_excl_scan<256>(sum, &total, scan_lds);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (q0 + k < nw) prefix_out[(size_t)e * W + w0 + q0 + k] = ex;
+      ex += pc[k];
+    }
+    carry += total;  // block_excl_scan ends with a barrier: row may be refilled
   }
-  __syncthreads();
-  // four consecutive words per thread (W <= 1024)
-  uint64_t* dst = tr_mask + (size_t)e * W;
-  const int w0 = 4 * threadIdx.x;
-  int pc[4], sum = 0;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint64_t v = w0 + k < W ? row[w0 + k] : 0ull;
-    if (w0 + k < W) dst[w0 + k] = v;
-    pc[k] = __popcll(v);
-    sum += pc[k];
-  }
-  int total;
-  int ex = block_excl_scan<256>(sum, &total, scan_lds);
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (w0 + k < W) prefix_out[(size_t)e * W + w0 + k] = ex;
-    ex += pc[k];
-  }
-  if (threadIdx.x == 0) counts_out[e] = total;
+  if (threadIdx.x == 0) counts_out[e] = carry;
 }
 
 hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, int T, int E, int M, int mode,
@@ -514,25 +445,31 @@ hipError_t launch_round(const moe_routing& tc, moe_routing& tr, const float* u, 
     need = tr.scratch;
     tr_decide_kernel<<<dim3(1), dim3(256), 0, s>>>(tc.counts, u, tr.round_dir, need, T, E, M, mode);
   }
+  if (list == nullptr) return hipErrorInvalidValue;
   const int nch = (T + kTrChunk - 1) / kTrChunk;
-  // two levels where the level-2 wave holds every list entry in 64 slots per
-  // lane and the rounding scratch has room for the lists
-  if (T <= kTrMaxTokens && (int64_t)nch * M <= 64 * 64 && list != nullptr) {
-    const int waves = E * nch;
-    tr_local_kernel<<<dim3((waves + 3) / 4), dim3(256), 0, s>>>(tc.mask, tc.scores_t, tr.round_dir, need, tc.counts,
-                                                                u, M, mode, T, E, tr.words, nch, list);
-    if (nch * M <= 64 * 32)
-      tr_merge_kernel<1><<<dim3(E), dim3(256), 0, s>>>(tc.mask, tr.mask, tr.round_dir, need, tc.counts, u, M, mode, T,
-                                                       tr.words, nch, list, tr.mask_prefix, tr.counts);
-    else
-      tr_merge_kernel<2><<<dim3(E), dim3(256), 0, s>>>(tc.mask, tr.mask, tr.round_dir, need, tc.counts, u, M, mode, T,
-                                                       tr.words, nch, list, tr.mask_prefix, tr.counts);
-    *counted = true;
-    return hipGetLastError();
+  tr_local_kernel<<<dim3(((int64_t)E * nch + 3) / 4), dim3(256), 0, s>>>(tc.mask, tc.scores_t, tr.round_dir, need,
+                                                                         tc.counts, u, M, mode, T, E, tr.words, nch,
+                                                                         list);
+  // reduce levels while the lists exceed what the final wave holds; the
+  // lists alternate between the two buffers
+  uint64_t* buf[2] = {list, list + (size_t)E * tr_level_entries(T, 256)};
+  int cur = 0;
+  int64_t nin = (int64_t)nch * M;
+  while (nin > kTrMergeMax) {
+    const int ngroups = (int)((nin + kTrChunk - 1) / kTrChunk);
+    tr_reduce_kernel<<<dim3(((int64_t)E * ngroups + 3) / 4), dim3(256), 0, s>>>(tr.round_dir, need, tc.counts, u, M,
+                                                                                mode, T, E, nin, ngroups, buf[cur],
+                                                                                buf[cur ^ 1]);
+    cur ^= 1;
+    nin = (int64_t)ngroups * M;
   }
-  tr_select_kernel<<<dim3(E), dim3(kSelThreads), 0, s>>>(tc.mask, tr.mask, tc.scores_t, tr.round_dir, need, tc.counts,
-                                                         u, M, mode, T, tr.words);
-  *counted = false;
+  if (nin <= kTrMergeMax / 2)
+    tr_merge_kernel<1><<<dim3(E), dim3(256), 0, s>>>(tc.mask, tr.mask, tr.round_dir, need, tc.counts, u, M, mode, T,
+                                                     tr.words, (int)nin, buf[cur], tr.mask_prefix, tr.counts);
+  else
+    tr_merge_kernel<2><<<dim3(E), dim3(256), 0, s>>>(tc.mask, tr.mask, tr.round_dir, need, tc.counts, u, M, mode, T,
+                                                     tr.words, (int)nin, buf[cur], tr.mask_prefix, tr.counts);
+  *counted = true;
   return hipGetLastError();
 }
 

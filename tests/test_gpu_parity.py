@@ -259,12 +259,12 @@ def test_rounding_selection_sizes_and_ties(T, quantised):
 @pytest.mark.parametrize("T,m_tile", [(5000, 8), (20000, 256), (40000, 256), (65536, 128), (65537, 128)])
 @pytest.mark.parametrize("quantised", [False, True])
 def test_rounding_selection_tiles(T, m_tile, quantised):
-    """The smallest and largest M_tile: two-level selection with one and two
-    slot groups in the second level (T = 5000 / 20000), and the one-block
-    form for rows whose chunk picks exceed the second level (T = 40000 at
-    M_tile = 256).  At M_tile = 128, T = 65536 is the largest row the two-level
-    form takes (1024 mask words in LDS, 4096 list entries) and T = 65537 the
-    smallest the one-block form takes."""
+    """The smallest and largest M_tile: selection in two levels with one and
+    two slot groups in the final one (T = 5000 / 20000), and with a reduce
+    level between them where the chunks' picks exceed what the final wave
+    holds (T = 40000 at M_tile = 256).  At M_tile = 128, T = 65536 is the
+    largest row without a reduce level (4096 picks) and T = 65537 the smallest
+    with one, and the first whose mask row takes two LDS passes."""
     torch = _torch()
     from paper_2512_14080_amd.layer import DeviceLayer
     cfg = W.MoEConfig("tiles", T=T, d=128, n=128, E=16, K=4, m_tile=m_tile)
