@@ -30,8 +30,8 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "l2_fabric_traffic_7b_tr128.md"
 KERNEL_CLASS_OF = [("OpUp<", "up_proj"), ("OpDown<", "down_proj"), ("OpDH<", "dH"), ("OpDW2<", "dW2"),
                    ("OpDXt<", "dXtilde"), ("OpDW1<", "dW1"), ("OpDWr<", "dWr"), ("OpRouter<", "router_gemm"),
                    ("agg_o_kernel", "aggregate_O"), ("agg_dx_kernel", "aggregate_dX"),
-                   ("topk_lane_kernel", "topk"), ("topk_route_kernel", "topk"), ("tr_select_kernel", "tr_select"),
-                   ("tr_local_kernel", "tr_local"), ("tr_merge_kernel", "tr_merge"),
+                   ("topk_lane_kernel", "topk"), ("topk_route_kernel", "topk"),
+                   ("tr_local_kernel", "tr_local"), ("tr_reduce_kernel", "tr_reduce"), ("tr_merge_kernel", "tr_merge"),
                    ("token_count_kernel", "token_count"), ("token_place_kernel", "token_place")]
 
 
