@@ -187,6 +187,22 @@ def test_single_token_and_one_hot_expert():
     assert R.counts[3] == 200
 
 
+@pytest.mark.parametrize("T,mode", [(1, "nearest"), (10, "down")])
+def test_rounding_that_drops_every_row(T, mode):
+    """Token rounding can leave no rows at all (T below M_tile: every expert's
+    ceiling exceeds T, so every expert is rounded down to zero).  The layer
+    then runs on an empty routing: O, dX, the weight gradients and the router
+    gradients are exactly zero (every output is written), with the routing
+    itself matching the oracle."""
+    inp, S, layer = run_layer(TINY, 8, T, mode, eb=expert_biases(TINY, 8))
+    idx, rdir, R = oracle_routing(S, TINY.K, mode, TINY.m_tile)
+    assert R.P == 0
+    check_routing(layer, R, idx, rdir)
+    for name in ("O", "dX", "dW1", "dW2", "dWr", "dbias", "db1", "db2"):
+        v = getattr(layer, name).float().cpu().numpy()
+        assert np.all(v == 0), (name, float(np.abs(v).max()))
+
+
 def test_device_router_matches_oracle_scores():
     torch = _torch()
     from paper_2512_14080_amd.layer import DeviceLayer
