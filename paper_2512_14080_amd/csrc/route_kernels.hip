@@ -188,7 +188,7 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
   }
 }
 
-// Lane-per-token selection (K <= KM <= 8; E a multiple of 4 * NW, E <= 256).
+// Lane-per-token selection (K <= KM <= 16; E a multiple of 4 * NW, E <= 256).
 // A workgroup owns the 64 tokens of one membership word, lane l token 64w + l,
 // and its NW waves split the experts into NW contiguous slices, so the
 // per-token work is ordinary per-lane arithmetic instead of wave-wide
@@ -742,7 +742,7 @@ static size_t topk_lds_bytes(int E, int K, bool stash) {
 
 hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, int32_t* topk_idx, float* topk_w,
                              uint64_t* mask, int T, int E, int K, int W, int do_softmax, hipStream_t s) {
-  if (E % 4 == 0 && E <= 256 && K <= 8 && K <= E) {
+  if (E % 4 == 0 && E <= 256 && K <= 16 && K <= E) {
     // LDS beyond the default 64 KB of dynamic LDS is granted per kernel
 #define SMOE_TOPK_LANE(KM, NW)                                                                                    \
   do {                                                                                                            \
@@ -761,8 +761,10 @@ hipError_t launch_topk_route(const float* in, float* scores, float* scores_t, in
       if (four) SMOE_TOPK_LANE(2, 4); else SMOE_TOPK_LANE(2, 1);
     } else if (K <= 4) {
       if (four) SMOE_TOPK_LANE(4, 4); else SMOE_TOPK_LANE(4, 1);
-    } else {
+    } else if (K <= 8) {
       if (four) SMOE_TOPK_LANE(8, 4); else SMOE_TOPK_LANE(8, 1);
+    } else {
+      if (four) SMOE_TOPK_LANE(16, 4); else SMOE_TOPK_LANE(16, 1);
     }
 #undef SMOE_TOPK_LANE
     return hipGetLastError();

@@ -159,10 +159,13 @@ def test_k_equals_e_and_k_one():
 
 
 def test_wave_per_token_topk_shapes():
-    """Shapes outside the lane-per-token top-K (E > 256, K > 8) take the
-    wave-per-token kernel; the routing and the layer still match."""
+    """E > 256 takes the wave-per-token top-K (here with K = 3 and K = 12);
+    K in (8, 16] at E <= 256 takes the lane-per-token kernel's 16-slot form
+    (K = 10, and K = E = 16).  The routing and the layer still match."""
     check_layer(W.MoEConfig("e264", T=300, d=128, n=64, E=264, K=3, m_tile=16), seed=13)
+    check_layer(W.MoEConfig("e264k12", T=300, d=128, n=64, E=264, K=12, m_tile=16), seed=16, round_mode="nearest")
     check_layer(W.MoEConfig("k10", T=300, d=128, n=64, E=16, K=10, m_tile=16), seed=14, round_mode="nearest")
+    check_layer(W.MoEConfig("k16", T=300, d=128, n=64, E=16, K=16, m_tile=16), seed=17)
 
 
 def test_weight_gradients_over_row_chunks():
