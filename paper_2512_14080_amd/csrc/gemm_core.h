@@ -459,9 +459,22 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   const int wm0 = Cfg::wave_m(wave) * (BM / Cfg::WM);
   const int wn0 = Cfg::wave_n(wave) * (BN / Cfg::WN);
   constexpr int kPerStage = Cfg::QM + Cfg::QN;  // DMA ops per wave per stage
-  // weight-gradient GEMMs spread each stage's DMA over its sub-steps; the
-  // others issue it at once and let rowless waves skip their MFMAs
+  // The next stage's DMA is interleaved with the MFMAs: instruction d goes
+  // just before MFMA number kDmaStride * d of the step.  A wave cannot issue
+  // past a DMA instruction until the CU's texture path accepts it, so a burst
+  // of a whole stage at the top of the step keeps every wave from issuing
+  // MFMAs meanwhile; one instruction every few MFMAs lets the other wave of
+  // the SIMD keep the matrix pipe busy while one waits.  Every 2nd MFMA puts
+  // the whole stage in the first half of the step, so it still has half a
+  // step to land from the Infinity Cache or HBM.
+  constexpr int kMfmaPerStep = Cfg::SUB * Cfg::RM * Cfg::RN;
+  constexpr int kDmaStride = kMfmaPerStep >= 2 * kPerStage ? 2 : 1;
+  // The weight-gradient GEMMs (k outer on both sides: gathered k rows, whose
+  // addresses take more registers) issue a quarter of the stage before each
+  // sub-step instead, with two sets of fragments, which they hold without
+  // spilling.
   constexpr bool kSpreadDma = Op::M_MODE == KOUTER && Op::N_MODE == KOUTER;
+  static_assert(kDmaStride * (kPerStage - 1) < kMfmaPerStep, "every DMA instruction has an MFMA after it");
 
   // stages 0 .. S-2 of a tile, and the row indices of stage S-1 (gathered k)
   auto prologue = [&](const TileInfo& t, MSide& a, NSide& b) {
@@ -539,51 +552,73 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
       const char* cur = smem + (kt % S) * Cfg::STAGE_BYTES;
       const char* lm = cur;
       const char* ln = cur + Cfg::M_BYTES;
-      // fragments of sub-step s+1 are read while the MFMAs of sub-step s issue
-      bf16x8 fm[2][Cfg::RM], fn[2][Cfg::RN];
-      auto mfma_substep = [&](int s) {
-        const int cb = s & 1, nb = cb ^ 1;
-        if (s + 1 < SUB) {
-#pragma unroll
-          for (int i = 0; i < Cfg::RM; ++i) fm[nb][i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
-#pragma unroll
-          for (int j = 0; j < Cfg::RN; ++j) fn[nb][j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
-        }
-#pragma unroll
-        for (int i = 0; i < Cfg::RM; ++i)
-#pragma unroll
-          for (int j = 0; j < Cfg::RN; ++j)
-            acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[cb][j], fm[cb][i], acc.acc[i][j], 0, 0, 0);
+      // DMA instruction d of this wave's share of the next stage
+      auto issue_one = [&](int d) {
+        if (d < Cfg::QM)
+          ms.issue(st_next, knext * BK, d, Cfg::QM);
+        else
+          ns.issue(st_next + Cfg::M_BYTES, knext * BK, d - Cfg::QM, Cfg::QN);
       };
-      auto first_frags = [&]() {
+      if constexpr (kSpreadDma) {
+        // fragments of sub-step s+1 are read while the MFMAs of sub-step s issue
+        bf16x8 fm[2][Cfg::RM], fn[2][Cfg::RN];
 #pragma unroll
         for (int i = 0; i < Cfg::RM; ++i) fm[0][i] = MSide::frag(lm, wm0 + 32 * i, 0);
 #pragma unroll
         for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = NSide::frag(ln, wn0 + 32 * j, 0);
-      };
-      if constexpr (kSpreadDma) {
-        // the next stage's DMA is spread over the sub-steps so the
-        // vector-memory issue does not stall the MFMA stream in one burst
-        first_frags();
 #pragma unroll
         for (int s = 0; s < SUB; ++s) {
           if (issue_next) {
             ms.issue(st_next, knext * BK, s, SUB);
             ns.issue(st_next + Cfg::M_BYTES, knext * BK, s, SUB);
           }
-          mfma_substep(s);
-        }
-      } else {
-        // the whole next stage is requested first: it has the full step to land
-        if (issue_next) {
-          ms.issue(st_next, knext * BK);
-          ns.issue(st_next + Cfg::M_BYTES, knext * BK);
-        }
-        if (active) {
-          first_frags();
+          const int cb = s & 1, nb = cb ^ 1;
+          if (s + 1 < SUB) {
 #pragma unroll
-          for (int s = 0; s < SUB; ++s) mfma_substep(s);
+            for (int i = 0; i < Cfg::RM; ++i) fm[nb][i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
+#pragma unroll
+            for (int j = 0; j < Cfg::RN; ++j) fn[nb][j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
+          }
+#pragma unroll
+          for (int i = 0; i < Cfg::RM; ++i)
+#pragma unroll
+            for (int j = 0; j < Cfg::RN; ++j)
+              acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[cb][j], fm[cb][i], acc.acc[i][j], 0, 0, 0);
         }
+      } else if (active) {
+        // One set of fragments: each is re-read for sub-step s+1 right after
+        // the last MFMA of sub-step s that uses it (A fragment i after MFMA
+        // (i, RN-1), B fragment j after MFMA (RM-1, j)), so its read has the
+        // rest of the sub-step to land and no second set of registers is
+        // needed.
+        bf16x8 fm[Cfg::RM], fn[Cfg::RN];
+#pragma unroll
+        for (int i = 0; i < Cfg::RM; ++i) fm[i] = MSide::frag(lm, wm0 + 32 * i, 0);
+#pragma unroll
+        for (int j = 0; j < Cfg::RN; ++j) fn[j] = NSide::frag(ln, wn0 + 32 * j, 0);
+#pragma unroll
+        for (int s = 0; s < SUB; ++s)
+#pragma unroll
+          for (int i = 0; i < Cfg::RM; ++i)
+#pragma unroll
+            for (int j = 0; j < Cfg::RN; ++j) {
+              const int c = (s * Cfg::RM + i) * Cfg::RN + j;  // MFMA number within the step
+              if (c % kDmaStride == 0 && c / kDmaStride < kPerStage) {
+                // the scheduling barriers keep the instruction between these MFMAs
+                __builtin_amdgcn_sched_barrier(0);
+                if (issue_next) issue_one(c / kDmaStride);
+                __builtin_amdgcn_sched_barrier(0);
+              }
+              acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc.acc[i][j], 0, 0, 0);
+              if (s + 1 < SUB) {
+                if (j == Cfg::RN - 1) fm[i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
+                if (i == Cfg::RM - 1) fn[j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
+              }
+            }
+      } else if (issue_next) {
+        // a wave without valid rows only requests its share of the stage
+        ms.issue(st_next, knext * BK);
+        ns.issue(st_next + Cfg::M_BYTES, knext * BK);
       }
       if (issue_next) {
         if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * BK);
