@@ -469,11 +469,11 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   // step to land from the Infinity Cache or HBM.
   constexpr int kMfmaPerStep = Cfg::SUB * Cfg::RM * Cfg::RN;
   constexpr int kDmaStride = kMfmaPerStep >= 2 * kPerStage ? 2 : 1;
-  // The weight-gradient GEMMs (k outer on both sides: gathered k rows, whose
-  // addresses take more registers) issue a quarter of the stage before each
-  // sub-step instead, with two sets of fragments, which they hold without
-  // spilling.
-  constexpr bool kSpreadDma = Op::M_MODE == KOUTER && Op::N_MODE == KOUTER;
+  // The weight-gradient GEMMs (k outer on both sides, gathered k rows) set up
+  // the next tile's sides after the k loop: that is plain arithmetic, and its
+  // registers would otherwise be held across the loop (with the interleaved
+  // DMA the 256x256 loop then spilled).
+  constexpr bool kLateSides = Op::M_MODE == KOUTER && Op::N_MODE == KOUTER;
   static_assert(kDmaStride * (kPerStage - 1) < kMfmaPerStep, "every DMA instruction has an MFMA after it");
 
   // stages 0 .. S-2 of a tile, and the row indices of stage S-1 (gathered k)
@@ -510,7 +510,10 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
     int idn = sched.id(k + 1);
     TileInfo tn;
     if (idn >= 0 && !Op::tile(p, idn, tn, sh + 4 * ((k + 1) & 1))) idn = -1;
-    if (idn >= 0) {
+    // Sides that gather rows by index DMA set up here, so those loads overlap
+    // this tile's k loop; the weight-gradient sides (plain arithmetic) set up
+    // after it, so their registers are free during the k loop.
+    if (idn >= 0 && !kLateSides) {
       Op::init_m(p, tn, ms_next);
       Op::init_n(p, tn, ns_next);
     }
@@ -559,33 +562,7 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
         else
           ns.issue(st_next + Cfg::M_BYTES, knext * BK, d - Cfg::QM, Cfg::QN);
       };
-      if constexpr (kSpreadDma) {
-        // fragments of sub-step s+1 are read while the MFMAs of sub-step s issue
-        bf16x8 fm[2][Cfg::RM], fn[2][Cfg::RN];
-#pragma unroll
-        for (int i = 0; i < Cfg::RM; ++i) fm[0][i] = MSide::frag(lm, wm0 + 32 * i, 0);
-#pragma unroll
-        for (int j = 0; j < Cfg::RN; ++j) fn[0][j] = NSide::frag(ln, wn0 + 32 * j, 0);
-#pragma unroll
-        for (int s = 0; s < SUB; ++s) {
-          if (issue_next) {
-            ms.issue(st_next, knext * BK, s, SUB);
-            ns.issue(st_next + Cfg::M_BYTES, knext * BK, s, SUB);
-          }
-          const int cb = s & 1, nb = cb ^ 1;
-          if (s + 1 < SUB) {
-#pragma unroll
-            for (int i = 0; i < Cfg::RM; ++i) fm[nb][i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
-#pragma unroll
-            for (int j = 0; j < Cfg::RN; ++j) fn[nb][j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
-          }
-#pragma unroll
-          for (int i = 0; i < Cfg::RM; ++i)
-#pragma unroll
-            for (int j = 0; j < Cfg::RN; ++j)
-              acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[cb][j], fm[cb][i], acc.acc[i][j], 0, 0, 0);
-        }
-      } else if (active) {
+      if (active) {
         // One set of fragments: each is re-read for sub-step s+1 right after
         // the last MFMA of sub-step s that uses it (A fragment i after MFMA
         // (i, RN-1), B fragment j after MFMA (RM-1, j)), so its read has the
@@ -627,6 +604,10 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
     }
     barrier_lds();  // every wave is done with the stage buffers
     if (idn >= 0) {
+      if constexpr (kLateSides) {
+        Op::init_m(p, tn, ms_next);
+        Op::init_n(p, tn, ns_next);
+      }
       // the last step's full drain covered the next tile's index loads
       ms_next.commit();
       ns_next.commit();
