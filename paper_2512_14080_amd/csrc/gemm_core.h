@@ -474,6 +474,13 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   // registers would otherwise be held across the loop (with the interleaved
   // DMA the 256x256 loop then spilled).
   constexpr bool kLateSides = Op::M_MODE == KOUTER && Op::N_MODE == KOUTER;
+  // The two-stage schedule with its barrier before the last sub-step (below)
+  // needs a stage's instructions to fit every second MFMA of one sub-step.
+  // It holds fragment addresses for both stage buffers across the step, and
+  // only the weight-gradient GEMMs stay spill-free with it (dW1 -4%, dW2 -2%;
+  // up, down and dH spilled 3-7 VGPRs and lost 2-7%, dX~ was unchanged).
+  constexpr bool kMidBarrier =
+      kLateSides && S == 2 && SUB >= 2 && Cfg::RM * Cfg::RN >= kPerStage && kPerStage % 2 == 0;
   static_assert(kDmaStride * (kPerStage - 1) < kMfmaPerStep, "every DMA instruction has an MFMA after it");
 
   // stages 0 .. S-2 of a tile, and the row indices of stage S-1 (gathered k)
@@ -527,79 +534,171 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
     bool gathered = false;
     if constexpr (Op::M_MODE == KOUTER) gathered = gathered || ms.gidx != nullptr;
     if constexpr (Op::N_MODE == KOUTER) gathered = gathered || ns.gidx != nullptr;
-    for (int kt = 0; kt < nk; ++kt) {
-      // stage kt is complete when at most (stages issued after it) * kPerStage
-      // ops remain.  At kt = 0 the previous epilogue's stores are younger than
-      // stage 0, and gathered index loads are younger than the DMA: full drain.
-      const int ahead = (kt == 0 || gathered) ? 0 : min(S - 2, nk - 1 - kt);
-      // stage 0: the younger prologue stages and epilogue stores may stay outstanding
-      constexpr int kYoung = (S - 2) * kPerStage;
-      constexpr int kYoungEpi = kYoung + EpiStores<Op>::value < 63 ? kYoung + EpiStores<Op>::value : 63;
-      if (kt == 0 && !gathered && nk >= S - 1 && (kYoung > 0 || prev_full)) {
-        if (prev_full)
-          wait_vm_barrier<kYoungEpi>();
-        else
-          wait_vm_barrier<kYoung>();
-      } else if (ahead >= 2)
-        wait_vm_barrier<(S >= 4 ? 2 : 0) * kPerStage>();
-      else if (ahead == 1)
-        wait_vm_barrier<(S >= 3 ? 1 : 0) * kPerStage>();
+    if constexpr (kMidBarrier) {
+      // Two stages, one barrier per step, placed before the last sub-step.
+      // By then every wave holds that sub-step's fragments in registers and
+      // has waited for its share of stage kt+1, so the barrier certifies both
+      // that stage kt's buffer is no longer read and that stage kt+1 is
+      // complete: stage kt+2's DMA (into stage kt's buffer) starts during the
+      // last sub-step, and the first fragments of step kt+1 are read while
+      // its MFMAs issue instead of after a barrier at the top of the step.
+      // A stage goes out in two halves, every second MFMA: the first in the
+      // last sub-step of the step before, the second in sub-step 0 (all of it
+      // in sub-step 0 of a tile's first step).
+      constexpr int kMf = Cfg::RM * Cfg::RN;  // MFMAs per sub-step
+      constexpr int kHalf = kPerStage / 2;
+      // stage 0 (the prologue's) is complete, and every wave is past the
+      // previous epilogue, whose stores may stay outstanding
+      if (!gathered && prev_full)
+        wait_vm_barrier<(EpiStores<Op>::value < 63 ? EpiStores<Op>::value : 63)>();
       else
         wait_vm_barrier<0>();
-      // with gathered k rows the wait above was a full drain, index loads included
       if constexpr (Op::M_MODE == KOUTER) ms.idx_commit();
       if constexpr (Op::N_MODE == KOUTER) ns.idx_commit();
-      const int knext = kt + S - 1;
-      const bool issue_next = knext < nk;
-      const uint32_t st_next = lds0 + (knext % S) * Cfg::STAGE_BYTES;
-      const char* cur = smem + (kt % S) * Cfg::STAGE_BYTES;
-      const char* lm = cur;
-      const char* ln = cur + Cfg::M_BYTES;
-      // DMA instruction d of this wave's share of the next stage
-      auto issue_one = [&](int d) {
+      // DMA instruction d of stage st (buffer st & 1)
+      auto issue_one = [&](int st, int d) {
+        const uint32_t dst = lds0 + (st & 1) * Cfg::STAGE_BYTES;
         if (d < Cfg::QM)
-          ms.issue(st_next, knext * BK, d, Cfg::QM);
+          ms.issue(dst, st * BK, d, Cfg::QM);
         else
-          ns.issue(st_next + Cfg::M_BYTES, knext * BK, d - Cfg::QM, Cfg::QN);
+          ns.issue(dst + Cfg::M_BYTES, st * BK, d - Cfg::QM, Cfg::QN);
       };
-      if (active) {
-        // One set of fragments: each is re-read for sub-step s+1 right after
-        // the last MFMA of sub-step s that uses it (A fragment i after MFMA
-        // (i, RN-1), B fragment j after MFMA (RM-1, j)), so its read has the
-        // rest of the sub-step to land and no second set of registers is
-        // needed.
-        bf16x8 fm[Cfg::RM], fn[Cfg::RN];
+      auto dma_at = [&](int st, int d) {
+        __builtin_amdgcn_sched_barrier(0);
+        issue_one(st, d);
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      bf16x8 fm[Cfg::RM], fn[Cfg::RN];
+      auto k_loop = [&](auto active_c) {
+        constexpr bool ACT = decltype(active_c)::value;
+        if constexpr (ACT) {
 #pragma unroll
-        for (int i = 0; i < Cfg::RM; ++i) fm[i] = MSide::frag(lm, wm0 + 32 * i, 0);
+          for (int i = 0; i < Cfg::RM; ++i) fm[i] = MSide::frag(smem, wm0 + 32 * i, 0);
 #pragma unroll
-        for (int j = 0; j < Cfg::RN; ++j) fn[j] = NSide::frag(ln, wn0 + 32 * j, 0);
+          for (int j = 0; j < Cfg::RN; ++j) fn[j] = NSide::frag(smem + Cfg::M_BYTES, wn0 + 32 * j, 0);
+        }
+        for (int kt = 0; kt < nk; ++kt) {
+          const char* cur = smem + (kt & 1) * Cfg::STAGE_BYTES;
+          const char* nxt = smem + ((kt + 1) & 1) * Cfg::STAGE_BYTES;
+          const bool has1 = kt + 1 < nk, has2 = kt + 2 < nk;
 #pragma unroll
-        for (int s = 0; s < SUB; ++s)
+          for (int s = 0; s < SUB; ++s)
 #pragma unroll
-          for (int i = 0; i < Cfg::RM; ++i)
+            for (int i = 0; i < Cfg::RM; ++i)
 #pragma unroll
-            for (int j = 0; j < Cfg::RN; ++j) {
-              const int c = (s * Cfg::RM + i) * Cfg::RN + j;  // MFMA number within the step
-              if (c % kDmaStride == 0 && c / kDmaStride < kPerStage) {
-                // the scheduling barriers keep the instruction between these MFMAs
-                __builtin_amdgcn_sched_barrier(0);
-                if (issue_next) issue_one(c / kDmaStride);
-                __builtin_amdgcn_sched_barrier(0);
+              for (int j = 0; j < Cfg::RN; ++j) {
+                const int cs = i * Cfg::RN + j;  // MFMA number within the sub-step
+                if (s == 0 && has1) {
+                  if (kt == 0) {
+                    if (cs < kPerStage) dma_at(kt + 1, cs);
+                  } else if (cs % 2 == 0 && kHalf + cs / 2 < kPerStage) {
+                    dma_at(kt + 1, kHalf + cs / 2);
+                  }
+                }
+                if (s == 1 && cs == 0 && has2) {
+                  // gathered k rows of stage kt+2: stage kt+1 no longer needs the index registers
+                  if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((kt + 2) * BK);
+                  if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((kt + 2) * BK);
+                }
+                if (s == SUB - 1 && cs == 0) {
+                  wait_vm_barrier<0>();
+                  if constexpr (Op::M_MODE == KOUTER) ms.idx_commit();
+                  if constexpr (Op::N_MODE == KOUTER) ns.idx_commit();
+                }
+                if (s == SUB - 1 && has2 && cs % 2 == 0 && cs / 2 < kHalf) dma_at(kt + 2, cs / 2);
+                if constexpr (ACT) {
+                  acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc.acc[i][j], 0, 0, 0);
+                  // each fragment is re-read right after its last use: the next
+                  // sub-step's from this stage, or sub-step 0 of the next step
+                  if (s + 1 < SUB || has1) {
+                    const char* b = s + 1 < SUB ? cur : nxt;
+                    const int sn = s + 1 < SUB ? s + 1 : 0;
+                    if (j == Cfg::RN - 1) fm[i] = MSide::frag(b, wm0 + 32 * i, sn);
+                    if (i == Cfg::RM - 1) fn[j] = NSide::frag(b + Cfg::M_BYTES, wn0 + 32 * j, sn);
+                  }
+                }
               }
-              acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc.acc[i][j], 0, 0, 0);
-              if (s + 1 < SUB) {
-                if (j == Cfg::RN - 1) fm[i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
-                if (i == Cfg::RM - 1) fn[j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
+        }
+      };
+      if (active)
+        k_loop(std::true_type{});
+      else
+        k_loop(std::false_type{});
+    } else {
+      for (int kt = 0; kt < nk; ++kt) {
+        // stage kt is complete when at most (stages issued after it) * kPerStage
+        // ops remain.  At kt = 0 the previous epilogue's stores are younger than
+        // stage 0, and gathered index loads are younger than the DMA: full drain.
+        const int ahead = (kt == 0 || gathered) ? 0 : min(S - 2, nk - 1 - kt);
+        // stage 0: the younger prologue stages and epilogue stores may stay outstanding
+        constexpr int kYoung = (S - 2) * kPerStage;
+        constexpr int kYoungEpi = kYoung + EpiStores<Op>::value < 63 ? kYoung + EpiStores<Op>::value : 63;
+        if (kt == 0 && !gathered && nk >= S - 1 && (kYoung > 0 || prev_full)) {
+          if (prev_full)
+            wait_vm_barrier<kYoungEpi>();
+          else
+            wait_vm_barrier<kYoung>();
+        } else if (ahead >= 2)
+          wait_vm_barrier<(S >= 4 ? 2 : 0) * kPerStage>();
+        else if (ahead == 1)
+          wait_vm_barrier<(S >= 3 ? 1 : 0) * kPerStage>();
+        else
+          wait_vm_barrier<0>();
+        // with gathered k rows the wait above was a full drain, index loads included
+        if constexpr (Op::M_MODE == KOUTER) ms.idx_commit();
+        if constexpr (Op::N_MODE == KOUTER) ns.idx_commit();
+        const int knext = kt + S - 1;
+        const bool issue_next = knext < nk;
+        const uint32_t st_next = lds0 + (knext % S) * Cfg::STAGE_BYTES;
+        const char* cur = smem + (kt % S) * Cfg::STAGE_BYTES;
+        const char* lm = cur;
+        const char* ln = cur + Cfg::M_BYTES;
+        // DMA instruction d of this wave's share of the next stage
+        auto issue_one = [&](int d) {
+          if (d < Cfg::QM)
+            ms.issue(st_next, knext * BK, d, Cfg::QM);
+          else
+            ns.issue(st_next + Cfg::M_BYTES, knext * BK, d - Cfg::QM, Cfg::QN);
+        };
+        if (active) {
+          // One set of fragments: each is re-read for sub-step s+1 right after
+          // the last MFMA of sub-step s that uses it (A fragment i after MFMA
+          // (i, RN-1), B fragment j after MFMA (RM-1, j)), so its read has the
+          // rest of the sub-step to land and no second set of registers is
+          // needed.
+          bf16x8 fm[Cfg::RM], fn[Cfg::RN];
+  #pragma unroll
+          for (int i = 0; i < Cfg::RM; ++i) fm[i] = MSide::frag(lm, wm0 + 32 * i, 0);
+  #pragma unroll
+          for (int j = 0; j < Cfg::RN; ++j) fn[j] = NSide::frag(ln, wn0 + 32 * j, 0);
+  #pragma unroll
+          for (int s = 0; s < SUB; ++s)
+  #pragma unroll
+            for (int i = 0; i < Cfg::RM; ++i)
+  #pragma unroll
+              for (int j = 0; j < Cfg::RN; ++j) {
+                const int c = (s * Cfg::RM + i) * Cfg::RN + j;  // MFMA number within the step
+                if (c % kDmaStride == 0 && c / kDmaStride < kPerStage) {
+                  // the scheduling barriers keep the instruction between these MFMAs
+                  __builtin_amdgcn_sched_barrier(0);
+                  if (issue_next) issue_one(c / kDmaStride);
+                  __builtin_amdgcn_sched_barrier(0);
+                }
+                acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc.acc[i][j], 0, 0, 0);
+                if (s + 1 < SUB) {
+                  if (j == Cfg::RN - 1) fm[i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
+                  if (i == Cfg::RM - 1) fn[j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
+                }
               }
-            }
-      } else if (issue_next) {
-        // a wave without valid rows only requests its share of the stage
-        ms.issue(st_next, knext * BK);
-        ns.issue(st_next + Cfg::M_BYTES, knext * BK);
-      }
-      if (issue_next) {
-        if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * BK);
-        if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * BK);
+        } else if (issue_next) {
+          // a wave without valid rows only requests its share of the stage
+          ms.issue(st_next, knext * BK);
+          ns.issue(st_next + Cfg::M_BYTES, knext * BK);
+        }
+        if (issue_next) {
+          if constexpr (Op::M_MODE == KOUTER) ms.prefetch_idx((knext + 1) * BK);
+          if constexpr (Op::N_MODE == KOUTER) ns.prefetch_idx((knext + 1) * BK);
+        }
       }
     }
     barrier_lds();  // every wave is done with the stage buffers
