@@ -180,6 +180,19 @@ def test_weight_gradients_over_row_chunks():
     assert R.counts[3] > 2 * 2048
 
 
+def test_weight_gradients_short_k_loops():
+    """Experts with 0, 12, 42, 80, 119, 134, 191 and 222 rows: the weight
+    gradients' 256 x 256 tiles (d = 512, n = 256) then run k loops of 0 to 4
+    steps of 64 rows, the cases where the two-stage pipeline has no stage, no
+    second stage or no stage after next to prefetch, and an odd step count.
+    dW1 and dW2 (and the empty expert's zero rows) match the oracle."""
+    cfg = W.MoEConfig("kshort", T=400, d=512, n=256, E=8, K=2, m_tile=128)
+    bias = np.array([-40, 0, 0.6, 1.0, 1.3, 1.5, 1.7, 2.0], np.float32)
+    layer, R = check_layer(cfg, seed=21, bias=bias)
+    steps = sorted(set(int(-(-c // 64)) for c in R.counts))
+    assert steps == [0, 1, 2, 3, 4], (R.counts, steps)
+
+
 def test_single_token_and_one_hot_expert():
     check_layer(TINY, seed=5, T=1)
     check_layer(TINY, seed=6, T=65, round_mode="nearest")
