@@ -1292,8 +1292,11 @@ using C256x256w = GemmCfg<256, 256, 4, 2, 2>;  // 64 x 128 per wave (up, dH, dX~
 using C256x128 = GemmCfg<256, 128, 4, 2, 3>;
 using C256x64 = GemmCfg<256, 64, 8, 1, 3>;
 using C128x256 = GemmCfg<128, 256, 2, 4, 3>;
-using C128x128 = GemmCfg<128, 128, 4, 2, 3>;
-using C128x64 = GemmCfg<128, 64, 4, 2, 3>;
+// the router and router-gradient GEMMs stream X once (no operand reuse across
+// tiles): four 64-deep stages keep three in flight (router 31 -> 28 us, dW_r
+// 31 -> 27 us at 7B against three stages)
+using C128x128 = GemmCfg<128, 128, 4, 2, 4>;
+using C128x64 = GemmCfg<128, 64, 4, 2, 4>;
 
 hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
   const int mt = (a.T + 255) / 256;
