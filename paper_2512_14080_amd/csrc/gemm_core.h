@@ -545,7 +545,6 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
       // A stage goes out in two halves, every second MFMA: the first in the
       // last sub-step of the step before, the second in sub-step 0 (all of it
       // in sub-step 0 of a tile's first step).
-      constexpr int kMf = Cfg::RM * Cfg::RN;  // MFMAs per sub-step
       constexpr int kHalf = kPerStage / 2;
       // stage 0 (the prologue's) is complete, and every wave is past the
       // previous epilogue, whose stores may stay outstanding
