@@ -200,16 +200,7 @@ def kernel_work(cls, cfg, P, T):
     GEMMs count their FLOPs and their unique operand and result bytes (each tensor once; gathered rows counted
     as the tensor they are gathered from) and are bound by whichever takes longer at peak: MFMA or HBM."""
     d, n, E, K = cfg.d, cfg.n, cfg.E, cfg.K
-    gemm = {  # FLOPs, bytes
-        "up_proj": (2.0 * P * d * 2 * n, 2.0 * T * d + 2.0 * E * d * 2 * n + 2.0 * P * 2 * n + 2.0 * P * n),
-        "down_proj": (2.0 * P * n * d, 2.0 * P * n + 2.0 * E * n * d + 2.0 * P * d),
-        "dH": (2.0 * P * d * n, 2.0 * T * d + 2.0 * E * n * d + 2 * 2.0 * P * 2 * n + 2.0 * P * n + 4.0 * P),
-        "dW2": (2.0 * P * n * d, 2.0 * P * n + 2.0 * T * d + 2.0 * E * n * d),
-        "dXtilde": (2.0 * P * 2 * n * d, 2.0 * P * 2 * n + 2.0 * E * d * 2 * n + 2.0 * P * d),
-        "dW1": (2.0 * P * d * 2 * n, 2.0 * T * d + 2.0 * P * 2 * n + 2.0 * E * d * 2 * n),
-        "router_gemm": (2.0 * T * d * E, 2.0 * T * d + 2.0 * d * E + 4.0 * T * E),
-        "dWr": (2.0 * T * d * E, 2.0 * T * d + 2.0 * T * E + 4.0 * d * E),
-    }
+    gemm = gemm_work(cfg, P, T)
     if cls in gemm:
         f, b = gemm[cls]
         if b / (PEAK_HBM_GBS * 1e9) > f / (PEAK_BF16_TFLOPS * 1e12):
@@ -226,6 +217,21 @@ def kernel_work(cls, cfg, P, T):
     if cls in hbm:
         return hbm[cls], "GB/s", "hbm"
     return None, None, None
+
+
+def gemm_work(cfg, P, T):
+    """{GEMM kernel class: (FLOPs, unique operand and result bytes)} of one launch."""
+    d, n, E = cfg.d, cfg.n, cfg.E
+    return {  # FLOPs, bytes
+        "up_proj": (2.0 * P * d * 2 * n, 2.0 * T * d + 2.0 * E * d * 2 * n + 2.0 * P * 2 * n + 2.0 * P * n),
+        "down_proj": (2.0 * P * n * d, 2.0 * P * n + 2.0 * E * n * d + 2.0 * P * d),
+        "dH": (2.0 * P * d * n, 2.0 * T * d + 2.0 * E * n * d + 2 * 2.0 * P * 2 * n + 2.0 * P * n + 4.0 * P),
+        "dW2": (2.0 * P * n * d, 2.0 * P * n + 2.0 * T * d + 2.0 * E * n * d),
+        "dXtilde": (2.0 * P * 2 * n * d, 2.0 * P * 2 * n + 2.0 * E * d * 2 * n + 2.0 * P * d),
+        "dW1": (2.0 * P * d * 2 * n, 2.0 * T * d + 2.0 * P * 2 * n + 2.0 * E * d * 2 * n),
+        "router_gemm": (2.0 * T * d * E, 2.0 * T * d + 2.0 * d * E + 4.0 * T * E),
+        "dWr": (2.0 * T * d * E, 2.0 * T * d + 2.0 * T * E + 4.0 * d * E),
+    }
 
 
 # the expert computation without router or routing (steps up-proj .. dX aggregation)
