@@ -29,6 +29,7 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "l2_fabric_traffic_7b_tr128.md"
 # kernel-name fragment -> kernel class (as in the library's timing classes)
 KERNEL_CLASS_OF = [("OpUp<", "up_proj"), ("OpDown<", "down_proj"), ("OpDH<", "dH"), ("OpDW2<", "dW2"),
                    ("OpDXt<", "dXtilde"), ("OpDW1<", "dW1"), ("OpDWr<", "dWr"), ("OpRouter<", "router_gemm"),
+                   ("OpRouterTopk<", "router_topk"),
                    ("agg_o_kernel", "aggregate_O"), ("agg_dx_kernel", "aggregate_dX"),
                    ("topk_lane_kernel", "topk"), ("topk_route_kernel", "topk"),
                    ("tr_local_kernel", "tr_local"), ("tr_reduce_kernel", "tr_reduce"), ("tr_merge_kernel", "tr_merge"),
@@ -230,6 +231,9 @@ def gemm_work(cfg, P, T):
         "dXtilde": (2.0 * P * 2 * n * d, 2.0 * P * 2 * n + 2.0 * E * d * 2 * n + 2.0 * P * d),
         "dW1": (2.0 * P * d * 2 * n, 2.0 * T * d + 2.0 * P * 2 * n + 2.0 * E * d * 2 * n),
         "router_gemm": (2.0 * T * d * E, 2.0 * T * d + 2.0 * d * E + 4.0 * T * E),
+        # X and W_r in; scores token- and expert-major (the rounded layer's
+        # step writes both), the top-K lists and the membership bitmap out
+        "router_topk": (2.0 * T * d * E, 2.0 * T * d + 2.0 * d * E + 8.0 * T * E + 8.0 * T * cfg.K + T * E / 8.0),
         "dWr": (2.0 * T * d * E, 2.0 * T * d + 2.0 * T * E + 4.0 * d * E),
     }
 
@@ -331,7 +335,8 @@ def measure(args, cfg, cpu):
     round_mode = None if args.round == "none" else args.round
     log(f"[bench] config {cfg}, rounding {round_mode}")
     inp = W.make_inputs(cfg, 0)
-    layer = DeviceLayer(inp, round_mode=round_mode)
+    # the logits feed nothing after the softmax: the step does not keep them
+    layer = DeviceLayer(inp, round_mode=round_mode, keep_logits=False)
     stream = torch.cuda.current_stream()
     for _ in range(max(1, args.warmup)):
         layer.step()
@@ -458,11 +463,16 @@ def ablation(args):
         B.moe_prof_select(-1)
         return out
 
-    layer = DeviceLayer(W.make_inputs(cfg, 0), round_mode="nearest")
+    layer = DeviceLayer(W.make_inputs(cfg, 0), round_mode="nearest", keep_logits=False)
     for _ in range(3):
         layer.step()
     P = layer.rows()
-    gathered = class_ms(layer, ["topk", "up_proj", "dH", "dW1"])
+    gathered = class_ms(layer, ["router_topk", "up_proj", "dH", "dW1"])
+    # the same routing as two launches (router GEMM, then softmax/top-K on the logits)
+    fused_flags = layer.route_flags
+    layer.route_flags = fused_flags | B.MOE_ROUTE_SEPARATE_TOPK
+    gathered.update(class_ms(layer, ["router_gemm", "topk"]))
+    layer.route_flags = fused_flags
 
     # expert-aggregation strategies: down-projection epilogue + aggregation kernel(s) per forward
     from paper_2512_14080_amd.layer import _aligned_empty
@@ -516,6 +526,12 @@ def ablation(args):
                       "torch_logit_read_GBps": round(rd / (t_torch * 1e-3), 1),
                       "note": "the fused kernel also writes the transposed scores and the membership bitmap"}),
           flush=True)
+    if gathered.get("router_topk") is not None:
+        two = gathered["router_gemm"] + gathered["topk"]
+        print(json.dumps({"ablation": "router GEMM with softmax/top-K in its epilogue",
+                          "workload": f"T={cfg.T} d={cfg.d} E={cfg.E} K={cfg.K}",
+                          "one_launch_ms": gathered["router_topk"], "router_gemm_ms": gathered["router_gemm"],
+                          "topk_ms": gathered["topk"], "two_launches_ms": round(two, 5)}), flush=True)
     del logits
     torch.cuda.empty_cache()
 

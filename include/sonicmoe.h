@@ -134,12 +134,15 @@ enum {
                                   an input holding S_full                      */
   MOE_ROUTE_WRITE_LOGITS = 2,  /* keep the logits in r->logits                 */
   MOE_ROUTE_WRITE_SCORES_T = 4, /* also write r->scores_t                      */
-  MOE_ROUTE_COUNTS_ONLY = 8     /* metadata stops at mask, mask_prefix and
+  MOE_ROUTE_COUNTS_ONLY = 8,    /* metadata stops at mask, mask_prefix and
                                    counts: enough for moe_round_tokens, which
                                    builds the rounded routing's own metadata;
                                    offsets and the row lists are not written,
                                    and r->state becomes MOE_ROUTING_STATE_COUNTS,
                                    which moe_fwd and moe_bwd refuse          */
+  MOE_ROUTE_SEPARATE_TOPK = 16  /* run the router GEMM and softmax/top-K as two
+                                   launches even where they fuse (the logits
+                                   then pass through r->logits or r->scores) */
 };
 
 /*
@@ -156,6 +159,11 @@ enum {
  * r->capacity must be >= T*K.  On success r->state is MOE_ROUTING_STATE_BUILT
  * (MOE_ROUTING_STATE_COUNTS with MOE_ROUTE_COUNTS_ONLY) and the device word
  * r->status is cleared by the metadata kernels.
+ * With E <= 128 and K <= 8 the softmax and top-K run in the
+ * router GEMM's epilogue (one launch; the logits are written only with
+ * MOE_ROUTE_WRITE_LOGITS).  Its scores may differ from the two-launch path's
+ * in the last bits (the order of the softmax sum); selection, mask and weights
+ * are those the two-launch path derives from the scores it writes.
  * Scores are compared through the order-preserving image of their fp32 bit
  * pattern, which is the float order for numbers (+0 = -0) and extends it to
  * NaN (sign clear: above +Inf; sign set: below -Inf), so non-finite scores
@@ -315,6 +323,7 @@ enum {
   MOE_KC_ROUTER_GEMM = 0, MOE_KC_TOPK, MOE_KC_META, MOE_KC_ROUND,
   MOE_KC_UP, MOE_KC_DOWN, MOE_KC_AGG_O,
   MOE_KC_DH, MOE_KC_DW2, MOE_KC_DXT, MOE_KC_DW1, MOE_KC_AGG_DX, MOE_KC_DWR,
+  MOE_KC_ROUTER_TOPK, /* the router GEMM with fused softmax/top-K */
   MOE_KC_COUNT
 };
 int moe_prof_select(int kernel_class);

@@ -26,6 +26,7 @@ MOE_ROUTE_SCORES_IN = 1
 MOE_ROUTE_WRITE_LOGITS = 2
 MOE_ROUTE_WRITE_SCORES_T = 4
 MOE_ROUTE_COUNTS_ONLY = 8
+MOE_ROUTE_SEPARATE_TOPK = 16
 
 MOE_ROUTING_STATE_EMPTY = 0
 MOE_ROUTING_STATE_COUNTS = 1
@@ -42,7 +43,7 @@ MOE_WS_FWD_AGG_ABLATION = 3
 AGG_STRATEGIES = {"gather_sum": 0, "scatter_sum": 1, "atomic_f32": 2}
 
 KERNEL_CLASSES = ["router_gemm", "topk", "routing_meta", "token_round", "up_proj", "down_proj", "aggregate_O",
-                  "dH", "dW2", "dXtilde", "dW1", "aggregate_dX", "dWr"]
+                  "dH", "dW2", "dXtilde", "dW1", "aggregate_dX", "dWr", "router_topk"]
 
 EXPORTS = ["moe_routing_bytes", "moe_routing_init", "moe_round_capacity", "moe_route", "moe_round_tokens",
            "moe_workspace_bytes", "moe_fwd", "moe_bwd", "moe_strerror", "moe_last_error", "moe_prof_select",

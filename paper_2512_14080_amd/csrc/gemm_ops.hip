@@ -13,6 +13,7 @@
 
 #include "gemm_core.h"
 #include "launch.h"
+#include "topk_net.h"
 
 namespace smoe {
 
@@ -498,6 +499,206 @@ struct OpRouter {
 #pragma unroll
           for (int q = 0; q < 4; ++q) v[q] = t.acc[i][j][4 * g + q] + (p.a.bias ? p.a.bias[col + q] : 0.f);
           *(f32x4*)(out + col) = v;
+        }
+    }
+  }
+};
+
+// ======================================================= router + softmax/top-K
+// The router GEMM with the routing of Section 2.3 / Appendix D in its
+// epilogue, for E <= BN (one N tile holds every logit of its 128 tokens).  A
+// token's row is spread over WN waves and two lanes per wave (the MFMA layout:
+// lane l and l + 32 hold alternate groups of four columns), NV = 16 RN values
+// per lane.  The epilogue:
+//   1. logits = acc (+ bias), written when asked for; row maximum and then the
+//      sum of exp(x - max) over the lane, its partner lane, and the WN waves
+//      (through LDS, in wave order, so every holder of the row agrees);
+//   2. scores = exp * (1 / sum), written token-major and expert-major;
+//   3. each lane sorts its NV (score, expert) pairs in groups of KM and merges
+//      them into a top-KM list, merges that with its partner lane's list and
+//      then with the other waves' lists (LDS): all holders of the row end with
+//      the row's sorted top-KM;
+//   4. membership: a pair at or above the K-th is selected; one ballot per
+//      (column group) gives 32 rows of two columns, parked in LDS per 32-row
+//      block, then written as the 64-bit words of the expert-major bitmap;
+//   5. the weights: the K selected scores summed in ascending expert order
+//      (the order the separate top-K kernel uses, so the two agree bit for bit
+//      on the same scores), then score / sum.
+// The results match launch_topk_route on these scores exactly; the scores
+// themselves differ from its own softmax of the same logits only in the
+// rounding of the sum.
+template <class Cfg_, int KM, bool FULL_N>
+struct OpRouterTopk {
+  using Cfg = Cfg_;
+  static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
+  static constexpr int BM = Cfg::BM, BN = Cfg::BN, WN = Cfg::WN, NV = Cfg::RN * 16;
+  static_assert(Cfg::RM == 1, "one 32-row block per wave");
+  static_assert(NV % KM == 0, "pairs per lane in groups of KM");
+  // LDS: row maxima, row sums [WN][BM] f32; top lists [WN][KM][BM] u64;
+  // membership pieces [BM / 32][BN] u32
+  static constexpr int kSumOff = WN * BM * 4, kListOff = 2 * WN * BM * 4;
+  static constexpr int kBitsOff = kListOff + WN * KM * BM * 8;
+  static constexpr int EPI_LDS = kBitsOff + (BM / 32) * BN * 4;
+  struct Params { RouterTopkArgs a; };
+  static __device__ int count(const Params& p, int*) { return (p.a.T + BM - 1) / BM; }
+  static __device__ bool tile(const Params& p, int id, TileInfo& ti, int*) {
+    return tile_plain_m<BM, BN>(p.a.T, p.a.E, p.a.d, id, ti);
+  }
+  static __device__ void init_m(const Params& p, const TileInfo& ti, RowsSide<BM, Cfg::BK, Cfg::NW>& s) {
+    s.init(p.a.X, p.a.d, nullptr, ti.row_base, ti.mrows);
+  }
+  static __device__ void init_n(const Params& p, const TileInfo& ti, KOuterSide<BN, Cfg::BK, Cfg::NW>& s) {
+    s.init(p.a.Wr, p.a.E, nullptr, 0, p.a.d, p.a.E, ColOffset{ti.n0});
+  }
+  static __device__ uint64_t xor32(uint64_t v) {
+    const uint32_t lo = __shfl_xor((uint32_t)v, 32, kWave), hi = __shfl_xor((uint32_t)(v >> 32), 32, kWave);
+    return ((uint64_t)hi << 32) | lo;
+  }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* lds) {
+    const RouterTopkArgs& a = p.a;
+    // lane-dependent coordinates from an opaque lane read: computed here, not
+    // hoisted out of the tile loop as constants that stay live through it
+    const int lane = volatile_lane(), wave = threadIdx.x >> 6;
+    const int wn = Cfg::wave_n(wave), wm = Cfg::wave_m(wave), h = lane >> 5, u = lane & 31;
+    const int m = wm * 32 + u;
+    // column of value 4 (4 j + g) + q: the MFMA output layout (Acc::n_of)
+    const int c0 = wn * (BN / WN) + 4 * h;
+    auto col_of = [&](int k) { return c0 + 32 * (k >> 4) + 8 * ((k >> 2) & 3) + (k & 3); };
+    // E a multiple of 8: a group of four columns is wholly inside or outside
+    auto col_ok = [&](int k) { return FULL_N || col_of(k) < a.E; };
+    const bool live = m < ti.mrows;
+    const size_t row = (size_t)(ti.row_base + m);
+    float* rmax = (float*)lds;
+    float* rsum = (float*)(lds + kSumOff);
+    uint64_t* lists = (uint64_t*)(lds + kListOff);
+    uint32_t* bits = (uint32_t*)(lds + kBitsOff);
+    float v[NV];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int k0 = 0; k0 < NV; k0 += 4) {
+      const int col = col_of(k0);
+      f32x4 x;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        x[q] = t.acc[0][k0 >> 4][(k0 & 15) + q];
+        if (a.bias) x[q] += col_ok(k0) ? a.bias[col + q] : 0.f;
+        v[k0 + q] = col_ok(k0) ? x[q] : -INFINITY;
+        mx = fmaxf(mx, v[k0 + q]);
+      }
+      if (a.logits && live && col_ok(k0)) *(f32x4*)(a.logits + row * a.E + col) = x;
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    if (h == 0) rmax[wn * BM + m] = mx;
+    barrier_lds();
+    mx = rmax[m];
+#pragma unroll
+    for (int w = 1; w < WN; ++w) mx = fmaxf(mx, rmax[w * BM + m]);
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      v[k] = __expf(v[k] - mx);  // 0 for the columns past E
+      sum += v[k];
+    }
+    sum += __shfl_xor(sum, 32, kWave);  // the same value in both lanes
+    if (h == 0) rsum[wn * BM + m] = sum;
+    barrier_lds();
+    sum = rsum[m];
+#pragma unroll
+    for (int w = 1; w < WN; ++w) sum += rsum[w * BM + m];
+    const float rs = 1.f / sum;
+#pragma unroll
+    for (int k0 = 0; k0 < NV; k0 += 4) {
+      const int col = col_of(k0);
+      f32x4 x;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = v[k0 + q] = v[k0 + q] * rs;
+      if (live && col_ok(k0)) {
+        *(f32x4*)(a.scores + row * a.E + col) = x;
+        if (a.scores_t) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) a.scores_t[(size_t)(col + q) * a.T + row] = x[q];
+        }
+      }
+    }
+    // (score, expert) pair of value k, 0 for a row past T or a column past E
+    // (masked, not branched around)
+    const uint64_t live_mask = live ? ~0ull : 0ull;
+    auto pair = [&](int k) -> uint64_t {
+      const uint64_t pk = topk_pair(v[k], col_of(k)) & live_mask;
+      if constexpr (FULL_N) return pk;
+      return col_ok(k) ? pk : 0ull;
+    };
+    uint64_t top[KM];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) top[k] = pair(k);
+    topk_sort<KM>(top);
+#pragma unroll
+    for (int g0 = KM; g0 < NV; g0 += KM) {
+      uint64_t grp[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) grp[k] = pair(g0 + k);
+      topk_sort<KM>(grp);
+      topk_merge<KM>(top, grp);
+    }
+    {
+      uint64_t o[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) o[k] = xor32(top[k]);
+      topk_merge<KM>(top, o);  // the row's pairs are distinct: both lanes get the same list
+    }
+    if (h == 0) {
+#pragma unroll
+      for (int k = 0; k < KM; ++k) lists[(wn * KM + k) * BM + m] = top[k];
+    }
+    barrier_lds();
+#pragma unroll
+    for (int w = 0; w < WN; ++w) {
+      if (w == wn) continue;
+      uint64_t o[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) o[k] = lists[(w * KM + k) * BM + m];
+      topk_merge<KM>(top, o);
+    }
+    uint64_t thr = top[0];
+#pragma unroll
+    for (int k = 1; k < KM; ++k)
+      if (k == a.K - 1) thr = top[k];
+    // membership: ballot k holds rows 0..31 of the wave for column col_of(k)
+    // of the lanes below 32 (low half) and of the lanes above (high half);
+    // lane u + 32 h keeps half h of ballot u, i.e. its own column col_of(u)
+    uint32_t mine = 0;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) asm volatile("" : "+v"(v[k]));  // recompute the pairs, do not keep them
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const uint64_t pk = pair(k);
+      const uint64_t b = __ballot(pk != 0ull && pk >= thr);
+      mine = u == k ? (uint32_t)(b >> (32 * h)) : mine;
+    }
+    if (u < NV) bits[wm * BN + col_of(u)] = mine;
+    barrier_lds();
+    const int w0 = ti.row_base / 64;
+    for (int i = threadIdx.x; i < (BM / 64) * a.E; i += Cfg::THREADS) {
+      const int e = i / (BM / 64), ww = i % (BM / 64);
+      if (w0 + ww < a.W)
+        a.mask[(size_t)e * a.W + w0 + ww] = bits[2 * ww * BN + e] | ((uint64_t)bits[(2 * ww + 1) * BN + e] << 32);
+    }
+    if (live && wn == 0 && h == 0) {
+      // the selected scores in ascending expert order: (expert, score) halves
+      // swapped, so the descending sort puts the lowest expert first
+      uint64_t byx[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) byx[k] = k < a.K ? (top[k] << 32) | (top[k] >> 32) : 0ull;
+      topk_sort<KM>(byx);
+      float den = 0.f;
+#pragma unroll
+      for (int k = 0; k < KM; ++k)
+        if (k < a.K) den += topk_value((uint32_t)byx[k]);
+#pragma unroll
+      for (int k = 0; k < KM; ++k)
+        if (k < a.K) {
+          a.topk_idx[row * a.K + k] = (int32_t)~(uint32_t)top[k];
+          a.topk_w[row * a.K + k] = topk_value((uint32_t)(top[k] >> 32)) / den;
         }
     }
   }
@@ -1308,6 +1509,17 @@ hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
   if (mt * ((a.E + 255) / 256) < cu_count())
     return run<OpRouter<C128x256>>({a}, (a.T + 127) / 128 * ((a.E + 255) / 256), s);
   return run<OpRouter<C256x256>>({a}, mt * ((a.E + 255) / 256), s);
+}
+
+bool router_topk_fusable(int E, int K) { return E % 8 == 0 && E <= 128 && K <= 8; }
+
+hipError_t launch_router_topk(const RouterTopkArgs& a, hipStream_t s) {
+  if (!router_topk_fusable(a.E, a.K)) return hipErrorInvalidValue;
+  const int tiles = (a.T + 127) / 128;
+  if (a.E == 64) return run<OpRouterTopk<C128x64, 8, true>>({a}, tiles, s);
+  if (a.E < 64) return run<OpRouterTopk<C128x64, 8, false>>({a}, tiles, s);
+  if (a.E == 128) return run<OpRouterTopk<C128x128, 8, true>>({a}, tiles, s);
+  return run<OpRouterTopk<C128x128, 8, false>>({a}, tiles, s);
 }
 
 hipError_t launch_up(const UpArgs& a, hipStream_t s) {

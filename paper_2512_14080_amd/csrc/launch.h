@@ -25,6 +25,16 @@ struct RouterGemmArgs {
   const uint16_t* X; const uint16_t* Wr; const float* bias; float* logits; int T, d, E;
 };
 hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s);
+// The router GEMM with softmax and top-K fused into its epilogue (one tile
+// spans every expert): the outputs of launch_topk_route with do_softmax = 1,
+// and the logits too when logits is not null.
+struct RouterTopkArgs {
+  const uint16_t* X; const uint16_t* Wr; const float* bias;
+  float* logits; float* scores; float* scores_t; int32_t* topk_idx; float* topk_w; uint64_t* mask;
+  int T, d, E, K, W;
+};
+bool router_topk_fusable(int E, int K);
+hipError_t launch_router_topk(const RouterTopkArgs& a, hipStream_t s);
 
 // The varlen-M m-tile list (mtiles_kernel): built from the expert offsets
 // once per forward / backward call, read by the up, down, dH and dX~ GEMMs.

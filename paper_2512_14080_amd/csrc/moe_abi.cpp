@@ -354,21 +354,29 @@ int moe_route(moe_dims m, const moe_bf16* X, const moe_bf16* Wr, const float* bi
     return fail(MOE_ERR_INVALID_ARG, "MOE_ROUTE_WRITE_LOGITS needs r->logits");
   if ((flags & MOE_ROUTE_WRITE_SCORES_T) && !r->scores_t)
     return fail(MOE_ERR_INVALID_ARG, "MOE_ROUTE_WRITE_SCORES_T needs r->scores_t");
-  if (flags & ~(MOE_ROUTE_SCORES_IN | MOE_ROUTE_WRITE_LOGITS | MOE_ROUTE_WRITE_SCORES_T | MOE_ROUTE_COUNTS_ONLY))
+  if (flags & ~(MOE_ROUTE_SCORES_IN | MOE_ROUTE_WRITE_LOGITS | MOE_ROUTE_WRITE_SCORES_T | MOE_ROUTE_COUNTS_ONLY |
+                MOE_ROUTE_SEPARATE_TOPK))
     return fail(MOE_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
   hipStream_t stream = (hipStream_t)stream_;
   float* scores_t = (flags & MOE_ROUTE_WRITE_SCORES_T) ? r->scores_t : nullptr;
   const float* in = r->scores;
-  if (!scores_in) {
-    float* logits = (flags & MOE_ROUTE_WRITE_LOGITS) ? r->logits : r->scores;
-    smoe::RouterGemmArgs a{X, Wr, bias, logits, m.T, m.d, m.E};
-    LAUNCH(MOE_KC_ROUTER_GEMM, smoe::launch_router_gemm(a, stream), "router gemm");
-    in = logits;
+  if (!scores_in && !(flags & MOE_ROUTE_SEPARATE_TOPK) && smoe::router_topk_fusable(m.E, m.K)) {
+    float* logits = (flags & MOE_ROUTE_WRITE_LOGITS) ? r->logits : nullptr;
+    smoe::RouterTopkArgs a{X, Wr, bias, logits, r->scores, scores_t, r->topk_idx, r->topk_w, r->mask,
+                           m.T, m.d, m.E, m.K, r->words};
+    LAUNCH(MOE_KC_ROUTER_TOPK, smoe::launch_router_topk(a, stream), "router gemm with softmax/top-K");
+  } else {
+    if (!scores_in) {
+      float* logits = (flags & MOE_ROUTE_WRITE_LOGITS) ? r->logits : r->scores;
+      smoe::RouterGemmArgs a{X, Wr, bias, logits, m.T, m.d, m.E};
+      LAUNCH(MOE_KC_ROUTER_GEMM, smoe::launch_router_gemm(a, stream), "router gemm");
+      in = logits;
+    }
+    LAUNCH(MOE_KC_TOPK,
+           smoe::launch_topk_route(in, r->scores, scores_t, r->topk_idx, r->topk_w, r->mask, m.T, m.E, m.K,
+                                   r->words, scores_in ? 0 : 1, stream),
+           "softmax/top-K");
   }
-  LAUNCH(MOE_KC_TOPK,
-         smoe::launch_topk_route(in, r->scores, scores_t, r->topk_idx, r->topk_w, r->mask, m.T, m.E, m.K, r->words,
-                                 scores_in ? 0 : 1, stream),
-         "softmax/top-K");
   const bool counts_only = (flags & MOE_ROUTE_COUNTS_ONLY) != 0;
   r->state = MOE_ROUTING_STATE_EMPTY;  // until the metadata launch is enqueued
   LAUNCH(MOE_KC_META, smoe::launch_tc_metadata(*r, m.T, m.E, m.K, counts_only, stream), "routing metadata");
@@ -625,7 +633,7 @@ int moe_prof_read(double* ms, int32_t* launches) {
 const char* moe_kernel_class_name(int kc) {
   static const char* names[MOE_KC_COUNT] = {"router_gemm", "topk", "routing_meta", "token_round", "up_proj",
                                             "down_proj", "aggregate_O", "dH", "dW2", "dXtilde",
-                                            "dW1", "aggregate_dX", "dWr"};
+                                            "dW1", "aggregate_dX", "dWr", "router_topk"};
   return (kc >= 0 && kc < MOE_KC_COUNT) ? names[kc] : "unknown";
 }
 

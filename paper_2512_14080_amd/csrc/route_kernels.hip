@@ -12,24 +12,11 @@
 // expert's membership bitmap, which it assembles in LDS.
 #include "device_common.h"
 #include "launch.h"
+#include "topk_net.h"
 
 namespace smoe {
 
 constexpr int kTopkWaves = 16;
-
-// Order-preserving integer image of an fp32 score (+0 and -0 map to one key).
-// Comparisons go through it so the selection order is total even for NaN
-// scores (a NaN never compares greater or smaller as a float, which would let
-// the lanes of a wave disagree on the winner and pick an expert twice).
-__device__ __forceinline__ uint32_t topk_key(float x) {
-  uint32_t b = __float_as_uint(x);
-  if (b == 0x80000000u) b = 0;
-  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-// inverse of topk_key (-0 comes back as +0)
-__device__ __forceinline__ float topk_value(uint32_t k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
-}
 
 // Workgroup = 64 tokens (one membership word).  `in` and `scores` may alias
 // (logits overwritten in place by the scores).  With STASH every output of the
@@ -211,42 +198,6 @@ __global__ __launch_bounds__(1024) void topk_route_kernel(const float* in, float
 //      the first wave adds the lists slice by slice).
 // The (score, index) pairs are compared exactly, as in the wave-per-token
 // kernel above: equal keys order by the lower expert.
-template <int KM>
-__device__ __forceinline__ void topk_cex(uint64_t& a, uint64_t& b) {  // a >= b afterwards
-  const bool sw = b > a;
-  const uint64_t hi = sw ? b : a;
-  b = sw ? a : b;
-  a = hi;
-}
-// bitonic sort of KM pairs, largest first (KM a power of two)
-template <int KM>
-__device__ __forceinline__ void topk_sort(uint64_t (&v)[KM]) {
-#pragma unroll
-  for (int k = 2; k <= KM; k <<= 1)
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1)
-#pragma unroll
-      for (int i = 0; i < KM; ++i) {
-        const int l = i ^ j;
-        if (l > i) {
-          if ((i & k) == 0)
-            topk_cex<KM>(v[i], v[l]);
-          else
-            topk_cex<KM>(v[l], v[i]);
-        }
-      }
-}
-template <int KM>
-__device__ __forceinline__ void topk_merge(uint64_t (&a)[KM], const uint64_t (&b)[KM]) {
-#pragma unroll
-  for (int i = 0; i < KM; ++i) a[i] = a[i] > b[KM - 1 - i] ? a[i] : b[KM - 1 - i];
-#pragma unroll
-  for (int h = KM / 2; h >= 1; h >>= 1)
-#pragma unroll
-    for (int i = 0; i < KM; ++i)
-      if ((i & h) == 0) topk_cex<KM>(a[i], a[i + h]);
-}
-
 template <int KM, int NW>
 __global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, float* scores, float* __restrict__ scores_t,
                                                             int32_t* __restrict__ topk_idx, float* __restrict__ topk_w,
@@ -333,7 +284,7 @@ __global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, flo
         }
 #pragma unroll
         for (int c = 0; c < 4; ++c)
-          pr[4 * gg + c] = live ? ((uint64_t)topk_key(p[c]) << 32) | (uint32_t)~(uint32_t)(eg + c) : 0ull;
+          pr[4 * gg + c] = live ? topk_pair(p[c], eg + c) : 0ull;
       } else {
 #pragma unroll
         for (int c = 0; c < 4; ++c) pr[4 * gg + c] = 0ull;
@@ -381,7 +332,7 @@ __global__ __launch_bounds__(64 * NW) void topk_lane_kernel(const float* in, flo
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const int el = 4 * g + c;  // expert e0 + el
-        const uint64_t x = ((uint64_t)topk_key(p[c]) << 32) | (uint32_t)~(uint32_t)(e0 + el);
+        const uint64_t x = topk_pair(p[c], e0 + el);
         const bool sel = live && x >= thr;
         const uint64_t word = __ballot(sel);
         if (lane == (el & 63)) mw[r] = word;

@@ -42,7 +42,7 @@ class DeviceLayer:
     """
 
     def __init__(self, inputs, round_mode=None, m_tile=None, scores_in=None, u=None, device="cuda",
-                 router_grad=True, b1=None, b2=None):
+                 router_grad=True, b1=None, b2=None, keep_logits=True):
         import torch
         cfg = inputs.cfg
         T, d, n, E, K = inputs.X.shape[0], cfg.d, cfg.n, cfg.E, cfg.K
@@ -56,7 +56,7 @@ class DeviceLayer:
         self.bias = None if inputs.bias is None else torch.from_numpy(inputs.bias).to(device)
         self.round_mode = round_mode
         self.m_tile = m_tile if m_tile is not None else cfg.m_tile
-        flags = B.MOE_ROUTING_LOGITS | (B.MOE_ROUTING_SCORES_T if round_mode else 0)
+        flags = (B.MOE_ROUTING_LOGITS if keep_logits else 0) | (B.MOE_ROUTING_SCORES_T if round_mode else 0)
         self.tc = B.Routing(self.D, T * K, flags, device)
         self.tr = None
         if round_mode:
@@ -64,7 +64,7 @@ class DeviceLayer:
         # token rounding builds its own metadata: the token-choice routing
         # only needs its mask, counts and transposed scores
         for_round = (B.MOE_ROUTE_WRITE_SCORES_T | B.MOE_ROUTE_COUNTS_ONLY) if round_mode else 0
-        self.route_flags = B.MOE_ROUTE_WRITE_LOGITS | for_round
+        self.route_flags = (B.MOE_ROUTE_WRITE_LOGITS if keep_logits else 0) | for_round
         if scores_in is not None:
             self.tc.arrays()["scores"].copy_(torch.from_numpy(np.ascontiguousarray(scores_in, np.float32)))
             self.route_flags = B.MOE_ROUTE_SCORES_IN | for_round
