@@ -29,12 +29,16 @@ __device__ __forceinline__ uint64_t topk_pair(float score, int expert) {
   return ((uint64_t)topk_key(score) << 32) | (uint32_t)~(uint32_t)expert;
 }
 
+// a >= b afterwards.  The swap selects the 32-bit halves on one 64-bit
+// comparison; written as a 64-bit select pair it becomes an unsigned max and
+// min, i.e. two comparisons.
 template <int KM>
-__device__ __forceinline__ void topk_cex(uint64_t& a, uint64_t& b) {  // a >= b afterwards
+__device__ __forceinline__ void topk_cex(uint64_t& a, uint64_t& b) {
   const bool sw = b > a;
-  const uint64_t hi = sw ? b : a;
-  b = sw ? a : b;
-  a = hi;
+  const uint32_t al = (uint32_t)a, ah = (uint32_t)(a >> 32), bl = (uint32_t)b, bh = (uint32_t)(b >> 32);
+  const uint32_t xl = sw ? bl : al, xh = sw ? bh : ah, yl = sw ? al : bl, yh = sw ? ah : bh;
+  a = ((uint64_t)xh << 32) | xl;
+  b = ((uint64_t)yh << 32) | yl;
 }
 // sort of KM pairs, largest first (KM a power of two): for KM = 8 Batcher's
 // odd-even merge sort (19 compare-exchanges: pairs, then odd-even merges of
