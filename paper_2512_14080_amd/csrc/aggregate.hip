@@ -106,9 +106,14 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
   if (t >= T) return;
   const int lane = lane_id();
   const int j0 = tok_offsets[t], j1 = tok_offsets[t + 1];
-  // g = sum_k s_k dS_k in row order; lanes 0..7 fetch a batch's terms
+  // g = sum_k s_k dS_k in row order; lanes 0..7 fetch a batch's terms.  A
+  // token whose rows fit one batch (every token-choice token with K <= 8,
+  // most rounded ones) forms g in the main loop's only iteration instead, from
+  // the weights and dS values that iteration loads anyway: one round trip of
+  // dependent loads fewer before its dX~ rows are requested.
+  const bool one_batch = j1 - j0 <= kAggBatch;
   float g = 0.f;
-  if (WrT)
+  if (WrT && !one_batch)
     for (int jb = j0; jb < j1; jb += kAggBatch) {
       const int slot = jb + (lane & 7);
       const int rl = tok_rows[min(slot, j1 - 1)];
@@ -129,6 +134,11 @@ __global__ __launch_bounds__(256) void agg_dx_kernel(const uint16_t* __restrict_
     const int slot = jb + (lane & 7);
     const int rl = tok_rows[min(slot, j1 - 1)];
     const int el = WrT ? row_expert[rl] : 0;
+    if (WrT && one_batch) {
+      const float pl = slot < j1 ? row_w[rl] * dS[rl] : 0.f;
+#pragma unroll
+      for (int u = 0; u < kAggBatch; ++u) g += bcast_f(pl, u);
+    }
     const float dll = (WrT && slot < j1) ? row_w[rl] * (dS[rl] - g) : 0.f;
     int r[kAggBatch];
 #pragma unroll
