@@ -29,13 +29,16 @@ def _torch():
     return torch
 
 
-def routings(cfg, seed, T=None, bias=None):
+def routings(cfg, seed, T=None, bias=None, edit_x=None):
     torch = _torch()
     from paper_2512_14080_amd import binding as B
     from paper_2512_14080_amd.layer import to_device_bf16
     inp = W.make_inputs(cfg, seed, T=T)
     if bias is not None:
         inp.bias = np.asarray(bias, np.float32)
+    if edit_x is not None:
+        inp.X = inp.X.copy()
+        edit_x(inp.X)
     T = inp.X.shape[0]
     D = B.dims(T, cfg.d, cfg.n, cfg.E, cfg.K)
     X, Wr = to_device_bf16(inp.X, "cuda"), to_device_bf16(inp.Wr, "cuda")
@@ -115,3 +118,34 @@ def test_fused_router_topk_several_tiles_per_workgroup():
 def test_fused_router_topk_7b_full_size():
     """The 7B routing shape (T=32768, d=1536, E=128, K=8)."""
     check(W.CONFIGS["7b"], seed=0)
+
+
+def test_fused_router_topk_nonfinite_logits():
+    """X rows holding NaN, +-Inf or values whose logits overflow give NaN and
+    infinite logits.  Every token still gets K distinct experts in [0, E)
+    (the exact (score, expert) order is total, NaN included), and the selection,
+    weights and bitmap equal those of the top-K kernel run on the fused
+    path's own scores."""
+    cfg = W.MoEConfig("e128nf", T=600, d=256, n=64, E=128, K=8, m_tile=128)
+    nan, pinf, ninf = np.uint16(0x7FC0), np.uint16(0x7F80), np.uint16(0xFF80)
+
+    def edit(X):
+        X[3, 7] = nan                  # a whole logit row of NaN
+        X[10, 0] = pinf                # +-Inf logits (and NaN where they cancel)
+        X[11, 5] = ninf
+        X[20, :] = np.uint16(0x7E00)   # about 4e37 everywhere: logits overflow
+        X[599, 1] = nan                # the ragged last tile
+    inp, o = routings(cfg, 35, edit_x=edit)
+    f, r = o["fused"], o["rerun"]
+    idx = f["topk_idx"]
+    assert ((idx >= 0) & (idx < cfg.E)).all()
+    assert all(len(set(row)) == cfg.K for row in idx)
+    assert np.isnan(f["logits"][3]).all() and not np.isfinite(f["logits"][10]).all()
+    for k in ("topk_idx", "topk_w", "mask", "counts", "scores_t"):
+        np.testing.assert_array_equal(f[k], r[k], err_msg=k)
+    np.testing.assert_array_equal(f["counts"], np.bincount(idx.ravel(), minlength=cfg.E))
+    # rows with finite inputs are untouched by the others
+    ok = np.isfinite(f["logits"]).all(axis=1)
+    assert ok.sum() >= cfg.T - 5
+    L = oracle.router_logits(inp.f32("X")[ok], inp.f32("Wr"), inp.bias, np.float32)
+    assert rel_err(f["logits"][ok], L) <= 1e-4
