@@ -160,6 +160,79 @@ def traffic_report(read_dir, write_dir, copy_read_dir, copy_write_dir, copy_byte
     return "\n".join(lines)
 
 
+MFMA_COUNTERS = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE"]
+MI355X_SIMDS = 256 * 4      # compute units x SIMDs
+MI355X_XCDS = 8             # GRBM_GUI_ACTIVE sums the busy cycles of the eight XCDs
+FLOP_PER_MFMA_MOP = 512     # SQ_INSTS_VALU_MFMA_MOPS_* count in units of 512 FLOPs
+
+
+def mfma_report(pmc_dir):
+    """Markdown summary of the matrix-core work and utilisation of each GEMM class from one rocprofv3 --pmc
+    run of MFMA_COUNTERS: bf16 MFMA FLOPs per launch (512 per counted MOP), the achieved rate over the
+    dispatch's own timestamps against the 2.5 PFLOP/s dense peak, the clock the dispatch ran at (busy cycles
+    per XCD over its duration) and the share of SIMD cycles the MFMA pipe was busy."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(pmc_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {pmc_dir}")
+    disp = {}  # dispatch id -> (kernel name, duration s, {counter: value})
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] not in MFMA_COUNTERS:
+                    continue
+                k = (f, r["Dispatch_Id"])
+                dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+                ent = disp.setdefault(k, (r["Kernel_Name"], dur, {}))
+                ent[2][r["Counter_Name"]] = ent[2].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    by_cls = {}
+    for name, dur, c in disp.values():
+        cls = next((cl for frag, cl in KERNEL_CLASS_OF if frag in name), None)
+        if cls is not None and c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0) > 0:
+            by_cls.setdefault(cls, []).append((dur, c))
+    run = "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline"
+    lines = [
+        "# MFMA work and utilisation per GEMM launch: 7B layer step (T=32768, d=1536, n=256, E=128, K=8), token "
+        "rounding M_tile=128 nearest",
+        "",
+        "Commands (repository root, one MI355X):",
+        "",
+        "```",
+        f"rocprofv3 --pmc {' '.join(MFMA_COUNTERS)} --output-format csv -d {pmc_dir} -o run -- {run}",
+        f"python3 bench.py --mfma-report {pmc_dir}",
+        "```",
+        "",
+        f"Per launch, averaged over the dispatches of the run: bf16 MFMA FLOPs = {FLOP_PER_MFMA_MOP} x "
+        "SQ_INSTS_VALU_MFMA_MOPS_BF16; time = the dispatch's end minus start timestamp; TFLOP/s = FLOPs / time, "
+        "against the 2.5 PFLOP/s dense bf16 peak (1024 SIMDs x 1024 FLOP per cycle x 2.4 GHz); clock = "
+        f"GRBM_GUI_ACTIVE / {MI355X_XCDS} XCDs / time; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / "
+        f"{MI355X_XCDS} x {MI355X_SIMDS} SIMDs), the share of SIMD cycles at the clock the kernel ran at in which "
+        "the matrix pipe was busy.  Under the power limit the clock falls below 2.4 GHz while the pipe is busy, "
+        "so the fraction of peak is below the busy share.  For launches of a few tens of microseconds the "
+        "counters' window is wider than the timestamps, which inflates their clock column.",
+        "",
+        "| kernel class | launches | MFMA GFLOP/launch | avg us | TFLOP/s | % of peak | clock GHz | MFMA busy |",
+        "|---|---|---|---|---|---|---|---|",
+    ]
+    for _, cls in KERNEL_CLASS_OF:
+        if cls not in by_cls:
+            continue
+        ent = by_cls.pop(cls)
+        n = len(ent)
+        t = sum(d for d, _ in ent) / n
+        mean = {c: sum(e[1].get(c, 0.0) for e in ent) / n for c in MFMA_COUNTERS}
+        flops = FLOP_PER_MFMA_MOP * mean["SQ_INSTS_VALU_MFMA_MOPS_BF16"]
+        cyc = mean["GRBM_GUI_ACTIVE"] / MI355X_XCDS
+        busy = mean["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * MI355X_SIMDS) if cyc else float("nan")
+        clock = cyc / t / 1e9 if t else float("nan")
+        rate = flops / t / 1e12 if t else float("nan")
+        lines.append(f"| {cls} | {n} | {flops / 1e9:.1f} | {t * 1e6:.1f} | {rate:.0f} | "
+                     f"{100 * rate / PEAK_BF16_TFLOPS:.1f} | {clock:.2f} | {100 * busy:.1f}% |")
+    lines += ["", f"kernel sources sha256: {kernel_source_hash()}", ""]
+    return "\n".join(lines)
+
+
 def stats_report(stats_csv, title, command):
     """Markdown table of a rocprofv3 --stats kernel summary (kernel_stats.csv)."""
     import csv
@@ -571,6 +644,8 @@ def main():
                     help="print the L2-to-fabric traffic markdown summary from rocprofv3 counter runs and exit")
     ap.add_argument("--stats-report", nargs=3, metavar=("KERNEL_STATS_CSV", "TITLE", "COMMAND"),
                     help="print a rocprofv3 --stats kernel summary as markdown and exit")
+    ap.add_argument("--mfma-report", metavar="PMC_DIR",
+                    help="print the MFMA work and utilisation of a rocprofv3 --pmc run of MFMA_COUNTERS and exit")
     args = ap.parse_args()
     if args.traffic_report:
         fd, wd, cfd, cwd, nb = args.traffic_report
@@ -578,6 +653,9 @@ def main():
         return
     if args.stats_report:
         print(stats_report(*args.stats_report), end="")
+        return
+    if args.mfma_report:
+        print(mfma_report(args.mfma_report), end="")
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the layer is built and measured on a "

@@ -154,3 +154,32 @@ def test_more_than_one_gpu_is_refused_before_any_device_use():
     assert r.returncode == 2
     assert "one GPU only" in r.stderr
     assert r.stdout == ""
+
+
+def test_mfma_report_from_counters(tmp_path):
+    """The MFMA report's arithmetic on a synthetic counter CSV: FLOPs from MOPs,
+    the rate over the dispatch timestamps, the clock per XCD and the busy share
+    of SIMD cycles, averaged over the dispatches of a class."""
+    run = tmp_path / "pmc"
+    run.mkdir()
+    gemm = "void smoe::grouped_gemm_kernel<OpUp<GemmCfg<256, 256, 4, 2, 2, 64, 1> > >(...)"
+    agg = "void smoe::agg_o_kernel<3, false>(...)"
+    fields = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+    rows = []
+    # two up-proj dispatches of 400 us at 2.0 GHz per XCD, 1e9 MOPs (512 GFLOP), pipe busy 25% of SIMD cycles
+    for did, t0 in ((1, 1_000_000), (2, 5_000_000)):
+        t1 = t0 + 400_000
+        cyc = 2.0e9 * 400e-6
+        for name, val in (("GRBM_GUI_ACTIVE", 8 * cyc), ("SQ_INSTS_VALU_MFMA_MOPS_BF16", 1e9),
+                          ("SQ_VALU_MFMA_BUSY_CYCLES", 0.25 * cyc * 1024), ("SQ_BUSY_CYCLES", 4 * cyc)):
+            rows.append((did, gemm, name, val, t0, t1))
+    rows.append((3, agg, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 0, 9_000_000, 9_100_000))
+    with open(run / "run_counter_collection.csv", "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(fields)
+        w.writerows(rows)
+    rep = bench.mfma_report(str(run))
+    rate = 512e9 / 400e-6 / 1e12
+    assert f"| up_proj | 2 | 512.0 | 400.0 | {rate:.0f} | {100 * rate / 2500:.1f} | 2.00 | 25.0% |" in rep
+    assert "aggregate_O" not in rep  # no MFMA work: not a GEMM row
+    assert f"kernel sources sha256: {bench.kernel_source_hash()}" in rep
