@@ -102,13 +102,29 @@ def _write_bytes(c):
     return 64.0 * n64 + 32.0 * (n - n64)
 
 
-def traffic_report(read_dir, write_dir, copy_read_dir, copy_write_dir, copy_bytes):
+def _stats_avg_s(stats_csv):
+    """{kernel class: mean launch duration in s} from a rocprofv3 --stats kernel summary."""
+    import csv
+    tot = {}
+    with open(stats_csv) as fh:
+        for r in csv.DictReader(fh):
+            cls = next((cl for frag, cl in KERNEL_CLASS_OF if frag in r["Name"]), None)
+            if cls is None:
+                continue
+            t, n = tot.get(cls, (0.0, 0))
+            tot[cls] = (t + float(r["TotalDurationNs"]) * 1e-9, n + int(r["Calls"]))
+    return {c: t / n for c, (t, n) in tot.items() if n}
+
+
+def traffic_report(read_dir, write_dir, copy_read_dir, copy_write_dir, copy_bytes, stats_csv=None):
     """Markdown summary of the bytes each kernel class moves between the L2 and the memory fabric per launch.
 
     Reads are the L2's read requests to the fabric by size (TCC_EA0_RDREQ_32B/_64B/_128B), writes its write
     requests (TCC_EA0_WRREQ, of which TCC_EA0_WRREQ_64B are 64-byte, the rest 32-byte).  These bytes include
     Infinity Cache (MALL) hits: the L2 counters cannot tell which requests reach DRAM.  A plain device copy of
-    copy_bytes calibrates the sizes (it should read and write copy_bytes)."""
+    copy_bytes calibrates the sizes (it should read and write copy_bytes).  With stats_csv (a rocprofv3 --stats
+    kernel summary of the same workload) the table adds each class's mean launch time and the bytes it moved
+    per second."""
     cr = _pmc_per_dispatch(copy_read_dir, READ_COUNTERS)
     cw = _pmc_per_dispatch(copy_write_dir, WRITE_COUNTERS)
     ck = [k for k in cr if "copyBuffer" in k or "copy" in k.lower()]
@@ -140,7 +156,8 @@ def traffic_report(read_dir, write_dir, copy_read_dir, copy_write_dir, copy_byte
         f"python3 bench.py --copy-calibration {copy_bytes}",
         f"rocprofv3 --pmc {' '.join(WRITE_COUNTERS)} --output-format csv -d {copy_write_dir} -o run -- "
         f"python3 bench.py --copy-calibration {copy_bytes}",
-        f"python3 bench.py --traffic-report {read_dir} {write_dir} {copy_read_dir} {copy_write_dir} {copy_bytes}",
+        f"python3 bench.py --traffic-report {read_dir} {write_dir} {copy_read_dir} {copy_write_dir} {copy_bytes}"
+        + (f" {stats_csv}" if stats_csv else ""),
         "```",
         "",
         "Bytes are the L2's requests to the memory fabric, by request size: reads 32 B x RDREQ_32B + 64 B x "
@@ -151,11 +168,23 @@ def traffic_report(read_dir, write_dir, copy_read_dir, copy_write_dir, copy_byte
         f"Calibration: a device copy of {copy_bytes} bytes reads {copy_r:.0f} and writes {copy_w:.0f} bytes by "
         f"these counters (sized read requests {sized:.0f} of {cr[ck[0]].get('TCC_EA0_RDREQ', 0):.0f} total).",
         "",
-        "| kernel class | read bytes/launch | write bytes/launch | total bytes/launch |",
-        "|---|---|---|---|",
     ]
+    avg = _stats_avg_s(stats_csv) if stats_csv else None
+    if avg is not None:
+        lines += [f"Launch times: mean durations from `{stats_csv}` (a rocprofv3 --kernel-trace --stats run of the "
+                  "same workload); GB/s = total bytes per launch / mean launch time.", ""]
+        lines += ["| kernel class | read bytes/launch | write bytes/launch | total bytes/launch | avg us | GB/s |",
+                  "|---|---|---|---|---|---|"]
+    else:
+        lines += ["| kernel class | read bytes/launch | write bytes/launch | total bytes/launch |", "|---|---|---|---|"]
     for cls, r, w in rows:
-        lines.append(f"| {cls} | {r:.0f} | {w:.0f} | {r + w:.0f} |")
+        if avg is not None and cls in avg:
+            lines.append(f"| {cls} | {r:.0f} | {w:.0f} | {r + w:.0f} | {avg[cls] * 1e6:.1f} | "
+                         f"{(r + w) / avg[cls] / 1e9:.0f} |")
+        elif avg is not None:
+            lines.append(f"| {cls} | {r:.0f} | {w:.0f} | {r + w:.0f} | | |")
+        else:
+            lines.append(f"| {cls} | {r:.0f} | {w:.0f} | {r + w:.0f} |")
     lines += ["", f"kernel sources sha256: {kernel_source_hash()}", ""]
     return "\n".join(lines)
 
@@ -260,7 +289,7 @@ def measured_traffic(kernel_class):
         return None
     for line in text.splitlines():
         cells = [c.strip() for c in line.strip().strip("|").split("|")]
-        if len(cells) == 4 and cells[0] == kernel_class:
+        if len(cells) >= 4 and cells[0] == kernel_class:
             try:
                 return float(cells[3])
             except ValueError:
@@ -639,17 +668,20 @@ def main():
                          "one JSON line each, no CPU baseline")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run one plain device copy of BYTES (HBM counter calibration) and exit")
-    ap.add_argument("--traffic-report", nargs=5, metavar=("READ_DIR", "WRITE_DIR", "COPY_READ_DIR",
-                                                          "COPY_WRITE_DIR", "COPY_BYTES"),
-                    help="print the L2-to-fabric traffic markdown summary from rocprofv3 counter runs and exit")
+    ap.add_argument("--traffic-report", nargs="+", metavar="ARG",
+                    help="READ_DIR WRITE_DIR COPY_READ_DIR COPY_WRITE_DIR COPY_BYTES [KERNEL_STATS_CSV]: print the "
+                         "L2-to-fabric traffic markdown summary from rocprofv3 counter runs and exit")
     ap.add_argument("--stats-report", nargs=3, metavar=("KERNEL_STATS_CSV", "TITLE", "COMMAND"),
                     help="print a rocprofv3 --stats kernel summary as markdown and exit")
     ap.add_argument("--mfma-report", metavar="PMC_DIR",
                     help="print the MFMA work and utilisation of a rocprofv3 --pmc run of MFMA_COUNTERS and exit")
     args = ap.parse_args()
     if args.traffic_report:
-        fd, wd, cfd, cwd, nb = args.traffic_report
-        print(traffic_report(fd, wd, cfd, cwd, int(nb)))
+        if len(args.traffic_report) not in (5, 6):
+            ap.error("--traffic-report takes 5 or 6 arguments")
+        fd, wd, cfd, cwd, nb = args.traffic_report[:5]
+        stats = args.traffic_report[5] if len(args.traffic_report) == 6 else None
+        print(traffic_report(fd, wd, cfd, cwd, int(nb), stats))
         return
     if args.stats_report:
         print(stats_report(*args.stats_report), end="")

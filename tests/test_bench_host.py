@@ -100,6 +100,16 @@ def test_traffic_report_sizes_requests_and_averages_dispatches(tmp_path):
     assert f"| dXtilde | {read:.0f} | {write:.0f} | {read + write:.0f} |" in rep
     assert "reads 1024 and writes 1024 bytes" in rep
     assert f"kernel sources sha256: {bench.kernel_source_hash()}" in rep
+    # with a kernel summary: mean launch time of the class and bytes per second
+    stats = tmp_path / "kernel_stats.csv"
+    with open(stats, "w", newline="") as fh:
+        w = csv.writer(fh)
+        w.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs"])
+        w.writerow([gemm, 4, 2000, 500, 100.0, 400, 600])
+    rep = bench.traffic_report(str(tmp_path / "rd"), str(tmp_path / "wr"), str(tmp_path / "crd"),
+                               str(tmp_path / "cwr"), 1024, str(stats))
+    total = read + write
+    assert f"| dXtilde | {read:.0f} | {write:.0f} | {total:.0f} | 0.5 | {total / 500e-9 / 1e9:.0f} |" in rep
 
 
 def test_stats_report_orders_by_total_time(tmp_path):
