@@ -89,16 +89,30 @@ __device__ __forceinline__ void wait_vm_barrier() {
 __device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // BM x BN tile, WM x WN waves (each BM/WM x BN/WN), STAGES LDS buffers of BK
-// k, OCC workgroups per CU.
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_ = kBK, int OCC_ = 1>
+// k, OCC workgroups per CU.  SPLIT: the M side gets one buffer more than the N
+// side (STAGES = 2: three M buffers, two N buffers), so its rows are requested
+// two steps ahead while the N side (weights, mostly L2 hits) stays one step
+// ahead.  Buffer order A0 A1 B0 A2 B1: the last STAGE_BYTES (A2, B1) are the
+// ones idle during an epilogue, as the last stage is in the plain layout.
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int BK_ = kBK, int OCC_ = 1, bool SPLIT_ = false>
 struct GemmCfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, BK = BK_, OCC = OCC_;
+  static constexpr bool SPLIT = SPLIT_;
   static constexpr int NW = WM * WN, THREADS = NW * 64;
   static constexpr int RM = BM / WM / 32, RN = BN / WN / 32;
   static constexpr int SUB = BK / 16;  // MFMA k steps per stage
   static constexpr int M_BYTES = BM * BK * 2, N_BYTES = BN * BK * 2;
   static constexpr int STAGE_BYTES = M_BYTES + N_BYTES;
-  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES;
+  static constexpr int A_STAGES = STAGES + (SPLIT ? 1 : 0);
+  static constexpr int LDS_BYTES = A_STAGES * M_BYTES + STAGES * N_BYTES;
+  static_assert(!SPLIT || STAGES == 2, "the split ring is three M buffers and two N buffers");
+  // byte offsets of M buffer st (st < A_STAGES) and N buffer st (st < STAGES)
+  static constexpr int a_off(int st) {
+    return SPLIT ? (st < 2 ? st * M_BYTES : 2 * M_BYTES + N_BYTES) : st * STAGE_BYTES;
+  }
+  static constexpr int b_off(int st) {
+    return SPLIT ? (st == 0 ? 2 * M_BYTES : 3 * M_BYTES + N_BYTES) : st * STAGE_BYTES + M_BYTES;
+  }
   static constexpr int QM = BM * BK / (NW * 512), QN = BN * BK / (NW * 512);  // DMA instructions per wave per stage
   static_assert(BK == 32 || BK == 64, "stage depth");
   static_assert(STAGES >= 2 && STAGES <= 4, "stages");
@@ -428,18 +442,30 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   constexpr int BM = Cfg::BM, BN = Cfg::BN, S = Cfg::STAGES, BK = Cfg::BK, SUB = Cfg::SUB;
   constexpr int kEpiBytes = (Op::EPI_LDS > 0 ? (Op::EPI_LDS + 255) / 256 * 256 : 256);
   constexpr int kIdxLds = IdxLds<Op>::value;
-  static_assert(Cfg::LDS_BYTES + kEpiBytes + kIdxLds <= 160 * 1024, "LDS");
-  __shared__ __attribute__((aligned(1024))) char smem[Cfg::LDS_BYTES + kEpiBytes + kIdxLds];
-  __shared__ int sh[16];  // [0..3], [4..7]: tile lookups of even / odd k; [8..9]: tile counts
+  // The split ring fills all 160 KB with stage buffers: no epilogue area (the
+  // epilogue stages its stores in the idle A2 and B1 buffers), no index area
+  // and no shared tile-lookup words (its ops' count() and tile() read the
+  // m-tile list directly and get a null pointer).
+  constexpr bool kSplit = Cfg::SPLIT;
+  // (its ops gather nothing: row-major M side, N side without k-row indices)
+  static_assert(!kSplit || (Op::M_MODE == ROWS && kIdxLds == 0 && Op::EPI_LDS == 0), "split-ring ops");
+  constexpr int kSmem = kSplit ? Cfg::LDS_BYTES : Cfg::LDS_BYTES + kEpiBytes + kIdxLds;
+  static_assert(kSmem <= 160 * 1024, "LDS");
+  __shared__ __attribute__((aligned(1024))) char smem[kSmem];
+  int* sh = nullptr;  // [0..3], [4..7]: tile lookups of even / odd k; [8..9]: tile counts
+  if constexpr (!kSplit) {
+    __shared__ int sh_words[16];
+    sh = sh_words;
+  }
   Sched sched;
   if constexpr (HasXcdRange<Op>::value) {
     int b, c;
     Op::xcd_range(p, blockIdx.x & 7, &b, &c);
     sched.init_range(b, c);
   } else {
-    const int ntiles = Op::count(p, sh + 8);
+    const int ntiles = Op::count(p, kSplit ? nullptr : sh + 8);
     int tail = 0;
-    if constexpr (HasCountTail<Op>::value) tail = Op::count_tail(p, sh + 8);
+    if constexpr (HasCountTail<Op>::value) tail = Op::count_tail(p, kSplit ? nullptr : sh + 8);
     sched.init(ntiles, tail);
   }
   const int id = sched.id(0);
@@ -486,6 +512,15 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
   // stages 0 .. S-2 of a tile, and the row indices of stage S-1 (gathered k)
   auto prologue = [&](const TileInfo& t, MSide& a, NSide& b) {
     const int nk = (t.k_len + BK - 1) / BK;
+    if constexpr (kSplit) {
+      // A0, B0, A1 (in this order: the waits count on it)
+      if (nk > 0) {
+        a.issue(lds0 + Cfg::a_off(0), 0);
+        b.issue(lds0 + Cfg::b_off(0), 0);
+      }
+      if (nk > 1) a.issue(lds0 + Cfg::a_off(1), BK);
+      return;
+    }
 #pragma unroll
     for (int st = 0; st < S - 1; ++st) {
       if (st < nk) {
@@ -516,7 +551,7 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
     // next tile: lookup and side setup overlap this tile's first DMA
     int idn = sched.id(k + 1);
     TileInfo tn;
-    if (idn >= 0 && !Op::tile(p, idn, tn, sh + 4 * ((k + 1) & 1))) idn = -1;
+    if (idn >= 0 && !Op::tile(p, idn, tn, kSplit ? nullptr : sh + 4 * ((k + 1) & 1))) idn = -1;
     // Sides that gather rows by index DMA set up here, so those loads overlap
     // this tile's k loop; the weight-gradient sides (plain arithmetic) set up
     // after it, so their registers are free during the k loop.
@@ -534,7 +569,73 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
     bool gathered = false;
     if constexpr (Op::M_MODE == KOUTER) gathered = gathered || ms.gidx != nullptr;
     if constexpr (Op::N_MODE == KOUTER) gathered = gathered || ns.gidx != nullptr;
-    if constexpr (kMidBarrier) {
+    if constexpr (kSplit) {
+      // Split ring: step kt reads A(kt) from M buffer kt % 3 and B(kt) from N
+      // buffer kt % 2, and requests B(kt+1) and then A(kt+2) (interleaved with
+      // its MFMAs, B first).  At the top of step kt the only requests younger
+      // than B(kt) are A(kt+1)'s QM (from the prologue or step kt-1) and, at
+      // kt = 0, the previous epilogue's stores; the barrier after the wait
+      // also certifies that step kt-1's buffers, which this step refills, are
+      // no longer read.
+      constexpr int QM = Cfg::QM, QN = Cfg::QN;
+      constexpr int kEpi = EpiStores<Op>::value;
+      static_assert(QM + kEpi <= 63, "vmcnt range");
+      for (int kt = 0; kt < nk; ++kt) {
+        const bool a_ahead = kt + 1 < nk;  // A(kt+1) was requested after B(kt)
+        if (kt == 0 && prev_full) {
+          if (a_ahead)
+            wait_vm_barrier<QM + kEpi>();
+          else
+            wait_vm_barrier<kEpi>();
+        } else if (kt == 0) {
+          wait_vm_barrier<0>();  // a partial tile's store count is not known
+        } else if (a_ahead) {
+          wait_vm_barrier<QM>();
+        } else {
+          wait_vm_barrier<0>();
+        }
+        const int kb = kt + 1, ka = kt + 2;
+        const bool issue_b = kb < nk, issue_a = ka < nk;
+        const uint32_t bdst = lds0 + Cfg::b_off(kb & 1), adst = lds0 + Cfg::a_off(ka % 3);
+        const char* lm = smem + Cfg::a_off(kt % 3);
+        const char* ln = smem + Cfg::b_off(kt & 1);
+        auto issue_one = [&](int d) {
+          if (d < QN) {
+            if (issue_b) ns.issue(bdst, kb * BK, d, QN);
+          } else if (issue_a) {
+            ms.issue(adst, ka * BK, d - QN, QM);
+          }
+        };
+        if (active) {
+          bf16x8 fm[Cfg::RM], fn[Cfg::RN];
+#pragma unroll
+          for (int i = 0; i < Cfg::RM; ++i) fm[i] = MSide::frag(lm, wm0 + 32 * i, 0);
+#pragma unroll
+          for (int j = 0; j < Cfg::RN; ++j) fn[j] = NSide::frag(ln, wn0 + 32 * j, 0);
+#pragma unroll
+          for (int s = 0; s < SUB; ++s)
+#pragma unroll
+            for (int i = 0; i < Cfg::RM; ++i)
+#pragma unroll
+              for (int j = 0; j < Cfg::RN; ++j) {
+                const int c = (s * Cfg::RM + i) * Cfg::RN + j;
+                if (c % kDmaStride == 0 && c / kDmaStride < kPerStage) {
+                  __builtin_amdgcn_sched_barrier(0);
+                  issue_one(c / kDmaStride);
+                  __builtin_amdgcn_sched_barrier(0);
+                }
+                acc.acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fn[j], fm[i], acc.acc[i][j], 0, 0, 0);
+                if (s + 1 < SUB) {
+                  if (j == Cfg::RN - 1) fm[i] = MSide::frag(lm, wm0 + 32 * i, s + 1);
+                  if (i == Cfg::RM - 1) fn[j] = NSide::frag(ln, wn0 + 32 * j, s + 1);
+                }
+              }
+        } else {
+          if (issue_b) ns.issue(bdst, kb * BK);
+          if (issue_a) ms.issue(adst, ka * BK);
+        }
+      }
+    } else if constexpr (kMidBarrier) {
       // Two stages, one barrier per step, placed before the last sub-step.
       // By then every wave holds that sub-step's fragments in registers and
       // has waited for its share of stage kt+1, so the barrier certifies both

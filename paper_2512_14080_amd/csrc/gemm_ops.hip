@@ -720,10 +720,13 @@ struct OpRouterTopk {
 constexpr int kStageBytesPerWave = 16 * 128;
 template <class Cfg>
 constexpr bool kStagedStores = Cfg::RN % 2 == 0 && Cfg::LDS_BYTES + Cfg::NW * kStageBytesPerWave + 256 <= 160 * 1024;
-// store instructions per wave of store_rows_bf16 on a full tile: staged, four
-// per 64-column row block (two rounds of two); direct, two per 32 columns
+// store instructions per wave of store_rows_bf16_any on a full tile: staged
+// (through the idle last stage or the epilogue area), four per 64-column row
+// block; direct, two per 32 columns
 template <class Cfg>
-constexpr int kStoresPerFullTile = kStagedStores<Cfg> ? Cfg::RM * (Cfg::RN / 2) * 4 : Cfg::RM * Cfg::RN * 2;
+constexpr int kStoresPerFullTile =
+    Cfg::RN % 2 == 0 && (Cfg::STAGE_BYTES >= Cfg::NW * 4096 || kStagedStores<Cfg>) ? Cfg::RM * (Cfg::RN / 2) * 4
+                                                                                   : Cfg::RM * Cfg::RN * 2;
 // Epilogue address arithmetic uses the lane index from a volatile asm, so
 // it stays in the epilogue instead of being hoisted out of the tile loop.
 __device__ __forceinline__ int epilogue_lane() { return volatile_lane(); }
@@ -1490,6 +1493,9 @@ static int mtiles_bound(int capacity, int E, int BM) { return capacity / BM + E;
 // tile configurations <BM, BN, WM, WN, STAGES>; varlen-M GEMMs use BM = 256
 using C256x256 = GemmCfg<256, 256, 2, 4, 2>;
 using C256x256w = GemmCfg<256, 256, 4, 2, 2>;  // 64 x 128 per wave (up, dH, dX~: measured faster)
+// the split ring (M rows two steps ahead) for the GEMMs that gather nothing
+using C256x256s = GemmCfg<256, 256, 2, 4, 2, kBK, 1, true>;
+using C256x256ws = GemmCfg<256, 256, 4, 2, 2, kBK, 1, true>;
 using C256x128 = GemmCfg<256, 128, 4, 2, 3>;
 using C256x64 = GemmCfg<256, 64, 8, 1, 3>;
 using C128x256 = GemmCfg<128, 256, 2, 4, 3>;
@@ -1529,7 +1535,7 @@ hipError_t launch_up(const UpArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_down(const DownArgs& a, hipStream_t s) {
-  if (a.d % 256 == 0) return run<OpDown<C256x256>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
+  if (a.d % 256 == 0) return run<OpDown<C256x256s>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
   return run<OpDown<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 128)), s);
 }
 
@@ -1560,7 +1566,7 @@ hipError_t launch_dh(const DHArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_dxt(const DXtArgs& a, hipStream_t s) {
-  if (a.d % 256 == 0) return run<OpDXt<C256x256w>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
+  if (a.d % 256 == 0) return run<OpDXt<C256x256ws>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 256)), s);
   return run<OpDXt<C256x128>>({a}, pad8(mtiles_bound(a.capacity, a.E, 256) * (a.d / 128)), s);
 }
 
