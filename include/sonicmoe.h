@@ -159,7 +159,7 @@ enum {
  * r->capacity must be >= T*K.  On success r->state is MOE_ROUTING_STATE_BUILT
  * (MOE_ROUTING_STATE_COUNTS with MOE_ROUTE_COUNTS_ONLY) and the device word
  * r->status is cleared by the metadata kernels.
- * With E <= 128 and K <= 8 the softmax and top-K run in the
+ * With E <= 256 and K <= 8 the softmax and top-K run in the
  * router GEMM's epilogue (one launch; the logits are written only with
  * MOE_ROUTE_WRITE_LOGITS).  Its scores may differ from the two-launch path's
  * in the last bits (the order of the softmax sum); selection, mask and weights

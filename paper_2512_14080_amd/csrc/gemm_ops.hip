@@ -532,7 +532,7 @@ struct OpRouterTopk {
   using Cfg = Cfg_;
   static constexpr int M_MODE = ROWS, N_MODE = KOUTER;
   static constexpr int BM = Cfg::BM, BN = Cfg::BN, WN = Cfg::WN, NV = Cfg::RN * 16;
-  static_assert(Cfg::RM == 1, "one 32-row block per wave");
+  static_assert(Cfg::RM <= 2, "one or two 32-row blocks per wave");
   static_assert(NV % KM == 0, "pairs per lane in groups of KM");
   // LDS: row maxima, row sums [WN][BM] f32; top lists [WN][KM][BM] u64;
   // membership pieces [BM / 32][BN] u32
@@ -554,13 +554,15 @@ struct OpRouterTopk {
     const uint32_t lo = __shfl_xor((uint32_t)v, 32, kWave), hi = __shfl_xor((uint32_t)(v >> 32), 32, kWave);
     return ((uint64_t)hi << 32) | lo;
   }
-  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* lds) {
+  // row block I of the wave (rows 32 I .. 32 I + 31 of its BM / WM)
+  template <int I>
+  static __device__ void row_block(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* lds) {
     const RouterTopkArgs& a = p.a;
     // lane-dependent coordinates from an opaque lane read: computed here, not
     // hoisted out of the tile loop as constants that stay live through it
     const int lane = volatile_lane(), wave = threadIdx.x >> 6;
     const int wn = Cfg::wave_n(wave), wm = Cfg::wave_m(wave), h = lane >> 5, u = lane & 31;
-    const int m = wm * 32 + u;
+    const int m = wm * (BM / Cfg::WM) + 32 * I + u;
     // column of value 4 (4 j + g) + q: the MFMA output layout (Acc::n_of)
     const int c0 = wn * (BN / WN) + 4 * h;
     auto col_of = [&](int k) { return c0 + 32 * (k >> 4) + 8 * ((k >> 2) & 3) + (k & 3); };
@@ -580,7 +582,7 @@ struct OpRouterTopk {
       f32x4 x;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        x[q] = t.acc[0][k0 >> 4][(k0 & 15) + q];
+        x[q] = t.acc[I][k0 >> 4][(k0 & 15) + q];
         if (a.bias) x[q] += col_ok(k0) ? a.bias[col + q] : 0.f;
         v[k0 + q] = col_ok(k0) ? x[q] : -INFINITY;
         mx = fmaxf(mx, v[k0 + q]);
@@ -665,24 +667,23 @@ struct OpRouterTopk {
       if (k == a.K - 1) thr = top[k];
     // membership: ballot k holds rows 0..31 of the wave for column col_of(k)
     // of the lanes below 32 (low half) and of the lanes above (high half);
-    // lane u + 32 h keeps half h of ballot u, i.e. its own column col_of(u)
-    uint32_t mine = 0;
+    // lane u + 32 h keeps half h of ballots u, u + 32, ..., i.e. its own
+    // columns col_of(u), col_of(u + 32), ...
+    constexpr int kMine = (NV + 31) / 32;  // ballots kept per lane
+    uint32_t mine[kMine];
+#pragma unroll
+    for (int r = 0; r < kMine; ++r) mine[r] = 0;
 #pragma unroll
     for (int k = 0; k < NV; ++k) asm volatile("" : "+v"(v[k]));  // recompute the pairs, do not keep them
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
       const uint64_t pk = pair(k);
       const uint64_t b = __ballot(pk != 0ull && pk >= thr);
-      mine = u == k ? (uint32_t)(b >> (32 * h)) : mine;
+      mine[k >> 5] = u == (k & 31) ? (uint32_t)(b >> (32 * h)) : mine[k >> 5];
     }
-    if (u < NV) bits[wm * BN + col_of(u)] = mine;
-    barrier_lds();
-    const int w0 = ti.row_base / 64;
-    for (int i = threadIdx.x; i < (BM / 64) * a.E; i += Cfg::THREADS) {
-      const int e = i / (BM / 64), ww = i % (BM / 64);
-      if (w0 + ww < a.W)
-        a.mask[(size_t)e * a.W + w0 + ww] = bits[2 * ww * BN + e] | ((uint64_t)bits[(2 * ww + 1) * BN + e] << 32);
-    }
+#pragma unroll
+    for (int r = 0; r < kMine; ++r)
+      if (32 * r + u < NV) bits[(wm * Cfg::RM + I) * BN + col_of(32 * r + u)] = mine[r];
     if (live && wn == 0 && h == 0) {
       // the selected scores in ascending expert order: (expert, score) halves
       // swapped, so the descending sort puts the lowest expert first
@@ -700,6 +701,20 @@ struct OpRouterTopk {
           a.topk_idx[row * a.K + k] = (int32_t)~(uint32_t)top[k];
           a.topk_w[row * a.K + k] = topk_value((uint32_t)(top[k] >> 32)) / den;
         }
+    }
+  }
+  static __device__ void epilogue(const Params& p, const TileInfo& ti, Acc<Cfg>& t, char* lds) {
+    row_block<0>(p, ti, t, lds);
+    if constexpr (Cfg::RM > 1) row_block<1>(p, ti, t, lds);
+    // the membership words: 64 tile rows (two 32-row pieces) per word
+    const RouterTopkArgs& a = p.a;
+    const uint32_t* bits = (const uint32_t*)(lds + kBitsOff);
+    barrier_lds();
+    const int w0 = ti.row_base / 64;
+    for (int i = threadIdx.x; i < (BM / 64) * a.E; i += Cfg::THREADS) {
+      const int e = i / (BM / 64), ww = i % (BM / 64);
+      if (w0 + ww < a.W)
+        a.mask[(size_t)e * a.W + w0 + ww] = bits[2 * ww * BN + e] | ((uint64_t)bits[(2 * ww + 1) * BN + e] << 32);
     }
   }
 };
@@ -1517,7 +1532,12 @@ hipError_t launch_router_gemm(const RouterGemmArgs& a, hipStream_t s) {
   return run<OpRouter<C256x256>>({a}, mt * ((a.E + 255) / 256), s);
 }
 
-bool router_topk_fusable(int E, int K) { return E % 8 == 0 && E <= 128 && K <= 8; }
+bool router_topk_fusable(int E, int K) { return E % 8 == 0 && E <= 256 && K <= 8; }
+
+// 128 x 256 tiles for E in (128, 256]: 64 rows x 64 columns per wave (two
+// row blocks of 32 values per lane, handled one after the other), two stages
+// (the epilogue's LDS does not fit a third)
+using C128x256r = GemmCfg<128, 256, 2, 4, 2>;
 
 hipError_t launch_router_topk(const RouterTopkArgs& a, hipStream_t s) {
   if (!router_topk_fusable(a.E, a.K)) return hipErrorInvalidValue;
@@ -1525,7 +1545,9 @@ hipError_t launch_router_topk(const RouterTopkArgs& a, hipStream_t s) {
   if (a.E == 64) return run<OpRouterTopk<C128x64, 8, true>>({a}, tiles, s);
   if (a.E < 64) return run<OpRouterTopk<C128x64, 8, false>>({a}, tiles, s);
   if (a.E == 128) return run<OpRouterTopk<C128x128, 8, true>>({a}, tiles, s);
-  return run<OpRouterTopk<C128x128, 8, false>>({a}, tiles, s);
+  if (a.E < 128) return run<OpRouterTopk<C128x128, 8, false>>({a}, tiles, s);
+  if (a.E == 256) return run<OpRouterTopk<C128x256r, 8, true>>({a}, tiles, s);
+  return run<OpRouterTopk<C128x256r, 8, false>>({a}, tiles, s);
 }
 
 hipError_t launch_up(const UpArgs& a, hipStream_t s) {

@@ -1,5 +1,5 @@
 """The router GEMM with softmax and top-K fused into its epilogue (E a multiple
-of 8, E <= 128, K <= 8), against the two-launch path and the oracle.
+of 8, E <= 256, K <= 8), against the two-launch path and the oracle.
 
 Three routings of the same inputs, through the C ABI:
   fused     moe_route (the default where the shapes fuse);
@@ -93,6 +93,8 @@ def check(cfg, seed, T=None, bias=None):
     (W.MoEConfig("e8k1", T=130, d=128, n=64, E=8, K=1, m_tile=16), None),
     (W.MoEConfig("e128t1", T=1, d=128, n=64, E=128, K=8, m_tile=128), None),
     (W.MoEConfig("e104k5", T=250, d=256, n=64, E=104, K=5, m_tile=16), None),  # 24 idle columns
+    (W.MoEConfig("e256", T=1000, d=256, n=64, E=256, K=8, m_tile=128), None),   # 128 x 256 tiles, two row blocks
+    (W.MoEConfig("e200k6", T=700, d=128, n=64, E=200, K=6, m_tile=64), None),  # 56 idle columns
 ])
 def test_fused_router_topk(cfg, T):
     check(cfg, seed=31, T=T)
@@ -149,3 +151,9 @@ def test_fused_router_topk_nonfinite_logits():
     assert ok.sum() >= cfg.T - 5
     L = oracle.router_logits(inp.f32("X")[ok], inp.f32("Wr"), inp.bias, np.float32)
     assert rel_err(f["logits"][ok], L) <= 1e-4
+
+
+def test_fused_router_topk_sparse_full_size():
+    """The high-sparsity routing shape (T=32768, d=2048, E=256, K=8, Zipf-skewed
+    router bias): 128 x 256 tiles."""
+    check(W.CONFIGS["sparse"], seed=0)
