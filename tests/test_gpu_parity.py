@@ -193,6 +193,15 @@ def test_weight_gradients_short_k_loops():
     assert steps == [0, 1, 2, 3, 4], (R.counts, steps)
 
 
+def test_split_ring_short_k_loops():
+    """d a multiple of 256 with n = 64: the down projection (k = n = 64) and
+    dX~ (k = 2n = 128) run one- and two-step k loops on the split LDS ring
+    (A rows two steps ahead), with token choice and with rounding."""
+    cfg = W.MoEConfig("ring", T=600, d=256, n=64, E=8, K=2, m_tile=64)
+    check_layer(cfg, seed=22)
+    check_layer(cfg, seed=23, round_mode="nearest")
+
+
 def test_single_token_and_one_hot_expert():
     check_layer(TINY, seed=5, T=1)
     check_layer(TINY, seed=6, T=65, round_mode="nearest")
