@@ -574,9 +574,11 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
       // buffer kt % 2, and requests B(kt+1) and then A(kt+2) (interleaved with
       // its MFMAs, B first).  At the top of step kt the only requests younger
       // than B(kt) are A(kt+1)'s QM (from the prologue or step kt-1) and, at
-      // kt = 0, the previous epilogue's stores; the barrier after the wait
-      // also certifies that step kt-1's buffers, which this step refills, are
-      // no longer read.
+      // kt = 0, the previous epilogue's stores.  Leaving QM outstanding is
+      // therefore always enough (whatever the youngest QM are, B(kt) is
+      // older), and after a full tile QM plus its exact store count is.  The
+      // barrier after the wait also certifies that step kt-1's buffers, which
+      // this step refills, are no longer read.
       constexpr int QM = Cfg::QM, QN = Cfg::QN;
       constexpr int kEpi = EpiStores<Op>::value;
       static_assert(QM + kEpi <= 63, "vmcnt range");
@@ -587,12 +589,10 @@ __global__ __launch_bounds__(Op::Cfg::THREADS, Op::Cfg::OCC) void grouped_gemm_k
             wait_vm_barrier<QM + kEpi>();
           else
             wait_vm_barrier<kEpi>();
-        } else if (kt == 0) {
-          wait_vm_barrier<0>();  // a partial tile's store count is not known
         } else if (a_ahead) {
           wait_vm_barrier<QM>();
         } else {
-          wait_vm_barrier<0>();
+          wait_vm_barrier<0>();  // (at kt = 0 after a partial tile: its store count is not known)
         }
         const int kb = kt + 1, ka = kt + 2;
         const bool issue_b = kb < nk, issue_a = ka < nk;
