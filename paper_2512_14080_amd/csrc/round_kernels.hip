@@ -379,6 +379,18 @@ __global__ __launch_bounds__(256) void tr_merge_kernel(const uint64_t* __restric
   const uint64_t* src = tc_mask + (size_t)e * W;
   uint64_t* dst = tr_mask + (size_t)e * W;
   const bool select = dir != 0 && need != 0;
+  // the first pass's row words are requested before the selection, so that
+  // their loads overlap it (wave 0's otherwise wait until it has selected)
+  constexpr int kPre = kTrRowWords / 256;
+  uint64_t pre[kPre];
+  {
+    const int nw0 = min(kTrRowWords, W);
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+      const int w = threadIdx.x + 256 * i;
+      pre[i] = w < nw0 ? src[w] : 0ull;
+    }
+  }
   uint32_t sel[G];
   int tok[G][32];
   if (select && wave == 0) {
@@ -401,7 +413,13 @@ __global__ __launch_bounds__(256) void tr_merge_kernel(const uint64_t* __restric
   int carry = 0;
   for (int w0 = 0; w0 < W; w0 += kTrRowWords) {
     const int nw = min(kTrRowWords, W - w0);
-    for (int w = threadIdx.x; w < nw; w += 256) row[w] = src[w0 + w];
+    if (w0 == 0) {
+#pragma unroll
+      for (int i = 0; i < kPre; ++i)
+        if (threadIdx.x + 256 * i < nw) row[threadIdx.x + 256 * i] = pre[i];
+    } else {
+      for (int w = threadIdx.x; w < nw; w += 256) row[w] = src[w0 + w];
+    }
     __syncthreads();
     if (select && wave == 0) {
 #pragma unroll
