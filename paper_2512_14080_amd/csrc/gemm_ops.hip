@@ -524,6 +524,8 @@ struct OpRouter {
 //   5. the weights: the K selected scores summed in ascending expert order
 //      (the order the separate top-K kernel uses, so the two agree bit for bit
 //      on the same scores), then score / sum.
+// A wave with two 32-row blocks (128 x 256 tiles) runs steps 1-5 for each
+// block in turn; the membership words go out once both are parked.
 // The results match launch_topk_route on these scores exactly; the scores
 // themselves differ from its own softmax of the same logits only in the
 // rounding of the sum.
