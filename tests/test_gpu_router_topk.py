@@ -122,6 +122,13 @@ def test_fused_router_topk_7b_full_size():
     check(W.CONFIGS["7b"], seed=0)
 
 
+@pytest.mark.parametrize("name", ["1b", "coarse"])
+def test_fused_router_topk_other_full_sizes(name):
+    """The 1B (E=64, K=8: 128 x 64 tiles, every column an expert) and coarse
+    (d=4096, E=8, K=2: 56 idle columns of a 128 x 64 tile) routing shapes."""
+    check(W.CONFIGS[name], seed=0)
+
+
 def test_fused_router_topk_nonfinite_logits():
     """X rows holding NaN, +-Inf or values whose logits overflow give NaN and
     infinite logits.  Every token still gets K distinct experts in [0, E)
