@@ -29,6 +29,25 @@ def test_exports_every_declared_symbol():
     assert set(B.EXPORTS) == set(names)
 
 
+def test_binding_constants_match_the_header():
+    """Every enumerator the header gives an explicit value (flags, states,
+    modes, error codes, kernel classes by position) has the same value in
+    the ctypes binding, where the binding defines it."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    explicit = {n: int(v) for n, v in re.findall(r"\b(MOE_[A-Z0-9_]+)\s*=\s*(-?\d+)", text)}
+    assert "MOE_ROUTE_SEPARATE_TOPK" in explicit
+    checked = 0
+    for name, value in explicit.items():
+        if hasattr(B, name):
+            assert getattr(B, name) == value, name
+            checked += 1
+    assert checked >= 10
+    # kernel classes: the enum's order is the binding's list order
+    kc = re.search(r"enum\s*\{\s*(MOE_KC_ROUTER_GEMM[^}]*)\}", text).group(1)
+    names = [n for n in re.findall(r"\b(MOE_KC_[A-Z0-9_]+)", kc) if n != "MOE_KC_COUNT"]
+    assert len(names) == len(B.KERNEL_CLASSES)
+
+
 def test_strerror_and_class_names():
     assert B.moe_strerror(0) == "success"
     assert "capacity" in B.moe_strerror(B.MOE_ERR_CAPACITY)
@@ -101,6 +120,10 @@ def test_route_validation_before_any_launch():
     r_nl.logits = None
     assert L.moe_route(D, 0x1000, 0x2000, None, B.MOE_ROUTE_WRITE_LOGITS, ctypes.byref(r_nl), None) == B.MOE_ERR_INVALID_ARG
     assert L.moe_route(D, 0x1000, 0x2000, None, 64, ctypes.byref(r), None) == B.MOE_ERR_INVALID_ARG
+    # the highest defined flag is MOE_ROUTE_SEPARATE_TOPK (16): the next bit is unknown
+    assert B.MOE_ROUTE_SEPARATE_TOPK == 16
+    assert L.moe_route(D, 0x1000, 0x2000, None, 32, ctypes.byref(r), None) == B.MOE_ERR_INVALID_ARG
+    assert "flags" in B.moe_last_error()
 
 
 def test_round_validation():
