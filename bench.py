@@ -691,7 +691,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the layer is built and measured on a "
-              f"single MI355X; multi-GPU sharding is a design note, not part of this build.", file=sys.stderr)
+              f"single MI355X; how the layer would shard over GPUs is described, not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch
